@@ -1,0 +1,299 @@
+/*
+ * mdnn.h -- C ABI of the MI355X (gfx950) hot path of a MagmaDNN-style
+ * minibatch SGD step: mixed-precision dense contractions (fully connected
+ * GEMMs and implicit-GEMM 2-D convolutions in forward, backward-data and
+ * backward-weight form), their fused epilogues, loss, optimizer and
+ * precision-conversion kernels.
+ *
+ * Paper: Archibald et al., "Integrating Deep Learning in Domain Sciences at
+ * Exascale".  The operations follow its statement of the problem:
+ *   - tensors, a compute graph of ops and backpropagation (section 2.1);
+ *   - memory handling hidden from the model code (section 2.1, MemoryManager):
+ *     here every buffer is owned by the caller;
+ *   - convolution algorithms are swappable (section 2.1): convolution has its
+ *     own entry points, separate from the GEMM;
+ *   - the mixed-precision multiply-accumulate D = C + A*B with fp16 (or bf16)
+ *     A, B and fp32 C, D (section 3.2);
+ *   - minibatch SGD (section 3.1).
+ *
+ * Conventions shared by every entry point
+ *   - All tensors are row-major.  Activations are [rows, features]; images are
+ *     NHWC; fully connected weights are W[in, out]; convolution filters are
+ *     [Cout][R][S][Cin] ("KRSC").  Convolutions have stride 1 and zero padding.
+ *   - Every pointer argument is a DEVICE pointer (memory the caller allocated,
+ *     e.g. through PyTorch) unless the comment says "host".  The library never
+ *     allocates, frees or retains device memory; the only library-owned memory
+ *     is the host-side net handle of the train-step API.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
+ *     only enqueues work on that stream and returns without synchronising.
+ *   - Every call validates its arguments on the host first and returns a
+ *     status; nothing aborts.  On a non-success status nothing was launched
+ *     (except MDNN_ERR_LAUNCH, which reports a failed launch), and
+ *     mdnn_last_error() returns a message naming the problem.
+ *   - Conditions that live in device data are data, not errors: a non-finite
+ *     gradient sets the loss scaler's overflow flag; a label outside [0, C)
+ *     makes that row's loss and gradient NaN.
+ *   - Low-precision stores round to nearest even, keep fp16 subnormals,
+ *     overflow to +-inf and keep NaN.
+ *   - Functions are reentrant; calls that overlap in time on different
+ *     streams must not write the same buffers.
+ */
+#ifndef MDNN_H
+#define MDNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MDNN_SUCCESS = 0,
+  MDNN_ERR_NULL = 1,        /* a required pointer is NULL                         */
+  MDNN_ERR_SHAPE = 2,       /* a size is negative / inconsistent / too large       */
+  MDNN_ERR_LAYOUT = 3,      /* unknown layout, leading dimension below the width   */
+  MDNN_ERR_DTYPE = 4,       /* unsupported combination of element types            */
+  MDNN_ERR_MISALIGNED = 5,  /* a base pointer is not aligned to its element size   */
+  MDNN_ERR_WORKSPACE = 6,   /* workspace missing or smaller than required          */
+  MDNN_ERR_LAUNCH = 7,      /* the HIP runtime reported an error                    */
+  MDNN_ERR_STATE = 8        /* net handle misuse (not bound, wrong kind of layer)   */
+} mdnn_status_t;
+
+typedef enum { MDNN_F32 = 0, MDNN_F16 = 1, MDNN_BF16 = 2 } mdnn_dtype_t;
+
+/* Operand storage of D = op(A) op(B), row-major:
+ *   NN: A[M,K], B[K,N]   -- forward           Y  = X  W
+ *   NT: A[M,K], B[N,K]   -- backward-data     dX = dY W^T
+ *   TN: A[K,M], B[K,N]   -- backward-weight   dW = X^T dY                       */
+typedef enum { MDNN_NN = 0, MDNN_NT = 1, MDNN_TN = 2 } mdnn_layout_t;
+
+typedef enum { MDNN_ACT_NONE = 0, MDNN_ACT_RELU = 1 } mdnn_act_t;
+
+typedef void* mdnn_stream_t; /* a hipStream_t */
+
+/* Message of the last non-success status returned on this host thread. */
+const char* mdnn_last_error(void);
+/* Library version string (static). */
+const char* mdnn_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Mixed-precision GEMM (section 3.2: D = C + A*B, low-precision A and B,
+ * fp32 accumulation), generalised to
+ *     D = epi(alpha * op(A) op(B) + beta * C)
+ *     epi(v) = mask( act( v + bias[n] ) )
+ *     mask(v) = (mask_src[m, n] > 0) ? v : 0        (if mask_src != NULL)
+ * computed in fp32 and rounded once to d_type.
+ *   ab_type: MDNN_F16 or MDNN_BF16 (MFMA path) or MDNN_F32 (fp32 path, then
+ *            d_type must be MDNN_F32).
+ *   d_type:  MDNN_F32 or ab_type.  C (read only if beta != 0) has d_type.
+ *   bias:    NULL or fp32[N].     mask_src: NULL or ab_type [M, ldm] -- the
+ *            stored output of the ReLU that produced the backward-data result
+ *            (a layer's input), applying the ReLU derivative [y > 0].
+ *   lda/ldb/ldc/ldd/ldm are in elements and must be >= the stored row width.
+ *   Any M, N, K >= 0 (M or N == 0: no-op; K == 0: D = epi(beta*C)).
+ * Deterministic: the same inputs give bitwise-identical D on every call.
+ * ------------------------------------------------------------------------- */
+mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
+                              float alpha, const void* A, int64_t lda, const void* B,
+                              int64_t ldb, mdnn_dtype_t ab_type, float beta, const void* C,
+                              int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
+                              const float* bias, mdnn_act_t act, const void* mask_src,
+                              int64_t ldm, mdnn_stream_t stream);
+
+/* Tuning knob for measurements (process-wide): force the MFMA tile shape of
+ * the GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128,
+ * 3 = 64x64.  Returns 0, or -1 for an unknown code.  Results do not depend on
+ * the tile shape except through the fp32 summation order of split-K. */
+int mdnn_set_gemm_tile(int code);
+
+/* ---------------------------------------------------------------------------
+ * 2-D convolution as implicit GEMM (section 2.1: a convolution is an
+ * interchangeable algorithm behind one operation).  Stride 1, zero padding
+ * `pad`, output Ho = h + 2*pad - r + 1, Wo = w + 2*pad - s + 1 (both >= 1).
+ *   x  [n, h, w, c_in]        w  [c_out, r, s, c_in]      y/dy [n, Ho, Wo, c_out]
+ *   fwd:        y[n,i,j,k]  = epi( sum_{r,s,c} x[n,i+r-p,j+s-p,c] * w[k,r,s,c] )
+ *   bwd_data:   dx[n,h,w,c] = mask( sum_{k,r,s} dy[n,h-r+p,w-s+p,k] * w[k,r,s,c] )
+ *   bwd_filter: dw[k,r,s,c] = sum_{n,i,j} dy[n,i,j,k] * x[n,i+r-p,j+s-p,c]
+ *               db[k]       = sum_{n,i,j} dy[n,i,j,k]
+ * io_type: MDNN_F16, MDNN_BF16 or MDNN_F32 for x, w, dy (and the mask source).
+ * Accumulation is fp32; dw and db are fp32; y_type / dx_type is MDNN_F32 or
+ * io_type.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int64_t n, h, w, c_in, c_out, r, s, pad;
+} mdnn_conv_shape_t;
+
+mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const void* x, const void* w,
+                              mdnn_dtype_t io_type, const float* bias, mdnn_act_t act, void* y,
+                              mdnn_dtype_t y_type, mdnn_stream_t stream);
+
+/* mask_src: NULL or io_type [n, h, w, c_in] (the stored, post-ReLU input of
+ * the layer); where it is <= 0 the result is 0. */
+mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, const void* dy, const void* w,
+                                   mdnn_dtype_t io_type, const void* mask_src, void* dx,
+                                   mdnn_dtype_t dx_type, mdnn_stream_t stream);
+
+/* Bytes of device workspace mdnn_conv2d_bwd_filter needs for this shape
+ * (fp32 split-K partial sums reduced in a fixed order); 0 on a bad shape. */
+size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape, mdnn_dtype_t io_type);
+
+/* dw: fp32 [c_out, r, s, c_in] (overwritten).  db: NULL or fp32 [c_out]
+ * (overwritten).  workspace: device memory of at least the size above (may be
+ * NULL when that size is 0).  Deterministic. */
+mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x, const void* dy,
+                                     mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
+                                     size_t ws_bytes, mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Bias + activation epilogue as stand-alone kernels (section 2.1: a layer's
+ * activation and its derivative in backpropagation).
+ *   fwd: y = act(x + bias[col]) rounded to y_type;  x fp32 [rows, cols];
+ *        bias NULL or fp32 [cols].
+ *   bwd: dz = dy * [y > 0] (act RELU) or dy (act NONE), stored in `dtype`
+ *        (dz may be NULL, may alias dy); db = column sums of dz in fp32
+ *        (db may be NULL), summed in a fixed order (deterministic).
+ *        dy, y, dz are `dtype` [rows, cols]; y may be NULL when act is NONE.
+ * ------------------------------------------------------------------------- */
+mdnn_status_t mdnn_bias_act_fwd(int64_t rows, int64_t cols, const float* x, const float* bias,
+                                mdnn_act_t act, void* y, mdnn_dtype_t y_type,
+                                mdnn_stream_t stream);
+mdnn_status_t mdnn_bias_act_bwd(int64_t rows, int64_t cols, const void* dy, const void* y,
+                                mdnn_act_t act, void* dz, float* db, mdnn_dtype_t dtype,
+                                mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * 2x2 stride-2 max pooling, NHWC (the LeNet-style workload's pooling layers).
+ * Output [n, h/2, w/2, c] (floor).  The window is scanned row-major and the
+ * first maximum wins; argmax (NULL allowed in fwd) holds that window index
+ * 0..3 per output element.  bwd writes every element of dx [n, h, w, c]:
+ * dy at the argmax position, 0 elsewhere.
+ * ------------------------------------------------------------------------- */
+mdnn_status_t mdnn_maxpool2_fwd(int64_t n, int64_t h, int64_t w, int64_t c, const void* x,
+                                void* y, uint8_t* argmax, mdnn_dtype_t dtype,
+                                mdnn_stream_t stream);
+mdnn_status_t mdnn_maxpool2_bwd(int64_t n, int64_t h, int64_t w, int64_t c, const void* dy,
+                                const uint8_t* argmax, void* dx, mdnn_dtype_t dtype,
+                                mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Losses, mean over the batch.  S = *loss_scale (device fp32; NULL means 1).
+ * softmax_xent: logits fp32 [B, C] (row stride ldl >= C), labels int32 [B];
+ *   *loss_out = -(1/B) sum_i log_softmax(z_i)[label_i]   (unscaled, fp32)
+ *   dlogits[i, j] = S * (softmax(z_i)_j - [j == label_i]) / B  in dlogits_type,
+ *   row stride ldd >= C.  C <= 1024.
+ * mse_loss: y, t fp32 [B, O] (contiguous);
+ *   *loss_out = (1/B) sum (y - t)^2 ;   dy = S * 2 (y - t) / B  in dy_type.
+ * Sums are taken in a fixed order (deterministic).
+ * ------------------------------------------------------------------------- */
+mdnn_status_t mdnn_softmax_xent(int64_t B, int64_t C, const float* logits, int64_t ldl,
+                                const int32_t* labels, const float* loss_scale, float* loss_out,
+                                void* dlogits, int64_t ldd, mdnn_dtype_t dlogits_type,
+                                mdnn_stream_t stream);
+mdnn_status_t mdnn_mse_loss(int64_t B, int64_t O, const float* y, const float* t,
+                            const float* loss_scale, float* loss_out, void* dy,
+                            mdnn_dtype_t dy_type, mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * SGD update (section 3.1) on the flat fp32 master parameters, with optional
+ * heavy-ball momentum and dynamic loss scaling, then the low-precision
+ * working copy:
+ *   if scaler: overflow = any(!isfinite(g));  on overflow the update is skipped
+ *              (w, v, w_lp untouched), scale = max(scale*backoff, min_scale),
+ *              good_steps = 0;  otherwise g /= scale and, after the update,
+ *              ++good_steps == growth_interval -> scale *= growth, good_steps = 0.
+ *   v = momentum*v + g; w -= lr*v        (v != NULL)
+ *   w -= lr*g                            (v == NULL)
+ *   w_lp = RNE(w)                        (w_lp != NULL, lp_type F16/BF16/F32)
+ * The scaler lives in device memory; its overflow field is written by the
+ * call (1 when the step was skipped).  With a scaler the call enqueues three
+ * kernels (finite check, update, scaler state update), otherwise one.
+ * w32 and g32 must be 16-byte aligned.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  float scale;
+  int32_t good_steps;
+  int32_t overflow;
+  int32_t growth_interval;
+  float growth;
+  float backoff;
+  float min_scale;
+  int32_t reserved;  /* internal pending-overflow flag: initialise to 0; every
+                        mdnn_sgd_update call leaves it 0 again */
+} mdnn_scaler_t;
+
+mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
+                              mdnn_dtype_t lp_type, float lr, float momentum,
+                              mdnn_scaler_t* scaler, mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Precision conversion (section 3.2: fp32 data stored as fp16 or bf16).
+ * dst[i] = convert(src[i]) for i < n, round to nearest even.
+ * ------------------------------------------------------------------------- */
+mdnn_status_t mdnn_cast(int64_t n, const void* src, mdnn_dtype_t src_type, void* dst,
+                        mdnn_dtype_t dst_type, mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Train step of a fixed layer chain (section 2.1 compute graph, fixed here;
+ * section 3.1 minibatch SGD).  One call = forward, loss, backpropagation and
+ * update of one minibatch, all enqueued on one stream with no host sync.
+ *
+ * Layer chain: FC (in=c_in, out=c_out), CONV (input [h, w, c_in], c_out
+ * filters r x s, pad; output "same" size required: 2*pad == r-1 == s-1),
+ * MAXPOOL2 (input [h, w, c_in], output [h/2, w/2, c_in], h and w even).
+ * act applies to FC / CONV.  The last layer must be FC or CONV with act NONE.
+ * Storage (section 3.2): activations, working weights and activation
+ * gradients in cfg.dtype; accumulation, bias, logits / outputs, weight
+ * gradients, master weights and momentum in fp32.
+ * Flat parameter packing: per layer in order, weights then bias.
+ * ------------------------------------------------------------------------- */
+typedef enum { MDNN_LAYER_FC = 0, MDNN_LAYER_CONV = 1, MDNN_LAYER_MAXPOOL2 = 2 } mdnn_layer_kind_t;
+typedef enum { MDNN_LOSS_XENT = 0, MDNN_LOSS_MSE = 1 } mdnn_loss_t;
+
+typedef struct {
+  int32_t kind;   /* mdnn_layer_kind_t */
+  int32_t act;    /* mdnn_act_t        */
+  int64_t c_in, h, w, c_out, r, s, pad;
+} mdnn_layer_t;
+
+typedef struct {
+  int32_t dtype;        /* mdnn_dtype_t storage type                          */
+  int32_t loss;         /* mdnn_loss_t                                         */
+  float lr;
+  float momentum;       /* 0: plain SGD (momentum buffer may be NULL)          */
+  int32_t loss_scaling; /* nonzero: dynamic loss scaling via the bound scaler  */
+  int32_t n_classes;    /* cross-entropy classes (= last layer's outputs)      */
+} mdnn_train_cfg_t;
+
+typedef struct mdnn_net mdnn_net_t;
+
+/* Validate the chain and create a host-side handle (host memory only). */
+mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_layers, int64_t batch,
+                              const mdnn_train_cfg_t* cfg, mdnn_net_t** net);
+/* Host outputs: number of parameters and bytes of workspace to bind. */
+mdnn_status_t mdnn_net_sizes(const mdnn_net_t* net, int64_t* n_params, size_t* workspace_bytes);
+/* Bind caller-owned device memory: master_w fp32[n_params] (initialised by the
+ * caller), grads fp32[n_params], momentum fp32[n_params] (NULL iff momentum
+ * is 0; caller zeroes it), lowp_w cfg.dtype[n_params] (NULL for fp32 nets;
+ * filled by mdnn_net_sync_lowp), workspace (>= workspace_bytes, 256-byte
+ * aligned), scaler (NULL iff loss scaling is off; caller initialises it). */
+mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* grads, float* momentum,
+                            void* lowp_w, void* workspace, size_t workspace_bytes,
+                            mdnn_scaler_t* scaler);
+/* Recompute the working low-precision weights from the master weights
+ * (call once after initialising master_w). */
+mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream);
+/* One SGD step.  x: fp32 [batch, in_features] (NHWC-flattened images);
+ * target: int32 labels [batch] (XENT) or fp32 [batch, out] (MSE);
+ * loss_out: device fp32 scalar, the unscaled loss of this step's forward pass. */
+mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
+                              float* loss_out, mdnn_stream_t stream);
+/* Device pointer of stored activation i (0 = the low-precision input, i = output
+ * of layer i-1) inside the bound workspace, for inspection; NULL if invalid. */
+const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i);
+void mdnn_net_destroy(mdnn_net_t* net);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MDNN_H */

@@ -1,0 +1,195 @@
+// 2-D convolution entry points: implicit GEMM on the shared MFMA engine.
+//   fwd:        M = n*Ho*Wo, N = c_out, K = r*s*c_in   (A = im2col(x), B = w as [c_out][K])
+//   bwd_data:   M = n*h*w,   N = c_in,  K = r*s*c_out  (A = im2col of dy with flipped taps, B = w)
+//   bwd_filter: M = c_out,   N = r*s*c_in, K = n*Ho*Wo (A = dy^T, B = shifted x), split over K
+// No im2col buffer is materialised: the operand sources compute addresses.
+#include "gemm_launch.h"
+
+namespace mdnn {
+
+static mdnn_status_t check_shape(const mdnn_conv_shape_t* s, ConvGeom& g) {
+  if (!s) return fail(MDNN_ERR_NULL, "conv: shape is NULL");
+  if (s->n < 0 || s->h < 1 || s->w < 1 || s->c_in < 1 || s->c_out < 1 || s->r < 1 || s->s < 1 ||
+      s->pad < 0)
+    return fail(MDNN_ERR_SHAPE, "conv: sizes must be positive (n >= 0, pad >= 0)");
+  const int64_t ho = s->h + 2 * s->pad - s->r + 1, wo = s->w + 2 * s->pad - s->s + 1;
+  if (ho < 1 || wo < 1) return fail(MDNN_ERR_SHAPE, "conv: empty output");
+  const int64_t lim = 0x7fffffffLL;
+  if (s->h > lim || s->w > lim || s->c_in > lim || s->c_out > lim || s->r > 64 || s->s > 64 ||
+      s->pad > 64 || s->n > lim)
+    return fail(MDNN_ERR_SHAPE, "conv: size out of range");
+  g = ConvGeom{(int32_t)s->n, (int32_t)s->h, (int32_t)s->w, (int32_t)s->c_in, (int32_t)s->c_out,
+               (int32_t)s->r, (int32_t)s->s, (int32_t)s->pad, (int32_t)ho, (int32_t)wo};
+  return MDNN_SUCCESS;
+}
+
+static Epilogue plain_epilogue(void* D, int64_t ldd, mdnn_dtype_t d_type) {
+  Epilogue ep{};
+  ep.alpha = 1.0f;
+  ep.beta = 0.0f;
+  ep.D = D;
+  ep.ldd = ldd;
+  ep.act = MDNN_ACT_NONE;
+  ep.vec4 = (ldd % 4 == 0) && aligned(D, 4 * dtype_size(d_type));
+  return ep;
+}
+
+template <class T, class OutT, class SrcA, class SrcB>
+static mdnn_status_t conv_run(const SrcA& a, const SrcB& b, int64_t M, int64_t N, int64_t K,
+                              const Epilogue& ep, int splits, hipStream_t st) {
+  if constexpr (sizeof(typename T::storage) == 4)
+    return run_gemm32(a, b, M, N, K, ep, splits, st);
+  else
+    return run_gemm16<T, OutT>(a, b, M, N, K, ep, splits, st);
+}
+
+template <class T>
+static mdnn_status_t fwd_impl(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep,
+                              mdnn_dtype_t y_type, hipStream_t st) {
+  typedef typename T::storage S;
+  const int64_t M = (int64_t)g.n * g.ho * g.wo, N = g.k, K = (int64_t)g.r * g.s * g.c;
+  const bool vx = aligned(x, 16) && g.c % 8 == 0;
+  const bool vw = aligned(w, 16) && K % 8 == 0;
+  SrcConvFwdA<S> a{(const S*)x, g, M, K, vx};
+  SrcMatK<S> b{(const S*)w, K, N, K, vw};
+  if (y_type == MDNN_F32) return conv_run<T, F32>(a, b, M, N, K, ep, 1, st);
+  return conv_run<T, T>(a, b, M, N, K, ep, 1, st);
+}
+
+template <class T>
+static mdnn_status_t bwd_data_impl(const ConvGeom& g, const void* dy, const void* w,
+                                   const Epilogue& ep, mdnn_dtype_t dx_type, hipStream_t st) {
+  typedef typename T::storage S;
+  const int64_t M = (int64_t)g.n * g.h * g.w, N = g.c, K = (int64_t)g.r * g.s * g.k;
+  const bool vdy = aligned(dy, 16) && g.k % 8 == 0;
+  const bool vw = aligned(w, 16) && g.c % 8 == 0;
+  SrcConvBwdA<S> a{(const S*)dy, g, M, K, vdy};
+  SrcConvBwdB<S> b{(const S*)w, g, N, K, vw};
+  if (dx_type == MDNN_F32) return conv_run<T, F32>(a, b, M, N, K, ep, 1, st);
+  return conv_run<T, T>(a, b, M, N, K, ep, 1, st);
+}
+
+// Split-K plan of the backward-filter GEMM; a function of the shape only.
+static constexpr size_t FILTER_WS_MAX = 64ull << 20;
+static SplitPlan filter_plan(const ConvGeom& g) {
+  const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
+  const int64_t tiles = ceil_div(M, 128) * ceil_div(N, 128);
+  return plan_splits(M, N, K, tiles, FILTER_WS_MAX);
+}
+
+template <class T>
+static mdnn_status_t bwd_filter_impl(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                                     void* ws, hipStream_t st) {
+  typedef typename T::storage S;
+  const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
+  const bool vdy = aligned(dy, 16) && g.k % 8 == 0;
+  const bool vx = aligned(x, 16) && g.c % 8 == 0;
+  SrcMatMN<S> a{(const S*)dy, g.k, M, K, vdy};
+  SrcConvFiltB<S> b{(const S*)x, g, N, K, vx};
+  SplitPlan p = filter_plan(g);
+  Epilogue ep = plain_epilogue(dw, N, MDNN_F32);
+  if (p.splits > 1) {
+    ep.partial = (float*)ws;
+    ep.k_per_split = p.k_per_split;
+  }
+  MDNN_TRY((conv_run<T, F32>(a, b, M, N, K, ep, p.splits, st)));
+  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st);
+  return MDNN_SUCCESS;
+}
+
+}  // namespace mdnn
+
+using namespace mdnn;
+
+extern "C" mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const void* x,
+                                         const void* w, mdnn_dtype_t io_type, const float* bias,
+                                         mdnn_act_t act, void* y, mdnn_dtype_t y_type,
+                                         mdnn_stream_t stream) {
+  ConvGeom g;
+  MDNN_TRY(check_shape(shape, g));
+  if (!dtype_ok(io_type) || !dtype_ok(y_type) || (y_type != MDNN_F32 && y_type != io_type))
+    return fail(MDNN_ERR_DTYPE, "conv fwd: y_type must be fp32 or io_type");
+  if (act != MDNN_ACT_NONE && act != MDNN_ACT_RELU) return fail(MDNN_ERR_DTYPE, "conv fwd: unknown act");
+  if (g.n == 0) return MDNN_SUCCESS;
+  if (!x || !w || !y) return fail(MDNN_ERR_NULL, "conv fwd: x, w and y are required");
+  const size_t es = dtype_size(io_type);
+  if (!aligned(x, es) || !aligned(w, es) || !aligned(y, dtype_size(y_type)) || (bias && !aligned(bias, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "conv fwd: misaligned base pointer");
+  Epilogue ep = plain_epilogue(y, g.k, y_type);
+  ep.bias = bias;
+  ep.act = act;
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  switch (io_type) {
+    case MDNN_F16: return fwd_impl<F16>(g, x, w, ep, y_type, st);
+    case MDNN_BF16: return fwd_impl<BF16>(g, x, w, ep, y_type, st);
+    default: return fwd_impl<F32>(g, x, w, ep, y_type, st);
+  }
+}
+
+extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, const void* dy,
+                                              const void* w, mdnn_dtype_t io_type,
+                                              const void* mask_src, void* dx,
+                                              mdnn_dtype_t dx_type, mdnn_stream_t stream) {
+  ConvGeom g;
+  MDNN_TRY(check_shape(shape, g));
+  if (!dtype_ok(io_type) || !dtype_ok(dx_type) || (dx_type != MDNN_F32 && dx_type != io_type))
+    return fail(MDNN_ERR_DTYPE, "conv bwd_data: dx_type must be fp32 or io_type");
+  if (g.n == 0) return MDNN_SUCCESS;
+  if (!dy || !w || !dx) return fail(MDNN_ERR_NULL, "conv bwd_data: dy, w and dx are required");
+  const size_t es = dtype_size(io_type);
+  if (!aligned(dy, es) || !aligned(w, es) || !aligned(dx, dtype_size(dx_type)) ||
+      (mask_src && !aligned(mask_src, es)))
+    return fail(MDNN_ERR_MISALIGNED, "conv bwd_data: misaligned base pointer");
+  Epilogue ep = plain_epilogue(dx, g.c, dx_type);
+  ep.mask = mask_src;
+  ep.ldm = g.c;
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  switch (io_type) {
+    case MDNN_F16: return bwd_data_impl<F16>(g, dy, w, ep, dx_type, st);
+    case MDNN_BF16: return bwd_data_impl<BF16>(g, dy, w, ep, dx_type, st);
+    default: return bwd_data_impl<F32>(g, dy, w, ep, dx_type, st);
+  }
+}
+
+extern "C" size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape,
+                                                   mdnn_dtype_t io_type) {
+  ConvGeom g;
+  if (check_shape(shape, g) != MDNN_SUCCESS || !dtype_ok(io_type)) return 0;
+  SplitPlan p = filter_plan(g);
+  if (p.splits <= 1) return 0;
+  return (size_t)p.splits * g.k * ((size_t)g.r * g.s * g.c) * sizeof(float);
+}
+
+extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x,
+                                                const void* dy, mdnn_dtype_t io_type, float* dw,
+                                                float* db, void* workspace, size_t ws_bytes,
+                                                mdnn_stream_t stream) {
+  ConvGeom g;
+  MDNN_TRY(check_shape(shape, g));
+  if (!dtype_ok(io_type)) return fail(MDNN_ERR_DTYPE, "conv bwd_filter: unknown io_type");
+  if (!dw) return fail(MDNN_ERR_NULL, "conv bwd_filter: dw is required");
+  if (g.n > 0 && (!x || !dy)) return fail(MDNN_ERR_NULL, "conv bwd_filter: x and dy are required");
+  const size_t es = dtype_size(io_type);
+  if ((x && !aligned(x, es)) || (dy && !aligned(dy, es)) || !aligned(dw, 4) || (db && !aligned(db, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "conv bwd_filter: misaligned base pointer");
+  const size_t need = mdnn_conv2d_bwd_filter_workspace(shape, io_type);
+  if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 16)))
+    return fail(MDNN_ERR_WORKSPACE, "conv bwd_filter: needs %zu bytes of 16-byte aligned workspace",
+                need);
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  if (g.n == 0) {
+    // empty batch: zero gradients
+    MDNN_TRY(fill_zero(dw, (size_t)g.k * g.r * g.s * g.c * 4, st));
+    return db ? fill_zero(db, (size_t)g.k * 4, st) : MDNN_SUCCESS;
+  }
+  switch (io_type) {
+    case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st)); break;
+    case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st)); break;
+    default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st)); break;
+  }
+  if (db) return column_sums(dy, io_type, (int64_t)g.n * g.ho * g.wo, g.k, db, st);
+  return MDNN_SUCCESS;
+}

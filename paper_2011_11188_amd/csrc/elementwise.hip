@@ -1,0 +1,564 @@
+// Memory-bound kernels of the SGD step: precision conversion, the stand-alone
+// bias+activation epilogue, 2x2 max pooling, the two losses and the SGD /
+// momentum update with dynamic loss scaling.  All reductions are taken in a
+// fixed order, so results are bitwise reproducible.
+#include "gemm_core.h"
+#include "internal.h"
+
+namespace mdnn {
+
+static inline unsigned grid_for(int64_t work, int per_block) {
+  int64_t b = ceil_div(work, per_block);
+  if (b < 1) b = 1;
+  if (b > 0x7fffffffLL) b = 0x7fffffffLL;
+  return (unsigned)b;
+}
+
+// ---------------------------------------------------------------------------
+// zero fill (used instead of memset nodes so callers can capture graphs)
+// ---------------------------------------------------------------------------
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n_words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return MDNN_SUCCESS;
+  if (bytes % 4 || !aligned(p, 4)) return fail(MDNN_ERR_MISALIGNED, "fill_zero: needs 4-byte units");
+  int64_t words = (int64_t)(bytes / 4);
+  unsigned g = grid_for(words, 256);
+  if (g > 4096) g = 4096;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(g), dim3(256), 0, st, (uint32_t*)p, words);
+  return check_launch("fill_zero_kernel");
+}
+
+// ---------------------------------------------------------------------------
+// cast
+// ---------------------------------------------------------------------------
+template <class Src, class Dst, bool VEC>
+__global__ void cast_kernel(const typename Src::storage* __restrict__ src,
+                            typename Dst::storage* __restrict__ dst, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if (VEC) {  // 4 elements per thread, n % 4 == 0, 16/8-byte aligned
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n; i += stride * 4) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_f<Src>(src[i + e]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[i + e] = from_f<Dst>(v[e]);
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+      dst[i] = from_f<Dst>(to_f<Src>(src[i]));
+  }
+}
+
+template <class Src, class Dst>
+static void cast_launch(const void* src, void* dst, int64_t n, bool vec, hipStream_t st) {
+  unsigned g = grid_for(ceil_div(n, vec ? 4 : 1), 256);
+  if (g > 8192) g = 8192;
+  if (vec)
+    hipLaunchKernelGGL((cast_kernel<Src, Dst, true>), dim3(g), dim3(256), 0, st,
+                       (const typename Src::storage*)src, (typename Dst::storage*)dst, n);
+  else
+    hipLaunchKernelGGL((cast_kernel<Src, Dst, false>), dim3(g), dim3(256), 0, st,
+                       (const typename Src::storage*)src, (typename Dst::storage*)dst, n);
+}
+
+mdnn_status_t cast_any(int64_t n, const void* src, mdnn_dtype_t s, void* dst, mdnn_dtype_t d,
+                       hipStream_t st) {
+  if (n == 0) return MDNN_SUCCESS;
+  const bool vec = n % 4 == 0 && aligned(src, 4 * dtype_size(s)) && aligned(dst, 4 * dtype_size(d));
+#define MDNN_CAST_CASE(S_, D_, SI, DI) \
+  if (s == SI && d == DI) { cast_launch<S_, D_>(src, dst, n, vec, st); return check_launch("cast_kernel"); }
+  MDNN_CAST_CASE(F32, F16, MDNN_F32, MDNN_F16)
+  MDNN_CAST_CASE(F32, BF16, MDNN_F32, MDNN_BF16)
+  MDNN_CAST_CASE(F16, F32, MDNN_F16, MDNN_F32)
+  MDNN_CAST_CASE(BF16, F32, MDNN_BF16, MDNN_F32)
+  MDNN_CAST_CASE(F32, F32, MDNN_F32, MDNN_F32)
+  MDNN_CAST_CASE(F16, F16, MDNN_F16, MDNN_F16)
+  MDNN_CAST_CASE(BF16, BF16, MDNN_BF16, MDNN_BF16)
+  MDNN_CAST_CASE(F16, BF16, MDNN_F16, MDNN_BF16)
+  MDNN_CAST_CASE(BF16, F16, MDNN_BF16, MDNN_F16)
+#undef MDNN_CAST_CASE
+  return fail(MDNN_ERR_DTYPE, "cast: unsupported pair");
+}
+
+// ---------------------------------------------------------------------------
+// bias + activation
+// ---------------------------------------------------------------------------
+template <class OutT>
+__global__ void bias_act_fwd_kernel(const float* __restrict__ x, const float* __restrict__ bias,
+                                    int act, typename OutT::storage* __restrict__ y, int64_t rows,
+                                    int64_t cols) {
+  const int64_t n = rows * cols;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float v = x[i];
+    if (bias) v += bias[i % cols];
+    if (act == MDNN_ACT_RELU) v = relu_f(v);
+    y[i] = from_f<OutT>(v);
+  }
+}
+
+template <class T>
+__global__ void relu_mask_kernel(const typename T::storage* __restrict__ dy,
+                                 const typename T::storage* __restrict__ y,
+                                 typename T::storage* __restrict__ dz, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    typename T::storage v = dy[i];
+    dz[i] = (y == nullptr || to_f<T>(y[i]) > 0.0f) ? v : (typename T::storage)0;
+  }
+}
+
+// Column sums of dy (masked by [y > 0] when y != null); 32 columns per block,
+// 8 row lanes each summing rows in order, combined in a fixed order.
+template <class T>
+__global__ void __launch_bounds__(256)
+masked_column_sums_kernel(const typename T::storage* __restrict__ dy,
+                          const typename T::storage* __restrict__ y, int64_t rows, int64_t cols,
+                          float* __restrict__ out) {
+  __shared__ float part[8][33];
+  const int cx = threadIdx.x & 31, ry = threadIdx.x >> 5;
+  const int64_t col = (int64_t)blockIdx.x * 32 + cx;
+  float s = 0.0f;
+  if (col < cols)
+    for (int64_t r = ry; r < rows; r += 8) {
+      const int64_t i = r * cols + col;
+      if (y == nullptr || to_f<T>(y[i]) > 0.0f) s += to_f<T>(dy[i]);
+    }
+  part[ry][cx] = s;
+  __syncthreads();
+  if (ry == 0 && col < cols) {
+    float t = part[0][cx];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += part[k][cx];
+    out[col] = t;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2x2 / stride 2 max pooling, NHWC
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ void maxpool2_fwd_kernel(const typename T::storage* __restrict__ x,
+                                    typename T::storage* __restrict__ y,
+                                    uint8_t* __restrict__ arg, int64_t n, int32_t h, int32_t w,
+                                    int32_t c) {
+  const int32_t ho = h / 2, wo = w / 2;
+  const int64_t total = n * ho * wo * c;
+  for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
+       o += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t ch = (int32_t)(o % c);
+    int64_t t = o / c;
+    const int32_t j = (int32_t)(t % wo);
+    t /= wo;
+    const int32_t i = (int32_t)(t % ho);
+    const int64_t b = t / ho;
+    const typename T::storage* p = x + ((b * h + 2 * i) * w + 2 * j) * c + ch;
+    typename T::storage cand[4] = {p[0], p[c], p[(int64_t)w * c], p[(int64_t)w * c + c]};
+    typename T::storage best = cand[0];
+    float bv = to_f<T>(best);
+    int bi = 0;
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      float v = to_f<T>(cand[k]);
+      if (v > bv) { bv = v; best = cand[k]; bi = k; }
+    }
+    y[o] = best;
+    if (arg) arg[o] = (uint8_t)bi;
+  }
+}
+
+template <class T>
+__global__ void maxpool2_bwd_kernel(const typename T::storage* __restrict__ dy,
+                                    const uint8_t* __restrict__ arg,
+                                    typename T::storage* __restrict__ dx, int64_t n, int32_t h,
+                                    int32_t w, int32_t c) {
+  const int32_t ho = h / 2, wo = w / 2;
+  const int64_t total = n * h * w * c;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t ch = (int32_t)(e % c);
+    int64_t t = e / c;
+    const int32_t xw = (int32_t)(t % w);
+    t /= w;
+    const int32_t xh = (int32_t)(t % h);
+    const int64_t b = t / h;
+    const int32_t i = xh >> 1, j = xw >> 1;
+    typename T::storage v = 0;
+    if (i < ho && j < wo) {
+      const int64_t o = ((b * ho + i) * wo + j) * c + ch;
+      if (arg[o] == (uint8_t)(((xh & 1) << 1) | (xw & 1))) v = dy[o];
+    }
+    dx[e] = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// losses: one block; waves own rows in a fixed order, block sum in a fixed order
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+constexpr int LOSS_THREADS = 1024;
+
+template <class OutT>
+__global__ void __launch_bounds__(LOSS_THREADS)
+softmax_xent_kernel(int64_t B, int64_t C, const float* __restrict__ z, int64_t ldl,
+                    const int32_t* __restrict__ labels, const float* __restrict__ scale_p,
+                    float* __restrict__ loss_out, typename OutT::storage* __restrict__ dz,
+                    int64_t ldd) {
+  __shared__ float wsum[LOSS_THREADS / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nw = LOSS_THREADS / 64;
+  const float S = scale_p ? *scale_p : 1.0f;
+  const float inv_b = 1.0f / (float)B;
+  float acc = 0.0f;  // lane 0: this wave's rows, in order
+  for (int64_t r = wave; r < B; r += nw) {
+    const float* zr = z + r * ldl;
+    float m = -INFINITY;
+    for (int64_t j = lane; j < C; j += 64) m = fmaxf(m, zr[j]);
+    m = wave_max(m);
+    float se = 0.0f;
+    for (int64_t j = lane; j < C; j += 64) se += expf(zr[j] - m);
+    se = wave_sum(se);
+    const float lse = m + logf(se);
+    const int32_t lab = labels[r];
+    const bool ok = lab >= 0 && lab < C;
+    for (int64_t j = lane; j < C; j += 64) {
+      const float p = expf(zr[j] - lse);
+      float g = S * (p - (j == lab ? 1.0f : 0.0f)) * inv_b;
+      if (!ok) g = NAN;
+      dz[r * ldd + j] = from_f<OutT>(g);
+    }
+    if (lane == 0) acc += ok ? (lse - zr[lab]) : NAN;
+  }
+  if (lane == 0) wsum[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int k = 0; k < nw; ++k) t += wsum[k];
+    *loss_out = t * inv_b;
+  }
+}
+
+template <class OutT>
+__global__ void __launch_bounds__(LOSS_THREADS)
+mse_kernel(int64_t n, int64_t B, const float* __restrict__ y, const float* __restrict__ t,
+           const float* __restrict__ scale_p, float* __restrict__ loss_out,
+           typename OutT::storage* __restrict__ dy) {
+  __shared__ float red[LOSS_THREADS];
+  const float S = scale_p ? *scale_p : 1.0f;
+  const float c = 2.0f * S / (float)B;
+  float acc = 0.0f;
+  for (int64_t i = threadIdx.x; i < n; i += LOSS_THREADS) {
+    const float d = y[i] - t[i];
+    acc = fmaf(d, d, acc);
+    dy[i] = from_f<OutT>(c * d);
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = LOSS_THREADS / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss_out = red[0] / (float)B;
+}
+
+// ---------------------------------------------------------------------------
+// SGD / momentum with dynamic loss scaling
+//   check:    scaler->reserved |= any(!isfinite(g))          (reserved starts at 0)
+//   update:   skipped when reserved != 0
+//   finalize: scale / good_steps / overflow state machine; reserved = 0
+// ---------------------------------------------------------------------------
+__global__ void finite_check_kernel(const float* __restrict__ g, int64_t n,
+                                    mdnn_scaler_t* __restrict__ sc) {
+  int bad = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n4 = n / 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 v = ((const float4*)g)[i];
+    bad |= (int)!isfinite(v.x) | (int)!isfinite(v.y) | (int)!isfinite(v.z) | (int)!isfinite(v.w);
+  }
+  for (int64_t i = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    bad |= !isfinite(g[i]);
+  bad = __syncthreads_or(bad);
+  if (bad && threadIdx.x == 0) atomicOr(&sc->reserved, 1);
+}
+
+template <class LpT, bool MOM, bool SCALE>
+__global__ void sgd_kernel(int64_t n, float* __restrict__ w, const float* __restrict__ g,
+                           float* __restrict__ v, typename LpT::storage* __restrict__ wlp, float lr,
+                           float mu, const mdnn_scaler_t* __restrict__ sc) {
+  float S = 1.0f;
+  if (SCALE) {
+    if (sc->reserved) return;  // overflow: skip the whole update
+    S = sc->scale;
+  }
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    float gi = g[i];
+    if (SCALE) gi = gi / S;
+    float wi = w[i];
+    if (MOM) {
+      const float vi = fmaf(mu, v[i], gi);
+      v[i] = vi;
+      wi = fmaf(-lr, vi, wi);
+    } else {
+      wi = fmaf(-lr, gi, wi);
+    }
+    w[i] = wi;
+    if (wlp) wlp[i] = from_f<LpT>(wi);
+  }
+}
+
+__global__ void scaler_finalize_kernel(mdnn_scaler_t* sc) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  if (sc->reserved) {
+    float s = sc->scale * sc->backoff;
+    sc->scale = s < sc->min_scale ? sc->min_scale : s;
+    sc->good_steps = 0;
+    sc->overflow = 1;
+  } else {
+    sc->overflow = 0;
+    sc->good_steps += 1;
+    if (sc->good_steps >= sc->growth_interval) {
+      sc->scale = sc->scale * sc->growth;
+      sc->good_steps = 0;
+    }
+  }
+  sc->reserved = 0;
+}
+
+template <class LpT>
+static void sgd_launch(int64_t n, float* w, const float* g, float* v, void* wlp, float lr, float mu,
+                       const mdnn_scaler_t* sc, hipStream_t st) {
+  unsigned grid = grid_for(n, 256);
+  if (grid > 8192) grid = 8192;
+  typedef typename LpT::storage L;
+#define MDNN_SGD(M_, S_) \
+  hipLaunchKernelGGL((sgd_kernel<LpT, M_, S_>), dim3(grid), dim3(256), 0, st, n, w, g, v, (L*)wlp, lr, mu, sc)
+  if (v && sc) MDNN_SGD(true, true);
+  else if (v) MDNN_SGD(true, false);
+  else if (sc) MDNN_SGD(false, true);
+  else MDNN_SGD(false, false);
+#undef MDNN_SGD
+}
+
+}  // namespace mdnn
+
+using namespace mdnn;
+
+extern "C" mdnn_status_t mdnn_cast(int64_t n, const void* src, mdnn_dtype_t src_type, void* dst,
+                                   mdnn_dtype_t dst_type, mdnn_stream_t stream) {
+  if (n < 0) return fail(MDNN_ERR_SHAPE, "cast: n < 0");
+  if (!dtype_ok(src_type) || !dtype_ok(dst_type)) return fail(MDNN_ERR_DTYPE, "cast: unknown dtype");
+  if (n == 0) return MDNN_SUCCESS;
+  if (!src || !dst) return fail(MDNN_ERR_NULL, "cast: NULL buffer");
+  if (!aligned(src, dtype_size(src_type)) || !aligned(dst, dtype_size(dst_type)))
+    return fail(MDNN_ERR_MISALIGNED, "cast: misaligned buffer");
+  clear_error();
+  return cast_any(n, src, src_type, dst, dst_type, as_stream(stream));
+}
+
+extern "C" mdnn_status_t mdnn_bias_act_fwd(int64_t rows, int64_t cols, const float* x,
+                                           const float* bias, mdnn_act_t act, void* y,
+                                           mdnn_dtype_t y_type, mdnn_stream_t stream) {
+  if (rows < 0 || cols < 0) return fail(MDNN_ERR_SHAPE, "bias_act_fwd: negative size");
+  if (!dtype_ok(y_type)) return fail(MDNN_ERR_DTYPE, "bias_act_fwd: unknown dtype");
+  if (act != MDNN_ACT_NONE && act != MDNN_ACT_RELU) return fail(MDNN_ERR_DTYPE, "bias_act_fwd: unknown act");
+  if (rows == 0 || cols == 0) return MDNN_SUCCESS;
+  if (!x || !y) return fail(MDNN_ERR_NULL, "bias_act_fwd: NULL buffer");
+  if (!aligned(x, 4) || !aligned(y, dtype_size(y_type)) || (bias && !aligned(bias, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "bias_act_fwd: misaligned buffer");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  unsigned g = grid_for(rows * cols, 256);
+  if (g > 8192) g = 8192;
+  switch (y_type) {
+    case MDNN_F32: hipLaunchKernelGGL(bias_act_fwd_kernel<F32>, dim3(g), dim3(256), 0, st, x, bias, (int)act, (float*)y, rows, cols); break;
+    case MDNN_F16: hipLaunchKernelGGL(bias_act_fwd_kernel<F16>, dim3(g), dim3(256), 0, st, x, bias, (int)act, (uint16_t*)y, rows, cols); break;
+    default: hipLaunchKernelGGL(bias_act_fwd_kernel<BF16>, dim3(g), dim3(256), 0, st, x, bias, (int)act, (uint16_t*)y, rows, cols); break;
+  }
+  return check_launch("bias_act_fwd_kernel");
+}
+
+template <class T>
+static mdnn_status_t bias_act_bwd_t(int64_t rows, int64_t cols, const void* dy, const void* y,
+                                    void* dz, float* db, hipStream_t st) {
+  typedef typename T::storage S;
+  if (db) {
+    hipLaunchKernelGGL(masked_column_sums_kernel<T>, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
+                       (const S*)dy, (const S*)y, rows, cols, db);
+    MDNN_TRY(check_launch("masked_column_sums_kernel"));
+  }
+  if (dz) {
+    unsigned g = grid_for(rows * cols, 256);
+    if (g > 8192) g = 8192;
+    hipLaunchKernelGGL(relu_mask_kernel<T>, dim3(g), dim3(256), 0, st, (const S*)dy, (const S*)y, (S*)dz,
+                       rows * cols);
+    MDNN_TRY(check_launch("relu_mask_kernel"));
+  }
+  return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_bias_act_bwd(int64_t rows, int64_t cols, const void* dy,
+                                           const void* y, mdnn_act_t act, void* dz, float* db,
+                                           mdnn_dtype_t dtype, mdnn_stream_t stream) {
+  if (rows < 0 || cols < 0) return fail(MDNN_ERR_SHAPE, "bias_act_bwd: negative size");
+  if (!dtype_ok(dtype)) return fail(MDNN_ERR_DTYPE, "bias_act_bwd: unknown dtype");
+  if (act != MDNN_ACT_NONE && act != MDNN_ACT_RELU) return fail(MDNN_ERR_DTYPE, "bias_act_bwd: unknown act");
+  if (cols == 0) return MDNN_SUCCESS;
+  if (db && rows == 0) {
+    clear_error();
+    return fill_zero(db, (size_t)cols * 4, as_stream(stream));
+  }
+  if (rows == 0) return MDNN_SUCCESS;
+  if (!dy) return fail(MDNN_ERR_NULL, "bias_act_bwd: dy is NULL");
+  if (act == MDNN_ACT_RELU && !y) return fail(MDNN_ERR_NULL, "bias_act_bwd: ReLU needs y");
+  const size_t es = dtype_size(dtype);
+  if (!aligned(dy, es) || (y && !aligned(y, es)) || (dz && !aligned(dz, es)) || (db && !aligned(db, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "bias_act_bwd: misaligned buffer");
+  const void* ym = act == MDNN_ACT_RELU ? y : nullptr;
+  if (dz == dy && act == MDNN_ACT_NONE) dz = nullptr;  // nothing to write
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  switch (dtype) {
+    case MDNN_F32: return bias_act_bwd_t<F32>(rows, cols, dy, ym, dz, db, st);
+    case MDNN_F16: return bias_act_bwd_t<F16>(rows, cols, dy, ym, dz, db, st);
+    default: return bias_act_bwd_t<BF16>(rows, cols, dy, ym, dz, db, st);
+  }
+}
+
+extern "C" mdnn_status_t mdnn_maxpool2_fwd(int64_t n, int64_t h, int64_t w, int64_t c,
+                                           const void* x, void* y, uint8_t* argmax,
+                                           mdnn_dtype_t dtype, mdnn_stream_t stream) {
+  if (n < 0 || h < 0 || w < 0 || c < 0 || h > 0x7fffffff || w > 0x7fffffff || c > 0x7fffffff)
+    return fail(MDNN_ERR_SHAPE, "maxpool2_fwd: bad size");
+  if (!dtype_ok(dtype)) return fail(MDNN_ERR_DTYPE, "maxpool2_fwd: unknown dtype");
+  const int64_t total = n * (h / 2) * (w / 2) * c;
+  if (total == 0) return MDNN_SUCCESS;
+  if (!x || !y) return fail(MDNN_ERR_NULL, "maxpool2_fwd: NULL buffer");
+  const size_t es = dtype_size(dtype);
+  if (!aligned(x, es) || !aligned(y, es)) return fail(MDNN_ERR_MISALIGNED, "maxpool2_fwd: misaligned");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  unsigned g = grid_for(total, 256);
+  if (g > 16384) g = 16384;
+  switch (dtype) {
+    case MDNN_F32: hipLaunchKernelGGL(maxpool2_fwd_kernel<F32>, dim3(g), dim3(256), 0, st, (const float*)x, (float*)y, argmax, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+    case MDNN_F16: hipLaunchKernelGGL(maxpool2_fwd_kernel<F16>, dim3(g), dim3(256), 0, st, (const uint16_t*)x, (uint16_t*)y, argmax, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+    default: hipLaunchKernelGGL(maxpool2_fwd_kernel<BF16>, dim3(g), dim3(256), 0, st, (const uint16_t*)x, (uint16_t*)y, argmax, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+  }
+  return check_launch("maxpool2_fwd_kernel");
+}
+
+extern "C" mdnn_status_t mdnn_maxpool2_bwd(int64_t n, int64_t h, int64_t w, int64_t c,
+                                           const void* dy, const uint8_t* argmax, void* dx,
+                                           mdnn_dtype_t dtype, mdnn_stream_t stream) {
+  if (n < 0 || h < 0 || w < 0 || c < 0 || h > 0x7fffffff || w > 0x7fffffff || c > 0x7fffffff)
+    return fail(MDNN_ERR_SHAPE, "maxpool2_bwd: bad size");
+  if (!dtype_ok(dtype)) return fail(MDNN_ERR_DTYPE, "maxpool2_bwd: unknown dtype");
+  const int64_t total = n * h * w * c;
+  if (total == 0) return MDNN_SUCCESS;
+  if (!dx) return fail(MDNN_ERR_NULL, "maxpool2_bwd: dx is NULL");
+  if ((n * (h / 2) * (w / 2) * c) > 0 && (!dy || !argmax))
+    return fail(MDNN_ERR_NULL, "maxpool2_bwd: dy and argmax are required");
+  const size_t es = dtype_size(dtype);
+  if ((dy && !aligned(dy, es)) || !aligned(dx, es)) return fail(MDNN_ERR_MISALIGNED, "maxpool2_bwd: misaligned");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  unsigned g = grid_for(total, 256);
+  if (g > 16384) g = 16384;
+  switch (dtype) {
+    case MDNN_F32: hipLaunchKernelGGL(maxpool2_bwd_kernel<F32>, dim3(g), dim3(256), 0, st, (const float*)dy, argmax, (float*)dx, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+    case MDNN_F16: hipLaunchKernelGGL(maxpool2_bwd_kernel<F16>, dim3(g), dim3(256), 0, st, (const uint16_t*)dy, argmax, (uint16_t*)dx, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+    default: hipLaunchKernelGGL(maxpool2_bwd_kernel<BF16>, dim3(g), dim3(256), 0, st, (const uint16_t*)dy, argmax, (uint16_t*)dx, n, (int32_t)h, (int32_t)w, (int32_t)c); break;
+  }
+  return check_launch("maxpool2_bwd_kernel");
+}
+
+extern "C" mdnn_status_t mdnn_softmax_xent(int64_t B, int64_t C, const float* logits, int64_t ldl,
+                                           const int32_t* labels, const float* loss_scale,
+                                           float* loss_out, void* dlogits, int64_t ldd,
+                                           mdnn_dtype_t dlogits_type, mdnn_stream_t stream) {
+  if (B < 1 || C < 1 || C > 1024) return fail(MDNN_ERR_SHAPE, "softmax_xent: need B >= 1, 1 <= C <= 1024");
+  if (ldl < C || ldd < C) return fail(MDNN_ERR_LAYOUT, "softmax_xent: row stride < C");
+  if (!dtype_ok(dlogits_type)) return fail(MDNN_ERR_DTYPE, "softmax_xent: unknown dtype");
+  if (!logits || !labels || !loss_out || !dlogits) return fail(MDNN_ERR_NULL, "softmax_xent: NULL buffer");
+  if (!aligned(logits, 4) || !aligned(labels, 4) || !aligned(loss_out, 4) ||
+      !aligned(dlogits, dtype_size(dlogits_type)) || (loss_scale && !aligned(loss_scale, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "softmax_xent: misaligned buffer");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  switch (dlogits_type) {
+    case MDNN_F32: hipLaunchKernelGGL(softmax_xent_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd); break;
+    case MDNN_F16: hipLaunchKernelGGL(softmax_xent_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
+    default: hipLaunchKernelGGL(softmax_xent_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
+  }
+  return check_launch("softmax_xent_kernel");
+}
+
+extern "C" mdnn_status_t mdnn_mse_loss(int64_t B, int64_t O, const float* y, const float* t,
+                                       const float* loss_scale, float* loss_out, void* dy,
+                                       mdnn_dtype_t dy_type, mdnn_stream_t stream) {
+  if (B < 1 || O < 1) return fail(MDNN_ERR_SHAPE, "mse_loss: need B, O >= 1");
+  if (!dtype_ok(dy_type)) return fail(MDNN_ERR_DTYPE, "mse_loss: unknown dtype");
+  if (!y || !t || !loss_out || !dy) return fail(MDNN_ERR_NULL, "mse_loss: NULL buffer");
+  if (!aligned(y, 4) || !aligned(t, 4) || !aligned(loss_out, 4) || !aligned(dy, dtype_size(dy_type)) ||
+      (loss_scale && !aligned(loss_scale, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "mse_loss: misaligned buffer");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  const int64_t n = B * O;
+  switch (dy_type) {
+    case MDNN_F32: hipLaunchKernelGGL(mse_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, n, B, y, t, loss_scale, loss_out, (float*)dy); break;
+    case MDNN_F16: hipLaunchKernelGGL(mse_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, n, B, y, t, loss_scale, loss_out, (uint16_t*)dy); break;
+    default: hipLaunchKernelGGL(mse_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), 0, st, n, B, y, t, loss_scale, loss_out, (uint16_t*)dy); break;
+  }
+  return check_launch("mse_kernel");
+}
+
+extern "C" mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v32,
+                                         void* w_lp, mdnn_dtype_t lp_type, float lr,
+                                         float momentum, mdnn_scaler_t* scaler,
+                                         mdnn_stream_t stream) {
+  if (n < 0) return fail(MDNN_ERR_SHAPE, "sgd_update: n < 0");
+  if (!dtype_ok(lp_type)) return fail(MDNN_ERR_DTYPE, "sgd_update: unknown lp_type");
+  if (n > 0 && (!w32 || !g32)) return fail(MDNN_ERR_NULL, "sgd_update: w32 and g32 are required");
+  if ((w32 && !aligned(w32, 16)) || (g32 && !aligned(g32, 16)) || (v32 && !aligned(v32, 4)) ||
+      (w_lp && !aligned(w_lp, dtype_size(lp_type))) || (scaler && !aligned(scaler, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "sgd_update: w32/g32 need 16-byte alignment");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  if (scaler && n > 0) {
+    unsigned g = grid_for(ceil_div(n, 4), 256);
+    if (g > 2048) g = 2048;
+    hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);
+    MDNN_TRY(check_launch("finite_check_kernel"));
+  }
+  if (n > 0) {
+    switch (lp_type) {
+      case MDNN_F32: sgd_launch<F32>(n, w32, g32, v32, w_lp, lr, momentum, scaler, st); break;
+      case MDNN_F16: sgd_launch<F16>(n, w32, g32, v32, w_lp, lr, momentum, scaler, st); break;
+      default: sgd_launch<BF16>(n, w32, g32, v32, w_lp, lr, momentum, scaler, st); break;
+    }
+    MDNN_TRY(check_launch("sgd_kernel"));
+  }
+  if (scaler) {
+    hipLaunchKernelGGL(scaler_finalize_kernel, dim3(1), dim3(64), 0, st, scaler);
+    MDNN_TRY(check_launch("scaler_finalize_kernel"));
+  }
+  return MDNN_SUCCESS;
+}

@@ -1,0 +1,515 @@
+// MFMA GEMM engine for gfx950: D = epi(alpha * op(A) op(B) + beta * C).
+//
+// Section 3.2 of the paper: the matrix unit computes D = C + A*B with
+// low-precision A, B and an fp32 accumulator; on CDNA4 that unit is
+// v_mfma_f32_16x16x32_{f16,bf16} (16x16 output, 32-deep, fp32 accumulate).
+//
+// Structure (one workgroup = one BM x BN output tile, WM x WN waves of 64):
+//   * operands are described by "sources" that return 16-byte chunks of 8
+//     consecutive elements along their contiguous dimension: plain row-major
+//     matrices, or implicit-im2col views of NHWC tensors for convolution;
+//   * each K step of BK = 64 is staged global -> registers -> LDS, with two
+//     LDS buffers so the next tile's global loads are in flight while the
+//     current tile feeds the MFMAs (one barrier per K step);
+//   * LDS holds both operands K-contiguous, [rows][BK + 8] (the 16-byte row
+//     pad spreads the 16-byte fragment reads of 16 rows over all banks);
+//     an operand stored MN-contiguous in memory is transposed in registers
+//     (4 k x 8 mn blocks) on its way to LDS;
+//   * the MFMA is issued with B as its first operand, so each lane ends with
+//     4 consecutive columns of one row (a 16-byte fp32 / 8-byte fp16 store);
+//   * the epilogue applies alpha, beta*C, bias, ReLU, the ReLU mask of a
+//     backward-data product and the rounding to the output type, or writes
+//     fp32 split-K partials that a second kernel reduces in a fixed order.
+//   * workgroup ids are remapped so that consecutive tiles land on the same
+//     XCD (8 XCDs, round-robin dispatch), grouped by GROUP_M tile rows.
+#pragma once
+
+#include "common.h"
+
+namespace mdnn {
+
+constexpr int GEMM_BK = 64;
+constexpr int GEMM_PAD = 8;                     // elements of row padding in LDS
+constexpr int GEMM_LDK = GEMM_BK + GEMM_PAD;    // LDS row pitch (elements)
+
+// ---------------------------------------------------------------------------
+// operand sources (16-bit element types; `vec` allows 16-byte loads)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint4 pack8(const uint16_t v[8]) {
+  uint4 r;
+  r.x = (uint32_t)v[0] | ((uint32_t)v[1] << 16);
+  r.y = (uint32_t)v[2] | ((uint32_t)v[3] << 16);
+  r.z = (uint32_t)v[4] | ((uint32_t)v[5] << 16);
+  r.w = (uint32_t)v[6] | ((uint32_t)v[7] << 16);
+  return r;
+}
+
+// Every source gives elem(mn, k) (bounds-checked, zero outside; mn is the
+// operand's M index for A and N index for B) for any storage type S, and, for
+// 16-bit storage, chunk(...) = 8 consecutive elements along the contiguous
+// dimension packed into 16 bytes: chunk(mn, k) for K-contiguous sources,
+// chunk(k, mn) for MN-contiguous ones.
+
+// Row-major matrix whose contiguous dimension is K: elem(mn, k) = p[mn*ld + k].
+template <class S>
+struct SrcMatK {
+  static constexpr bool KC = true;
+  const S* p;
+  int64_t ld, MN, K;
+  bool vec;
+  __device__ __forceinline__ S elem(int64_t mn, int64_t k) const {
+    return (mn < MN && k < K) ? p[mn * ld + k] : (S)0;
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t mn, int64_t k) const {
+    if (mn < MN && vec && k + 8 <= K) return *(const uint4*)(p + mn * ld + k);
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = elem(mn, k + e);
+    return pack8(v);
+  }
+};
+
+// Row-major matrix whose contiguous dimension is M (or N): elem(mn, k) = p[k*ld + mn].
+template <class S>
+struct SrcMatMN {
+  static constexpr bool KC = false;
+  const S* p;
+  int64_t ld, MN, K;
+  bool vec;
+  __device__ __forceinline__ S elem(int64_t mn, int64_t k) const {
+    return (k < K && mn < MN) ? p[k * ld + mn] : (S)0;
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t k, int64_t mn) const {
+    if (k < K && vec && mn + 8 <= MN) return *(const uint4*)(p + k * ld + mn);
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = elem(mn + e, k);
+    return pack8(v);
+  }
+};
+
+// Convolution geometry, stride 1, zero padding.
+struct ConvGeom {
+  int32_t n, h, w, c, k, r, s, pad, ho, wo;
+};
+
+// Forward, operand A[m, kk]: m = (n, i, j) over the output, kk = (r, s, c);
+// elem = x[n, i + r - pad, j + s - pad, c].  K-contiguous (c fastest).
+template <class S>
+struct SrcConvFwdA {
+  static constexpr bool KC = true;
+  const S* x;
+  ConvGeom g;
+  int64_t MN, K;
+  bool vec;  // c % 8 == 0 and 16-byte aligned base
+  // offset of (m, kk) in x, or -1 in the zero padding
+  __device__ __forceinline__ int64_t offset(int64_t m, int64_t kk) const {
+    int32_t c = (int32_t)(kk % g.c);
+    int32_t rs = (int32_t)(kk / g.c);
+    int32_t s = rs % g.s, r = rs / g.s;
+    int32_t j = (int32_t)(m % g.wo);
+    int64_t t = m / g.wo;
+    int32_t i = (int32_t)(t % g.ho);
+    int32_t n = (int32_t)(t / g.ho);
+    int32_t hi = i + r - g.pad, wi = j + s - g.pad;
+    if (hi < 0 || hi >= g.h || wi < 0 || wi >= g.w) return -1;
+    return (((int64_t)n * g.h + hi) * g.w + wi) * g.c + c;
+  }
+  __device__ __forceinline__ S elem(int64_t m, int64_t kk) const {
+    if (m >= MN || kk >= K) return (S)0;
+    int64_t o = offset(m, kk);
+    return o < 0 ? (S)0 : x[o];
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
+    if (vec && m < MN && kk + 8 <= K) {
+      int64_t o = offset(m, kk);
+      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(x + o);
+    }
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = elem(m, kk + e);
+    return pack8(v);
+  }
+};
+
+// Backward-data, operand A[m, kk]: m = (n, h, w) over the input image,
+// kk = (r, s, k); elem = dy[n, h - r + pad, w - s + pad, k].  K-contiguous.
+template <class S>
+struct SrcConvBwdA {
+  static constexpr bool KC = true;
+  const S* dy;
+  ConvGeom g;
+  int64_t MN, K;
+  bool vec;  // k % 8 == 0
+  __device__ __forceinline__ int64_t offset(int64_t m, int64_t kk) const {
+    int32_t ch = (int32_t)(kk % g.k);
+    int32_t rs = (int32_t)(kk / g.k);
+    int32_t s = rs % g.s, r = rs / g.s;
+    int32_t wj = (int32_t)(m % g.w);
+    int64_t t = m / g.w;
+    int32_t hi = (int32_t)(t % g.h);
+    int32_t n = (int32_t)(t / g.h);
+    int32_t i = hi - r + g.pad, j = wj - s + g.pad;
+    if (i < 0 || i >= g.ho || j < 0 || j >= g.wo) return -1;
+    return (((int64_t)n * g.ho + i) * g.wo + j) * g.k + ch;
+  }
+  __device__ __forceinline__ S elem(int64_t m, int64_t kk) const {
+    if (m >= MN || kk >= K) return (S)0;
+    int64_t o = offset(m, kk);
+    return o < 0 ? (S)0 : dy[o];
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
+    if (vec && m < MN && kk + 8 <= K) {
+      int64_t o = offset(m, kk);
+      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(dy + o);
+    }
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = elem(m, kk + e);
+    return pack8(v);
+  }
+};
+
+// Backward-data, operand B[kk, c] with kk = (r, s, k): elem = w[k, r, s, c].
+// MN-contiguous along c.
+template <class S>
+struct SrcConvBwdB {
+  static constexpr bool KC = false;
+  const S* wt;
+  ConvGeom g;
+  int64_t MN, K;  // MN = c, K = r*s*k
+  bool vec;       // c % 8 == 0
+  __device__ __forceinline__ int64_t row(int64_t kk) const {
+    int32_t ch = (int32_t)(kk % g.k);
+    int32_t rs = (int32_t)(kk / g.k);
+    return ((int64_t)ch * g.r * g.s + rs) * g.c;
+  }
+  __device__ __forceinline__ S elem(int64_t c, int64_t kk) const {
+    return (kk < K && c < MN) ? wt[row(kk) + c] : (S)0;
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t c) const {
+    if (kk >= K) return make_uint4(0, 0, 0, 0);
+    const S* p = wt + row(kk);
+    if (vec && c + 8 <= MN) return *(const uint4*)(p + c);
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (c + e < MN) ? p[c + e] : (S)0;
+    return pack8(v);
+  }
+};
+
+// Backward-filter, operand B[kk, nn] with kk = (n, i, j) over the output and
+// nn = (r, s, c): elem = x[n, i + r - pad, j + s - pad, c].  MN-contiguous.
+template <class S>
+struct SrcConvFiltB {
+  static constexpr bool KC = false;
+  const S* x;
+  ConvGeom g;
+  int64_t MN, K;  // MN = r*s*c, K = n*ho*wo
+  bool vec;       // c % 8 == 0
+  __device__ __forceinline__ int64_t offset(int64_t kk, int64_t nn) const {
+    int32_t c = (int32_t)(nn % g.c);
+    int32_t rs = (int32_t)(nn / g.c);
+    int32_t s = rs % g.s, r = rs / g.s;
+    int32_t j = (int32_t)(kk % g.wo);
+    int64_t t = kk / g.wo;
+    int32_t i = (int32_t)(t % g.ho);
+    int32_t n = (int32_t)(t / g.ho);
+    int32_t hi = i + r - g.pad, wi = j + s - g.pad;
+    if (hi < 0 || hi >= g.h || wi < 0 || wi >= g.w) return -1;
+    return (((int64_t)n * g.h + hi) * g.w + wi) * g.c + c;
+  }
+  __device__ __forceinline__ S elem(int64_t nn, int64_t kk) const {
+    if (kk >= K || nn >= MN) return (S)0;
+    int64_t o = offset(kk, nn);
+    return o < 0 ? (S)0 : x[o];
+  }
+  __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t nn) const {
+    if (vec && kk < K && nn + 8 <= MN) {
+      int64_t o = offset(kk, nn);
+      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(x + o);
+    }
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = elem(nn + e, kk);
+    return pack8(v);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// epilogue description
+// ---------------------------------------------------------------------------
+struct Epilogue {
+  float alpha, beta;
+  const void* C;       // d_type [M, ldc], read iff beta != 0
+  int64_t ldc;
+  void* D;             // d_type [M, ldd]  (or fp32 partials when split)
+  int64_t ldd;
+  const float* bias;   // [N] or null
+  const void* mask;    // ab_type [M, ldm] or null
+  int64_t ldm;
+  int32_t act;
+  int32_t vec4;        // 4-wide stores allowed (ldd, ldc, ldm % 4 == 0 and aligned bases)
+  float* partial;      // split-K: fp32 [splits][M][N]; null otherwise
+  int64_t k_per_split; // multiple of GEMM_BK
+};
+
+template <class MaskT, class OutT>
+__device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, int64_t N, int64_t m,
+                                                int64_t n, float4_t acc) {
+  if (m >= M) return;
+  float v[4] = {acc[0], acc[1], acc[2], acc[3]};
+  const bool full = ep.vec4 && n + 4 <= N;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] *= ep.alpha;
+  }
+  if (ep.beta != 0.0f) {
+    const typename OutT::storage* c = (const typename OutT::storage*)ep.C + m * ep.ldc + n;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < N) v[e] += ep.beta * to_f<OutT>(c[e]);
+  }
+  if (ep.bias) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < N) v[e] += ep.bias[n + e];
+  }
+  if (ep.act == MDNN_ACT_RELU) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = relu_f(v[e]);
+  }
+  if (ep.mask) {
+    const typename MaskT::storage* mk = (const typename MaskT::storage*)ep.mask + m * ep.ldm + n;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < N && !(to_f<MaskT>(mk[e]) > 0.0f)) v[e] = 0.0f;
+  }
+  typename OutT::storage* d = (typename OutT::storage*)ep.D + m * ep.ldd + n;
+  if (full) {
+    if constexpr (sizeof(typename OutT::storage) == 4) {
+      *(float4*)d = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+      uint2 u;
+      u.x = (uint32_t)from_f<OutT>(v[0]) | ((uint32_t)from_f<OutT>(v[1]) << 16);
+      u.y = (uint32_t)from_f<OutT>(v[2]) | ((uint32_t)from_f<OutT>(v[3]) << 16);
+      *(uint2*)d = u;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < N) d[e] = from_f<OutT>(v[e]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// the kernel
+// ---------------------------------------------------------------------------
+template <class T> struct Mfma;
+template <> struct Mfma<F16> {
+  static __device__ __forceinline__ float4_t run(uint4 a, uint4 b, float4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a),
+                                                  __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<BF16> {
+  static __device__ __forceinline__ float4_t run(uint4 a, uint4 b, float4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bhalf8_t, a),
+                                                   __builtin_bit_cast(bhalf8_t, b), c, 0, 0, 0);
+  }
+};
+
+template <int BM, int BN, int WM, int WN>
+struct TileShape {
+  static constexpr int NT = WM * WN * 64;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
+  static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 fragments per wave
+  static constexpr int RA = BM * GEMM_BK / 8 / NT;    // 16-byte chunks per thread (A)
+  static constexpr int RB = BN * GEMM_BK / 8 / NT;    // (B)
+  static constexpr int LDS_ELEMS = (BM + BN) * GEMM_LDK;
+  static_assert(BM % (WM * 16) == 0 && BN % (WN * 16) == 0, "wave tile");
+  static_assert(RA >= 1 && RB >= 1 && RA * NT * 8 == BM * GEMM_BK && RB * NT * 8 == BN * GEMM_BK,
+                "loader split");
+  static_assert(BM % 32 == 0 && BN % 32 == 0, "MN-contiguous loader granularity");
+};
+
+// Global -> registers for one operand tile of ROWS rows x BK.
+// K-contiguous: chunk c = tid + i*NT -> (row = c / 8, k = (c % 8) * 8).
+// MN-contiguous: chunk c -> a 4(k) x 8(mn) block: within each group of 64
+//   chunks, 16 k-quads x 4 mn-octets; each block = 4 loads of 8 mn values.
+template <class Src, int ROWS, int NT, int R>
+__device__ __forceinline__ void load_tile(const Src& src, int64_t mn0, int64_t k0, int tid,
+                                          uint4 (&reg)[R]) {
+  if constexpr (Src::KC) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      int c = tid + i * NT;
+      reg[i] = src.chunk(mn0 + (c >> 3), k0 + (c & 7) * 8);
+    }
+  } else {
+    static_assert(R % 4 == 0 || R < 4, "");
+    // R chunks = R/4 blocks of 4 loads (R >= 4), or one block spread over
+    // 4/R threads... only R % 4 == 0 is supported.
+    static_assert(R % 4 == 0, "MN-contiguous loader needs 4 chunks per thread");
+#pragma unroll
+    for (int b = 0; b < R / 4; ++b) {
+      int blk = tid + b * NT;
+      int lane = blk & 63, grp = blk >> 6;
+      int k4 = lane & 15, mn8 = grp * 4 + (lane >> 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) reg[b * 4 + j] = src.chunk(k0 + k4 * 4 + j, mn0 + mn8 * 8);
+    }
+  }
+}
+
+// Registers -> LDS ([ROWS][LDK], K-contiguous).
+template <bool KC, int ROWS, int NT, int R>
+__device__ __forceinline__ void store_tile(uint16_t* lds, int tid, const uint4 (&reg)[R]) {
+  if constexpr (KC) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      int c = tid + i * NT;
+      *(uint4*)(lds + (c >> 3) * GEMM_LDK + (c & 7) * 8) = reg[i];
+    }
+  } else {
+#pragma unroll
+    for (int b = 0; b < R / 4; ++b) {
+      int blk = tid + b * NT;
+      int lane = blk & 63, grp = blk >> 6;
+      int k4 = lane & 15, mn8 = grp * 4 + (lane >> 4);
+      const uint4 r0 = reg[b * 4 + 0], r1 = reg[b * 4 + 1], r2 = reg[b * 4 + 2], r3 = reg[b * 4 + 3];
+      const uint32_t a0[4] = {r0.x, r0.y, r0.z, r0.w};
+      const uint32_t a1[4] = {r1.x, r1.y, r1.z, r1.w};
+      const uint32_t a2[4] = {r2.x, r2.y, r2.z, r2.w};
+      const uint32_t a3[4] = {r3.x, r3.y, r3.z, r3.w};
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        // mn = 2d: low halves of k = 0..3 ; mn = 2d+1: high halves
+        uint2 lo, hi;
+        lo.x = __builtin_amdgcn_perm(a1[d], a0[d], 0x05040100u);
+        lo.y = __builtin_amdgcn_perm(a3[d], a2[d], 0x05040100u);
+        hi.x = __builtin_amdgcn_perm(a1[d], a0[d], 0x07060302u);
+        hi.y = __builtin_amdgcn_perm(a3[d], a2[d], 0x07060302u);
+        *(uint2*)(lds + (mn8 * 8 + 2 * d) * GEMM_LDK + k4 * 4) = lo;
+        *(uint2*)(lds + (mn8 * 8 + 2 * d + 1) * GEMM_LDK + k4 * 4) = hi;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int& tm, int& tn) {
+  constexpr int GROUP_M = 8;
+  int64_t nb = (int64_t)gridDim.x;
+  int64_t bid = blockIdx.x;
+  if (nb % 8 == 0) bid = (bid % 8) * (nb / 8) + bid / 8;  // consecutive ids on one XCD
+  int64_t group = GROUP_M * tiles_n;
+  int64_t gid = bid / group;
+  int64_t first = gid * GROUP_M;
+  int64_t gsize = tiles_m - first < GROUP_M ? tiles_m - first : GROUP_M;
+  int64_t in = bid % group;
+  tm = (int)(first + in % gsize);
+  tn = (int)(in / gsize);
+}
+
+template <class T, class OutT, class SrcA, class SrcB, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_mfma_kernel(SrcA srcA, SrcB srcB, int64_t M, int64_t N, int64_t K, Epilogue ep) {
+  using TS = TileShape<BM, BN, WM, WN>;
+  constexpr int NT = TS::NT;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * TS::LDS_ELEMS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  int tm, tn;
+  tile_coords(ceil_div(M, BM), ceil_div(N, BN), tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+
+  int64_t kbeg = 0, kend = K;
+  if (ep.partial) {
+    kbeg = (int64_t)blockIdx.y * ep.k_per_split;
+    kend = kbeg + ep.k_per_split < K ? kbeg + ep.k_per_split : K;
+  }
+  const int nk = (int)ceil_div(kend - kbeg, GEMM_BK);
+
+  float4_t acc[TS::FM][TS::FN];
+#pragma unroll
+  for (int i = 0; i < TS::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TS::FN; ++j) acc[i][j] = (float4_t){0.f, 0.f, 0.f, 0.f};
+
+  uint4 ra[TS::RA], rb[TS::RB];
+  if (nk > 0) {
+    load_tile<SrcA, BM, NT>(srcA, m0, kbeg, tid, ra);
+    load_tile<SrcB, BN, NT>(srcB, n0, kbeg, tid, rb);
+    store_tile<SrcA::KC, BM, NT>(smem, tid, ra);
+    store_tile<SrcB::KC, BN, NT>(smem + BM * GEMM_LDK, tid, rb);
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int64_t kn = kbeg + (int64_t)(kt + 1) * GEMM_BK;
+      load_tile<SrcA, BM, NT>(srcA, m0, kn, tid, ra);
+      load_tile<SrcB, BN, NT>(srcB, n0, kn, tid, rb);
+    }
+    const uint16_t* As = smem + cur * TS::LDS_ELEMS;
+    const uint16_t* Bs = As + BM * GEMM_LDK;
+#pragma unroll
+    for (int kk = 0; kk < GEMM_BK / 32; ++kk) {
+      uint4 af[TS::FM], bf[TS::FN];
+      const int koff = kk * 32 + (lane >> 4) * 8;
+#pragma unroll
+      for (int i = 0; i < TS::FM; ++i)
+        af[i] = *(const uint4*)(As + (wm * TS::WTM + i * 16 + (lane & 15)) * GEMM_LDK + koff);
+#pragma unroll
+      for (int j = 0; j < TS::FN; ++j)
+        bf[j] = *(const uint4*)(Bs + (wn * TS::WTN + j * 16 + (lane & 15)) * GEMM_LDK + koff);
+#pragma unroll
+      for (int i = 0; i < TS::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < TS::FN; ++j) acc[i][j] = Mfma<T>::run(bf[j], af[i], acc[i][j]);
+    }
+    if (more) {
+      uint16_t* nxt = smem + (cur ^ 1) * TS::LDS_ELEMS;
+      store_tile<SrcA::KC, BM, NT>(nxt, tid, ra);
+      store_tile<SrcB::KC, BN, NT>(nxt + BM * GEMM_LDK, tid, rb);
+    }
+    __syncthreads();
+  }
+
+  // lane holds D[m0 + wm*WTM + i*16 + (lane & 15)][n0 + wn*WTN + j*16 + 4*(lane >> 4) + e]
+  const int64_t mb = m0 + wm * TS::WTM + (lane & 15);
+  const int64_t nb = n0 + wn * TS::WTN + 4 * (lane >> 4);
+  if (ep.partial) {
+    float* P = ep.partial + (int64_t)blockIdx.y * M * N;
+#pragma unroll
+    for (int i = 0; i < TS::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < TS::FN; ++j) {
+        const int64_t m = mb + i * 16, n = nb + j * 16;
+        if (m >= M) continue;
+        float* p = P + m * N + n;
+        if ((N & 3) == 0 && n + 4 <= N) {
+          *(float4*)p = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (n + e < N) p[e] = acc[i][j][e];
+        }
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < TS::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TS::FN; ++j)
+      epilogue_store4<T, OutT>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j]);
+}
+
+}  // namespace mdnn

@@ -1,0 +1,129 @@
+// Launch helpers of the GEMM engine, shared by the GEMM and convolution
+// entry points.  Tile selection is a fixed table keyed on the problem size.
+#pragma once
+
+#include "gemm_core.h"
+#include "internal.h"
+
+namespace mdnn {
+
+// fp32 path: 64x64 tiles, 256 threads, 4x4 outputs per thread, K step 16,
+// operands staged through LDS element by element (vector FMA; config-sized
+// fp32 problems are small and latency-bound).
+template <class SrcA, class SrcB>
+__global__ void __launch_bounds__(256)
+gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int tid = threadIdx.x;
+  const int tx = tid & 15, ty = tid >> 4;
+  const int64_t m0 = (int64_t)blockIdx.x * 64, n0 = (int64_t)blockIdx.y * 64;
+  int64_t kbeg = 0, kend = K;
+  if (ep.partial) {
+    kbeg = (int64_t)blockIdx.z * ep.k_per_split;
+    kend = kbeg + ep.k_per_split < K ? kbeg + ep.k_per_split : K;
+  }
+  float acc[4][4] = {};
+  for (int64_t k0 = kbeg; k0 < kend; k0 += 16) {
+    for (int idx = tid; idx < 64 * 16; idx += 256) {
+      int r, kk;
+      if (SrcA::KC) { r = idx >> 4; kk = idx & 15; } else { kk = idx >> 6; r = idx & 63; }
+      As[kk][r] = (k0 + kk < kend) ? a.elem(m0 + r, k0 + kk) : 0.0f;
+      if (SrcB::KC) { r = idx >> 4; kk = idx & 15; } else { kk = idx >> 6; r = idx & 63; }
+      Bs[kk][r] = (k0 + kk < kend) ? b.elem(n0 + r, k0 + kk) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { av[i] = As[kk][ty * 4 + i]; bv[i] = Bs[kk][tx * 4 + i]; }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  const int64_t n = n0 + tx * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = m0 + ty * 4 + i;
+    if (ep.partial) {
+      if (m < M) {
+        float* p = ep.partial + ((int64_t)blockIdx.z * M + m) * N + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (n + j < N) p[j] = acc[i][j];
+      }
+    } else {
+      epilogue_store4<F32, F32>(ep, M, N, m, n, (float4_t){acc[i][0], acc[i][1], acc[i][2], acc[i][3]});
+    }
+  }
+}
+
+// Tile configurations of the MFMA kernel.
+enum TileCfg { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2, TILE_64x64 = 3 };
+
+int gemm_tile_override();
+
+inline TileCfg choose_tile(int64_t M, int64_t N, int splits) {
+  int o = gemm_tile_override();
+  if (o >= TILE_256x256 && o <= TILE_64x64) return (TileCfg)o;
+  const int64_t t256 = ceil_div(M, 256) * ceil_div(N, 256) * splits;
+  if (t256 >= 256) return TILE_256x256;
+  const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128) * splits;
+  if (t128 >= 160) return TILE_128x128;
+  return TILE_64x64;
+}
+
+template <class T, class OutT, class SrcA, class SrcB, int BM, int BN, int WM, int WN>
+inline void launch_mfma(const SrcA& a, const SrcB& b, int64_t M, int64_t N, int64_t K,
+                        const Epilogue& ep, int splits, hipStream_t stream) {
+  dim3 grid((unsigned)(ceil_div(M, BM) * ceil_div(N, BN)), (unsigned)splits, 1);
+  hipLaunchKernelGGL((gemm_mfma_kernel<T, OutT, SrcA, SrcB, BM, BN, WM, WN>), grid,
+                     dim3(WM * WN * 64), 0, stream, a, b, M, N, K, ep);
+}
+
+// D (or split partials) = op(A) op(B) with the epilogue; T is F16 or BF16.
+template <class T, class OutT, class SrcA, class SrcB>
+inline mdnn_status_t run_gemm16(const SrcA& a, const SrcB& b, int64_t M, int64_t N, int64_t K,
+                                const Epilogue& ep, int splits, hipStream_t stream) {
+  if (ceil_div(M, 64) * ceil_div(N, 64) > 0x7fffffffLL || splits > 65535)
+    return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the launch grid");
+  switch (choose_tile(M, N, splits)) {
+    case TILE_256x256: launch_mfma<T, OutT, SrcA, SrcB, 256, 256, 2, 4>(a, b, M, N, K, ep, splits, stream); break;
+    case TILE_128x128: launch_mfma<T, OutT, SrcA, SrcB, 128, 128, 2, 2>(a, b, M, N, K, ep, splits, stream); break;
+    default:           launch_mfma<T, OutT, SrcA, SrcB, 64, 64, 1, 2>(a, b, M, N, K, ep, splits, stream); break;
+  }
+  return check_launch("gemm_mfma_kernel");
+}
+
+template <class SrcA, class SrcB>
+inline mdnn_status_t run_gemm32(const SrcA& a, const SrcB& b, int64_t M, int64_t N, int64_t K,
+                                const Epilogue& ep, int splits, hipStream_t stream) {
+  if (ceil_div(M, 64) > 0x7fffffffLL || ceil_div(N, 64) > 65535 || splits > 65535)
+    return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the fp32 launch grid");
+  dim3 grid((unsigned)ceil_div(M, 64), (unsigned)ceil_div(N, 64), (unsigned)splits);
+  hipLaunchKernelGGL((gemm_f32_kernel<SrcA, SrcB>), grid, dim3(256), 0, stream, a, b, M, N, K, ep);
+  return check_launch("gemm_f32_kernel");
+}
+
+// Number of K splits so that the grid fills the chip, each split a multiple
+// of the K step, and the partials stay within `max_ws` bytes.
+inline SplitPlan plan_splits(int64_t M, int64_t N, int64_t K, int64_t tiles, size_t max_ws) {
+  SplitPlan p{1, K};
+  const int64_t target = 512;
+  if (tiles >= target || K <= 2 * GEMM_BK) return p;
+  int64_t s = ceil_div(target, tiles);
+  int64_t max_s = K / (2 * GEMM_BK);
+  if (s > max_s) s = max_s;
+  while (s > 1 && (size_t)s * M * N * 4 > max_ws) --s;
+  if (s < 1) s = 1;
+  int64_t kps = ceil_div(ceil_div(K, s), GEMM_BK) * GEMM_BK;
+  p.splits = (int)ceil_div(K, kps);
+  p.k_per_split = kps;
+  return p;
+}
+
+}  // namespace mdnn

@@ -1,0 +1,50 @@
+// Host-side internals of libmdnn: error reporting, argument checks and the
+// launchers shared between translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "../../include/mdnn.h"
+
+namespace mdnn {
+
+mdnn_status_t fail(mdnn_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+mdnn_status_t check_launch(const char* what);
+
+inline size_t dtype_size(mdnn_dtype_t t) { return t == MDNN_F32 ? 4 : 2; }
+inline bool dtype_ok(int t) { return t == MDNN_F32 || t == MDNN_F16 || t == MDNN_BF16; }
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+inline hipStream_t as_stream(mdnn_stream_t s) { return (hipStream_t)s; }
+
+#define MDNN_TRY(expr)                          \
+  do {                                          \
+    mdnn_status_t st__ = (expr);                \
+    if (st__ != MDNN_SUCCESS) return st__;      \
+  } while (0)
+
+// Split-K GEMM used by the convolution backward-filter path: partial sums
+// are reduced by reduce_splits() in split order.
+struct SplitPlan {
+  int splits;
+  int64_t k_per_split;
+};
+
+// Sum `splits` fp32 [rows, cols] partial matrices in split order into
+// out[rows, cols] (fp32).
+mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int64_t cols,
+                            float* out, hipStream_t stream);
+// Zero `bytes` (a multiple of 4) with a fill kernel (no memset nodes, so the
+// caller may capture the stream into a graph).
+mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t stream);
+// Element-wise conversion between any two storage types (RNE when narrowing).
+mdnn_status_t cast_any(int64_t n, const void* src, mdnn_dtype_t s, void* dst, mdnn_dtype_t d,
+                       hipStream_t stream);
+// Deterministic column sums of a [rows, cols] matrix of type t into fp32.
+mdnn_status_t column_sums(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols,
+                          float* out, hipStream_t stream);
+
+}  // namespace mdnn

@@ -1,0 +1,305 @@
+// mdnn_train_step: one minibatch SGD step of a fixed layer chain.
+//
+// Section 2.1 (tensors, a graph of ops, backpropagation) and section 3.1
+// (minibatch SGD); storage types per section 3.2 (low-precision activations
+// and working weights, fp32 accumulation and master weights).  The chain is
+// fixed at creation; every op is enqueued on the caller's stream, nothing
+// synchronises with the host, and all device memory is caller-owned.
+//
+// Workspace layout (each piece 256-byte aligned):
+//   act[0]          low-precision copy of the input batch
+//   act[i+1]        stored output of layer i (fp32 for the last layer)
+//   argmax[i]       window index of each max-pool output
+//   grad0, grad1    ping-pong buffers for activation gradients (low precision)
+//   filter_ws       split-K partials of the convolution backward-filter
+#include <new>
+#include <vector>
+
+#include "internal.h"
+
+using namespace mdnn;
+
+struct LayerPlan {
+  mdnn_layer_t L;
+  int64_t w_off = 0, b_off = 0, nw = 0, nb = 0;
+  int64_t in_feat = 0, out_feat = 0;  // per sample
+  size_t out_off = 0;                 // act[i+1]
+  size_t arg_off = 0;                 // pool argmax
+  bool input_relu = false;            // input produced by a ReLU (directly or through pooling)
+  bool last = false;
+};
+
+struct mdnn_net {
+  std::vector<LayerPlan> layers;
+  int64_t batch = 0;
+  mdnn_train_cfg_t cfg{};
+  mdnn_dtype_t lp = MDNN_F32;
+  int64_t n_params = 0;
+  int64_t in_feat = 0;
+  size_t in_off = 0, g0_off = 0, g1_off = 0, fws_off = 0, fws_bytes = 0, ws_bytes = 0;
+  // bound memory
+  bool bound = false;
+  float* master = nullptr;
+  float* grads = nullptr;
+  float* mom = nullptr;
+  void* lowp = nullptr;
+  char* ws = nullptr;
+  mdnn_scaler_t* scaler = nullptr;
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static mdnn_conv_shape_t conv_shape(const mdnn_layer_t& L, int64_t batch) {
+  return mdnn_conv_shape_t{batch, L.h, L.w, L.c_in, L.c_out, L.r, L.s, L.pad};
+}
+
+extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_layers,
+                                         int64_t batch, const mdnn_train_cfg_t* cfg,
+                                         mdnn_net_t** out) {
+  if (!layers || !cfg || !out) return fail(MDNN_ERR_NULL, "net_create: NULL argument");
+  *out = nullptr;
+  if (n_layers < 1 || n_layers > 256) return fail(MDNN_ERR_SHAPE, "net_create: 1..256 layers");
+  if (batch < 1 || batch > (1 << 24)) return fail(MDNN_ERR_SHAPE, "net_create: bad batch");
+  if (!dtype_ok(cfg->dtype)) return fail(MDNN_ERR_DTYPE, "net_create: unknown dtype");
+  if (cfg->loss != MDNN_LOSS_XENT && cfg->loss != MDNN_LOSS_MSE)
+    return fail(MDNN_ERR_SHAPE, "net_create: unknown loss");
+
+  mdnn_net* net = new (std::nothrow) mdnn_net();
+  if (!net) return fail(MDNN_ERR_SHAPE, "net_create: out of host memory");
+  net->batch = batch;
+  net->cfg = *cfg;
+  net->lp = (mdnn_dtype_t)cfg->dtype;
+  const size_t lps = dtype_size(net->lp);
+
+  int64_t off = 0;
+  bool prev_relu = false;
+  // spatial output of the previous layer (h, w, c), or none
+  bool prev_spatial = false;
+  int64_t ph = 0, pw = 0, pc = 0, prev_out = -1;
+  for (int i = 0; i < n_layers; ++i) {
+    const mdnn_layer_t& L = layers[i];
+    LayerPlan p;
+    p.L = L;
+    p.last = i == n_layers - 1;
+    auto bad = [&](const char* why) {
+      delete net;
+      return fail(MDNN_ERR_SHAPE, "net_create: layer %d: %s", i, why);
+    };
+    if (L.act != MDNN_ACT_NONE && L.act != MDNN_ACT_RELU) return bad("unknown activation");
+    if (L.kind == MDNN_LAYER_FC) {
+      if (L.c_in < 1 || L.c_out < 1) return bad("FC sizes must be positive");
+      p.in_feat = L.c_in;
+      p.out_feat = L.c_out;
+      p.nw = L.c_in * L.c_out;
+      p.nb = L.c_out;
+      prev_spatial = false;
+    } else if (L.kind == MDNN_LAYER_CONV) {
+      if (L.c_in < 1 || L.c_out < 1 || L.h < 1 || L.w < 1 || L.r < 1 || L.s < 1 || L.pad < 0)
+        return bad("conv sizes must be positive");
+      if (2 * L.pad != L.r - 1 || 2 * L.pad != L.s - 1) return bad("conv must keep the size (2*pad == r-1 == s-1)");
+      if (prev_spatial && (ph != L.h || pw != L.w || pc != L.c_in)) return bad("conv input does not match");
+      p.in_feat = L.h * L.w * L.c_in;
+      p.out_feat = L.h * L.w * L.c_out;
+      p.nw = L.c_out * L.r * L.s * L.c_in;
+      p.nb = L.c_out;
+      prev_spatial = true;
+      ph = L.h; pw = L.w; pc = L.c_out;
+    } else if (L.kind == MDNN_LAYER_MAXPOOL2) {
+      if (L.c_in < 1 || L.h < 2 || L.w < 2 || (L.h & 1) || (L.w & 1)) return bad("maxpool needs even h, w >= 2");
+      if (prev_spatial && (ph != L.h || pw != L.w || pc != L.c_in)) return bad("maxpool input does not match");
+      if (p.last) return bad("the last layer must be FC or CONV");
+      p.in_feat = L.h * L.w * L.c_in;
+      p.out_feat = (L.h / 2) * (L.w / 2) * L.c_in;
+      prev_spatial = true;
+      ph = L.h / 2; pw = L.w / 2; pc = L.c_in;
+    } else {
+      return bad("unknown kind");
+    }
+    if (prev_out >= 0 && prev_out != p.in_feat) return bad("input size does not match the previous output");
+    if (p.last && L.act != MDNN_ACT_NONE) return bad("the last layer has no activation");
+    p.w_off = off;
+    p.b_off = off + p.nw;
+    off += p.nw + p.nb;
+    p.input_relu = prev_relu;
+    if (L.kind != MDNN_LAYER_MAXPOOL2) prev_relu = L.act == MDNN_ACT_RELU;
+    prev_out = p.out_feat;
+    net->layers.push_back(p);
+  }
+  net->n_params = off;
+  net->in_feat = net->layers[0].in_feat;
+  const LayerPlan& last = net->layers.back();
+  if (cfg->loss == MDNN_LOSS_XENT && (last.out_feat != cfg->n_classes || cfg->n_classes > 1024)) {
+    delete net;
+    return fail(MDNN_ERR_SHAPE, "net_create: n_classes must equal the last layer's outputs (<= 1024)");
+  }
+
+  // workspace plan
+  size_t w = 0;
+  net->in_off = w;
+  w = align256(w + (size_t)batch * net->in_feat * lps);
+  int64_t max_feat = net->in_feat;
+  size_t fws = 0;
+  for (auto& p : net->layers) {
+    p.out_off = w;
+    w = align256(w + (size_t)batch * p.out_feat * (p.last ? 4 : lps));
+    if (p.L.kind == MDNN_LAYER_MAXPOOL2) {
+      p.arg_off = w;
+      w = align256(w + (size_t)batch * p.out_feat);
+    }
+    if (p.L.kind == MDNN_LAYER_CONV) {
+      mdnn_conv_shape_t cs = conv_shape(p.L, batch);
+      size_t need = mdnn_conv2d_bwd_filter_workspace(&cs, net->lp);
+      if (need > fws) fws = need;
+    }
+    if (p.in_feat > max_feat) max_feat = p.in_feat;
+    if (p.out_feat > max_feat) max_feat = p.out_feat;
+  }
+  net->g0_off = w;
+  w = align256(w + (size_t)batch * max_feat * lps);
+  net->g1_off = w;
+  w = align256(w + (size_t)batch * max_feat * lps);
+  net->fws_off = w;
+  net->fws_bytes = fws;
+  w = align256(w + fws);
+  net->ws_bytes = w;
+  clear_error();
+  *out = net;
+  return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_net_sizes(const mdnn_net_t* net, int64_t* n_params,
+                                        size_t* workspace_bytes) {
+  if (!net) return fail(MDNN_ERR_NULL, "net_sizes: NULL net");
+  if (n_params) *n_params = net->n_params;
+  if (workspace_bytes) *workspace_bytes = net->ws_bytes;
+  return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* grads,
+                                       float* momentum, void* lowp_w, void* workspace,
+                                       size_t workspace_bytes, mdnn_scaler_t* scaler) {
+  if (!net) return fail(MDNN_ERR_NULL, "net_bind: NULL net");
+  if (!master_w || !grads || !workspace) return fail(MDNN_ERR_NULL, "net_bind: master_w, grads and workspace are required");
+  if (net->cfg.momentum != 0.0f && !momentum) return fail(MDNN_ERR_NULL, "net_bind: momentum buffer required");
+  if (net->lp != MDNN_F32 && !lowp_w) return fail(MDNN_ERR_NULL, "net_bind: lowp_w required for a low-precision net");
+  if (net->cfg.loss_scaling && !scaler) return fail(MDNN_ERR_NULL, "net_bind: scaler required with loss scaling");
+  if (workspace_bytes < net->ws_bytes) return fail(MDNN_ERR_WORKSPACE, "net_bind: workspace needs %zu bytes", net->ws_bytes);
+  if (!aligned(workspace, 256) || !aligned(master_w, 16) || !aligned(grads, 16) ||
+      (momentum && !aligned(momentum, 4)) || (lowp_w && !aligned(lowp_w, 16)) || (scaler && !aligned(scaler, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "net_bind: workspace must be 256-byte and parameter buffers 16-byte aligned");
+  net->master = master_w;
+  net->grads = grads;
+  net->mom = net->cfg.momentum != 0.0f ? momentum : nullptr;
+  net->lowp = net->lp == MDNN_F32 ? nullptr : lowp_w;
+  net->ws = (char*)workspace;
+  net->scaler = net->cfg.loss_scaling ? scaler : nullptr;
+  net->bound = true;
+  clear_error();
+  return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream) {
+  if (!net) return fail(MDNN_ERR_NULL, "net_sync_lowp: NULL net");
+  if (!net->bound) return fail(MDNN_ERR_STATE, "net_sync_lowp: net not bound");
+  if (!net->lowp) return MDNN_SUCCESS;
+  return mdnn_cast(net->n_params, net->master, MDNN_F32, net->lowp, net->lp, stream);
+}
+
+extern "C" const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i) {
+  if (!net || !net->bound || i < 0 || i > (int32_t)net->layers.size()) return nullptr;
+  if (i == 0) return net->ws + net->in_off;
+  return net->ws + net->layers[i - 1].out_off;
+}
+
+extern "C" void mdnn_net_destroy(mdnn_net_t* net) { delete net; }
+
+extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
+                                         float* loss_out, mdnn_stream_t stream) {
+  if (!net) return fail(MDNN_ERR_NULL, "train_step: NULL net");
+  if (!net->bound) return fail(MDNN_ERR_STATE, "train_step: net not bound");
+  if (!x || !target || !loss_out) return fail(MDNN_ERR_NULL, "train_step: x, target and loss_out are required");
+  if (!aligned(x, 4) || !aligned(target, 4) || !aligned(loss_out, 4))
+    return fail(MDNN_ERR_MISALIGNED, "train_step: misaligned buffer");
+  const int64_t B = net->batch;
+  const mdnn_dtype_t lp = net->lp;
+  char* ws = net->ws;
+  const void* wlp = net->lowp ? net->lowp : (const void*)net->master;
+  const size_t lps = dtype_size(lp);
+  const float* scale = net->scaler ? &net->scaler->scale : nullptr;
+  auto act_ptr = [&](size_t i) -> char* {
+    return i == 0 ? ws + net->in_off : ws + net->layers[i - 1].out_off;
+  };
+  auto wptr = [&](const LayerPlan& p) { return (const char*)wlp + p.w_off * lps; };
+
+  // a1: input batch to the storage type
+  MDNN_TRY(mdnn_cast(B * net->in_feat, x, MDNN_F32, act_ptr(0), lp, stream));
+
+  // forward
+  for (size_t i = 0; i < net->layers.size(); ++i) {
+    const LayerPlan& p = net->layers[i];
+    const mdnn_dtype_t out_t = p.last ? MDNN_F32 : lp;
+    const float* bias = net->master + p.b_off;
+    const mdnn_act_t act = (mdnn_act_t)p.L.act;
+    if (p.L.kind == MDNN_LAYER_FC) {
+      MDNN_TRY(mdnn_gemm_mixed(MDNN_NN, B, p.L.c_out, p.L.c_in, 1.0f, act_ptr(i), p.L.c_in, wptr(p),
+                               p.L.c_out, lp, 0.0f, nullptr, 0, act_ptr(i + 1), p.L.c_out, out_t, bias,
+                               act, nullptr, 0, stream));
+    } else if (p.L.kind == MDNN_LAYER_CONV) {
+      mdnn_conv_shape_t cs = conv_shape(p.L, B);
+      MDNN_TRY(mdnn_conv2d_fwd(&cs, act_ptr(i), wptr(p), lp, bias, act, act_ptr(i + 1), out_t, stream));
+    } else {
+      MDNN_TRY(mdnn_maxpool2_fwd(B, p.L.h, p.L.w, p.L.c_in, act_ptr(i), act_ptr(i + 1),
+                                 (uint8_t*)(ws + p.arg_off), lp, stream));
+    }
+  }
+
+  // loss and its gradient (scaled by the loss scale), into grad0
+  char* gcur = ws + net->g0_off;
+  char* gnxt = ws + net->g1_off;
+  const LayerPlan& last = net->layers.back();
+  const float* out = (const float*)act_ptr(net->layers.size());
+  if (net->cfg.loss == MDNN_LOSS_XENT) {
+    MDNN_TRY(mdnn_softmax_xent(B, last.out_feat, out, last.out_feat, (const int32_t*)target, scale,
+                               loss_out, gcur, last.out_feat, lp, stream));
+  } else {
+    MDNN_TRY(mdnn_mse_loss(B, last.out_feat, out, (const float*)target, scale, loss_out, gcur, lp,
+                           stream));
+  }
+
+  // backward
+  for (size_t ii = net->layers.size(); ii-- > 0;) {
+    const LayerPlan& p = net->layers[ii];
+    const char* a_in = act_ptr(ii);
+    float* gw = net->grads + p.w_off;
+    float* gb = net->grads + p.b_off;
+    const void* mask = p.input_relu ? (const void*)a_in : nullptr;
+    if (p.L.kind == MDNN_LAYER_FC) {
+      const int64_t in = p.L.c_in, o = p.L.c_out;
+      // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
+      MDNN_TRY(mdnn_gemm_mixed(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o,
+                               MDNN_F32, nullptr, MDNN_ACT_NONE, nullptr, 0, stream));
+      MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, stream));
+      if (ii > 0) {
+        // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
+        MDNN_TRY(mdnn_gemm_mixed(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0,
+                                 gnxt, in, lp, nullptr, MDNN_ACT_NONE, mask, in, stream));
+      }
+    } else if (p.L.kind == MDNN_LAYER_CONV) {
+      mdnn_conv_shape_t cs = conv_shape(p.L, B);
+      MDNN_TRY(mdnn_conv2d_bwd_filter(&cs, a_in, gcur, lp, gw, gb, ws + net->fws_off, net->fws_bytes,
+                                      stream));
+      if (ii > 0)
+        MDNN_TRY(mdnn_conv2d_bwd_data(&cs, gcur, wptr(p), lp, mask, gnxt, lp, stream));
+    } else {
+      MDNN_TRY(mdnn_maxpool2_bwd(B, p.L.h, p.L.w, p.L.c_in, gcur, (const uint8_t*)(ws + p.arg_off),
+                                 gnxt, lp, stream));
+    }
+    char* t = gcur;
+    gcur = gnxt;
+    gnxt = t;
+  }
+
+  // update (and the low-precision working copy)
+  return mdnn_sgd_update(net->n_params, net->master, net->grads, net->mom, net->lowp, lp,
+                         net->cfg.lr, net->cfg.momentum, net->scaler, stream);
+}
