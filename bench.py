@@ -1,0 +1,320 @@
+"""Benchmark of the MI355X SGD-step hot path.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--quick] [--no-cpu]
+
+Headline workload: one SGD step of the wide regression MLP (batch 4096,
+1024 -> 4 x 4096 ReLU -> 1, MSE, fp16 storage, fp32 accumulation and master
+weights, dynamic loss scaling, momentum 0.9): forward, loss, backward and
+update of one minibatch of synthetic inputs already resident in HBM.  `value`
+is train samples per second.
+
+Also on the same JSON line:
+  roofline      the step's dominant kernel: its average launch duration from
+                HIP events over a replay of exactly its launches in the step
+                (same shapes and buffers), against the fp16 MFMA peak;
+  cpu_baseline  the fp64 oracle's step on this host on one full batch;
+  gemm_sweep    the fp16 GEMM sweep (M = N = K in 1024/4096/8192, NN/NT/TN);
+  conv          the ResNet-style 3x3 layers (batch 128) fwd / bwd-data /
+                bwd-filter;
+  workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step.
+Only one GPU is used; --gpus > 1 exits with a message.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "train samples/sec per step; mixed-precision GEMM/conv TFLOP/s (% MFMA peak)"
+PEAK_F16_TFLOPS = 2516.6   # MI355X dense fp16/bf16 MFMA (256 CU x 4096 FLOP/clk x 2.4 GHz)
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+class _Timer:
+    """HIP events on torch's current stream (the stream every call uses)."""
+
+    def __init__(self):
+        import torch
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def __enter__(self):
+        _sync()
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        _sync()
+        self.ms = self.a.elapsed_time(self.b)
+
+
+def _train_setup(mdnn, cfg, n_batches=10):
+    import torch
+    import workloads as W
+    net = mdnn.Net(cfg.layers, cfg.batch, {"f32": 0, "f16": 1, "bf16": 2}[cfg.dtype], cfg.loss,
+                   cfg.lr, cfg.momentum, cfg.loss_scaling, cfg.init_scale, cfg.n_classes)
+    net.set_params(W.init_params(cfg))
+    xs, ts = [], []
+    for s in range(n_batches):
+        x, t = W.batch_inputs(cfg, s)
+        xs.append(torch.from_numpy(x).cuda())
+        ts.append(torch.from_numpy(t).cuda())
+    _sync()
+    return net, xs, ts
+
+
+def _time_steps(net, xs, ts, steps, warmup):
+    for i in range(warmup):
+        net.step(xs[i % len(xs)], ts[i % len(ts)])
+    with _Timer() as tm:
+        for i in range(steps):
+            net.step(xs[i % len(xs)], ts[i % len(ts)])
+    return tm.ms / steps
+
+
+def _step_gemms(cfg):
+    """Every GEMM one step of an FC chain issues, as (layout, M, N, K, out)."""
+    import workloads as W
+    out, B = [], cfg.batch
+    n = len(cfg.layers)
+    for i, l in enumerate(cfg.layers):
+        if l.kind != W.FC:
+            continue
+        out.append(("NN", B, l.c_out, l.c_in, "f32" if i == n - 1 else cfg.dtype, i))
+        out.append(("TN", l.c_in, l.c_out, B, "f32", i))
+        if i > 0:
+            out.append(("NT", B, l.c_in, l.c_out, cfg.dtype, i))
+    return out
+
+
+def _tile(m: int, n: int) -> str:
+    """The GEMM engine's automatic tile choice (a fixed table keyed on M, N)."""
+    cd = lambda a, b: -(-a // b)  # noqa: E731
+    if cd(m, 256) * cd(n, 256) >= 256:
+        return "256x256"
+    if cd(m, 128) * cd(n, 128) >= 160:
+        return "128x128"
+    return "64x64"
+
+
+def _replay_group(mdnn, net, cfg, group, reps):
+    """Replay the launches of one kernel instantiation exactly as the step
+    issues them (same shapes, leading dimensions, epilogues and buffers);
+    returns (mean ms per launch, mean FLOP per launch)."""
+    import torch
+    lp = {"f32": 0, "f16": 1, "bf16": 2}[cfg.dtype]
+    es = 2 if lp else 4
+    offs = cfg.param_offsets()
+    wbase = net.lowp.data_ptr() if net.lowp is not None else net.master.data_ptr()
+    widest = max([cfg.in_features] + [l.c_out for l in cfg.layers])
+    # stand-ins for the step's activation-gradient buffers (same shapes)
+    g0 = torch.empty((cfg.batch, widest), dtype=torch.float16, device="cuda").normal_(0, 1e-2)
+    g1 = torch.empty_like(g0)
+    calls = []
+    for (layout, M, N, K, out_t, i) in group:
+        l = cfg.layers[i]
+        a_in = net.activation_ptr(i)
+        a_out = net.activation_ptr(i + 1)
+        wptr = wbase + offs[i][0] * es
+        bias = net.master.data_ptr() + offs[i][1] * 4
+        if layout == "NN":
+            calls.append((0, M, N, K, a_in, K, wptr, N, a_out, N, 0 if out_t == "f32" else lp,
+                          bias, l.act, None, 0))
+        elif layout == "TN":
+            calls.append((2, M, N, K, a_in, M, g0.data_ptr(), N, net.grads.data_ptr() + offs[i][0] * 4,
+                          N, 0, None, 0, None, 0))
+        else:
+            calls.append((1, M, N, K, g0.data_ptr(), K, wptr, K, g1.data_ptr(), N, lp, None, 0,
+                          a_in, N))
+    flops = sum(2.0 * c[1] * c[2] * c[3] for c in calls) / len(calls)
+    for c in calls:  # warm
+        mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0, None, 0,
+                             c[8], c[9], c[10], c[11], c[12], c[13], c[14])
+    with _Timer() as tm:
+        for _ in range(reps):
+            for c in calls:
+                mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
+                                     None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
+    return tm.ms / (reps * len(calls)), flops
+
+
+def _gemm_sweep(mdnn, reps_scale=1.0):
+    import torch
+    import workloads as W
+    res = {}
+    for size in W.GEMM_SIZES:
+        for layout in W.GEMM_LAYOUTS:
+            a, b = W.gemm_operands(layout, size, size, size)
+            A, B = torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()
+            D = torch.empty((size, size), dtype=torch.float32, device="cuda")
+            lay = {"NN": 0, "NT": 1, "TN": 2}[layout]
+
+            def run():
+                mdnn.mdnn_gemm_mixed(lay, size, size, size, 1.0, A, A.stride(0), B, B.stride(0), 1,
+                                     0.0, None, 0, D, size, 0)
+            for _ in range(3):
+                run()
+            reps = max(5, int(reps_scale * {1024: 200, 4096: 40, 8192: 10}[size]))
+            with _Timer() as tm:
+                for _ in range(reps):
+                    run()
+            ms = tm.ms / reps
+            tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
+            res[f"{layout}_{size}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
+                                       "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
+            del A, B, D
+    return res
+
+
+def _conv_bench(mdnn, reps=20):
+    import torch
+    import workloads as W
+    res = {}
+    for li, sh in enumerate(W.RESNET_LAYERS):
+        x, w, dy = W.conv_operands(sh)
+        X, Wt, DY = (torch.from_numpy(v).cuda() for v in (x, w, dy))
+        cs = mdnn.ConvShape(sh.n, sh.h, sh.w, sh.c_in, sh.c_out, sh.r, sh.s, sh.pad)
+        y = torch.empty(dy.shape, dtype=torch.float16, device="cuda")
+        dx = torch.empty(x.shape, dtype=torch.float16, device="cuda")
+        dw = torch.empty(w.shape, dtype=torch.float32, device="cuda")
+        wsb = mdnn.mdnn_conv2d_bwd_filter_workspace(cs, 1)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        fns = {
+            "fwd": lambda: mdnn.mdnn_conv2d_fwd(cs, X, Wt, 1, None, 0, y, 1),
+            "bwd_data": lambda: mdnn.mdnn_conv2d_bwd_data(cs, DY, Wt, 1, None, dx, 1),
+            "bwd_filter": lambda: mdnn.mdnn_conv2d_bwd_filter(cs, X, DY, 1, dw, None, ws, wsb),
+        }
+        for op, fn in fns.items():
+            for _ in range(3):
+                fn()
+            with _Timer() as tm:
+                for _ in range(reps):
+                    fn()
+            ms = tm.ms / reps
+            tf = sh.flops() / (ms * 1e-3) / 1e12
+            res[f"L{li + 1}_{sh.c_in}x{sh.h}_{op}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
+                                                       "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
+    return res
+
+
+def _cpu_baseline(cfg):
+    """The fp64 oracle's step on one full batch of the headline workload."""
+    import numpy as np
+    import workloads as W
+    from oracle import train
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    orc = train.from_config(cfg, W.init_params(cfg))
+    x, t = W.batch_inputs(cfg, 0)
+    t0 = time.perf_counter()
+    orc.step(x, t)
+    dt = time.perf_counter() - t0
+    del np
+    return {"value": round(cfg.batch / dt, 2), "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"one full SGD step (batch {cfg.batch}) of {cfg.name} in fp64 numpy, "
+                      f"{dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--quick", action="store_true", help="headline only (no sub-benchmarks)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (no collectives); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2011_11188_amd as mdnn
+    import workloads as W
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+
+    cfg = W.wide_mlp_fp16()
+    net, xs, ts = _train_setup(mdnn, cfg)
+    ms = _time_steps(net, xs, ts, args.steps, args.warmup)
+    samples = cfg.batch / (ms * 1e-3)
+    step_tf = cfg.flops_per_step() / (ms * 1e-3) / 1e12
+    print(f"[bench] {cfg.name}: {ms:.3f} ms/step, {samples:.0f} samples/s, "
+          f"{step_tf:.1f} TFLOP/s", file=sys.stderr, flush=True)
+
+    # dominant kernel: the kernel instantiation (layout, output type, tile)
+    # whose launches in the step take the most time
+    gemms = _step_gemms(cfg)
+    groups = {}
+    for g in gemms:
+        groups.setdefault((g[0], g[4], _tile(g[1], g[2])), []).append(g)
+    best = None
+    for key, grp in groups.items():
+        mpl, fpl = _replay_group(mdnn, net, cfg, grp, reps=max(5, args.steps // 2))
+        total = mpl * len(grp)
+        if best is None or total > best[0]:
+            best = (total, key, mpl, fpl, len(grp))
+    _, key, mpl, fpl, nl = best
+    achieved = fpl / (mpl * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_F16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_F16_TFLOPS, 4), "traffic": None,
+                "kernel": f"gemm_mfma_kernel {key[0]} f16 -> {key[1]}, tile {key[2]}, "
+                          f"{nl} launches per step",
+                "avg_launch_ms": round(mpl, 4), "flop_per_launch": fpl}
+    print(f"[bench] dominant kernel {roofline['kernel']}: {mpl:.4f} ms/launch, "
+          f"{achieved:.1f} TFLOP/s", file=sys.stderr, flush=True)
+
+    line = {
+        "metric": METRIC, "value": round(samples, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic (seeded N(0,1) inputs and targets, He-normal weights)",
+        "config": {"workload": f"{cfg.name}: wide regression MLP 1024->4x4096(ReLU)->1, MSE, "
+                               "fp16 storage, fp32 accumulate + master weights, dynamic loss "
+                               "scaling (2^16), SGD momentum 0.9, lr 1e-3",
+                   "global_batch": cfg.batch, "parallelism": "single GPU",
+                   "step_tflops": round(step_tf, 1),
+                   "step_mfma_frac": round(step_tf / PEAK_F16_TFLOPS, 4),
+                   "flop_per_step": cfg.flops_per_step()},
+        "roofline": roofline,
+    }
+    if not args.quick:
+        line["gemm_sweep"] = _gemm_sweep(mdnn)
+        print("[bench] gemm sweep done", file=sys.stderr, flush=True)
+        line["conv"] = _conv_bench(mdnn)
+        print("[bench] conv done", file=sys.stderr, flush=True)
+        wl = {}
+        for c in (W.lenet_bf16(), W.mlp784_fp32()):
+            n2, xs2, ts2 = _train_setup(mdnn, c)
+            m2 = _time_steps(n2, xs2, ts2, 50, 5)
+            wl[c.name] = {"ms_per_step": round(m2, 4), "samples_per_s": round(c.batch / (m2 * 1e-3), 1),
+                          "tflops": round(c.flops_per_step() / (m2 * 1e-3) / 1e12, 2)}
+            n2.close()
+        line["workloads"] = wl
+        print("[bench] workloads done", file=sys.stderr, flush=True)
+    if not args.no_cpu:
+        line["cpu_baseline"] = _cpu_baseline(cfg)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

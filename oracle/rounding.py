@@ -5,9 +5,16 @@ IEEE half precision (fp16: 11 significand bits, exponents -14..15) and
 bfloat16 (8 significand bits with fp32's exponent range -126..127, so that
 converting fp32 data to it cannot overflow or underflow for lack of range).
 
-``round_to(x, fmt)`` returns the fp64 value of the nearest ``fmt`` number,
-ties to even, with gradual underflow (subnormals kept), overflow to +-inf and
-NaN kept NaN.  It rounds *directly* from fp64 (one rounding).
+``round_generic(x, fmt)`` is the definition: the nearest ``fmt`` number, ties
+to even, with gradual underflow (subnormals kept), overflow to +-inf and NaN
+kept NaN, rounded *directly* from fp64 (one rounding).
+
+``round_to(x, fmt)`` computes the same function faster: numpy's IEEE
+conversions for fp16 and fp32 (library routines), and for bfloat16 the
+round-half-even rule applied to the fp64 bit pattern (add half an ulp minus
+one plus the kept lowest bit, then truncate) wherever the result is a normal
+number, the definition elsewhere.  Tests pin both against each other and
+against numpy / torch conversions.
 
 Test infrastructure only (see the package header).
 """
@@ -29,8 +36,8 @@ def max_finite(fmt: str) -> float:
     return (2.0 - 2.0 ** (1 - p)) * 2.0 ** emax
 
 
-def round_to(x, fmt: str) -> np.ndarray:
-    """Nearest ``fmt`` value of each fp64 element, ties to even."""
+def round_generic(x, fmt: str) -> np.ndarray:
+    """Nearest ``fmt`` value of each fp64 element, ties to even (definition)."""
     x = np.asarray(x, dtype=np.float64)
     if fmt == "f64":
         return x.copy()
@@ -45,6 +52,40 @@ def round_to(x, fmt: str) -> np.ndarray:
     r = np.where(r > max_finite(fmt), np.inf, r)
     out[sel] = np.copysign(r, x[sel])
     return out
+
+
+_BF16_DROP = 52 - 7                   # fp64 fraction bits below bfloat16's 7
+_BF16_MIN_NORMAL = 2.0 ** -126
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    u = x.view(np.uint64)
+    lsb = (u >> np.uint64(_BF16_DROP)) & np.uint64(1)
+    r = (u + (np.uint64((1 << (_BF16_DROP - 1)) - 1) + lsb)) & \
+        ~np.uint64((1 << _BF16_DROP) - 1)
+    out = r.view(np.float64)
+    ax = np.abs(x)
+    out = np.where(np.abs(out) > max_finite("bf16"), np.copysign(np.inf, x), out)
+    out = np.where(np.isnan(x), x, out)
+    small = (ax < _BF16_MIN_NORMAL) & (ax != 0.0)
+    if np.any(small):
+        out[small] = round_generic(x[small], "bf16")
+    return out
+
+
+def round_to(x, fmt: str) -> np.ndarray:
+    """Nearest ``fmt`` value of each fp64 element, ties to even."""
+    x = np.asarray(x, dtype=np.float64)
+    if fmt == "f64":
+        return x.copy()
+    with np.errstate(over="ignore", invalid="ignore"):
+        if fmt == "f32":
+            return x.astype(np.float32).astype(np.float64)
+        if fmt == "f16":
+            return x.astype(np.float16).astype(np.float64)
+    if fmt == "bf16":
+        return _round_bf16(np.ascontiguousarray(x))
+    raise ValueError(fmt)
 
 
 def decode(a: np.ndarray, fmt: str) -> np.ndarray:

@@ -103,9 +103,9 @@ class OracleNet:
         return w, self.w32[bo:bo + nb]
 
     # -- forward / backward -------------------------------------------------
-    def forward(self, x: np.ndarray):
+    def forward(self, x: np.ndarray, wl: Optional[np.ndarray] = None):
         """Returns (stored activations a_0..a_L, pool argmaxes, output)."""
-        wl = self.w_lp()
+        wl = self.w_lp() if wl is None else wl
         b = self.batch
         a = self.R(np.asarray(x, np.float64).reshape(b, -1))
         acts, args = [a], {}
@@ -136,9 +136,9 @@ class OracleNet:
             loss, dz = ops.mse_loss(out, np.asarray(target, np.float64).reshape(out.shape), scale)
         return loss, self.R(dz)
 
-    def backward(self, acts, args, dz: np.ndarray) -> np.ndarray:
+    def backward(self, acts, args, dz: np.ndarray, wl: Optional[np.ndarray] = None) -> np.ndarray:
         """Gradient of the loss (times the loss scale) w.r.t. the flat params."""
-        wl = self.w_lp()
+        wl = self.w_lp() if wl is None else wl
         b = self.batch
         g = np.zeros(self.n_params)
         for i in range(len(self.layers) - 1, -1, -1):
@@ -175,10 +175,11 @@ class OracleNet:
 
     def step(self, x: np.ndarray, target: np.ndarray) -> float:
         """One SGD step; returns the (unscaled) loss of the forward pass."""
-        acts, args, out = self.forward(x)
+        wl = self.w_lp()
+        acts, args, out = self.forward(x, wl)
         s = 1.0 if self.scaler is None else self.scaler["scale"]
         loss, dz = self.loss_and_grad(out, target, s)
-        g = self.backward(acts, args, dz)
+        g = self.backward(acts, args, dz, wl)
         w, v, sc, _ = ops.sgd_update(self.w32, g, self.v32, self.lr, self.momentum, self.scaler)
         self.w32 = self.R32(w)
         self.v32 = None if v is None else self.R32(v)

@@ -1,0 +1,147 @@
+"""CPU checks of the C ABI boundary: the library loads, exports every entry
+point include/mdnn.h declares, and rejects bad arguments on the host (every
+case below fails validation before any GPU work, so it runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mdnn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mdnn_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def m():
+    import paper_2011_11188_amd as mdnn
+    return mdnn
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ["mdnn_gemm_mixed", "mdnn_conv2d_fwd", "mdnn_conv2d_bwd_data", "mdnn_conv2d_bwd_filter",
+              "mdnn_bias_act_fwd", "mdnn_bias_act_bwd", "mdnn_softmax_xent", "mdnn_sgd_update",
+              "mdnn_train_step", "mdnn_cast", "mdnn_mse_loss", "mdnn_maxpool2_fwd"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(m):
+    lib = ctypes.CDLL(m.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(m.exported_symbols()) == _declared()
+
+
+def test_binding_has_same_names(m):
+    for n in _declared():
+        if n in ("mdnn_last_error", "mdnn_version"):
+            continue
+        assert callable(getattr(m, n)), n
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+@pytest.mark.parametrize("args,status", [
+    # layout, M, N, K, alpha, A, lda, B, ldb, ab, beta, C, ldc, D, ldd, d
+    ((7, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 3),     # bad layout
+    ((0, -1, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 2),    # negative M
+    ((0, 4, 4, 4, 1.0, None, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 1),     # A NULL
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, None, 4, 0), 1),     # D NULL
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 1.0, None, 0, FAKE, 4, 0), 1),     # beta without C
+    ((0, 4, 4, 8, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 3),     # lda < K
+    ((1, 4, 4, 8, 1.0, FAKE, 8, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 3),     # NT: ldb < K
+    ((2, 8, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 3),     # TN: lda < M
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 2, 0), 3),     # ldd < N
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 2), 4),     # f16 in, bf16 out
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 0, 0.0, None, 0, FAKE, 4, 1), 4),     # f32 in, f16 out
+    ((0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 9, 0.0, None, 0, FAKE, 4, 0), 4),     # unknown dtype
+    ((0, 4, 4, 4, 1.0, FAKE + 1, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0), 5),  # odd A address
+])
+def test_gemm_rejects_bad_arguments(m, args, status):
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_gemm_mixed(*args, stream=0)
+    assert e.value.status == status
+    assert m.last_error()
+
+
+def test_conv_rejects_bad_arguments(m):
+    sh = m.ConvShape(2, 5, 5, 8, 8, 3, 3, 1)
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_conv2d_fwd(sh, None, FAKE, 1, None, 0, FAKE, 1, stream=0)
+    assert e.value.status == m.ERR_NULL
+    bad = m.ConvShape(2, 2, 2, 8, 8, 7, 7, 0)              # empty output
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_conv2d_fwd(bad, FAKE, FAKE, 1, None, 0, FAKE, 1, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    big = m.ConvShape(256, 28, 28, 32, 32, 5, 5, 2)
+    need = m.mdnn_conv2d_bwd_filter_workspace(big, 2)
+    assert need > 0
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_conv2d_bwd_filter(big, FAKE, FAKE, 2, FAKE, None, FAKE, need - 4, stream=0)
+    assert e.value.status == m.ERR_WORKSPACE
+    assert m.mdnn_conv2d_bwd_filter_workspace(bad, 1) == 0
+
+
+def test_other_entry_points_reject_bad_arguments(m):
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_cast(-1, FAKE, 0, FAKE, 1, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_softmax_xent(4, 2000, FAKE, 2000, FAKE, None, FAKE, FAKE, 2000, 0, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_softmax_xent(4, 10, FAKE, 8, FAKE, None, FAKE, FAKE, 10, 0, stream=0)
+    assert e.value.status == m.ERR_LAYOUT
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_sgd_update(10, FAKE + 4, FAKE, None, None, 0, 0.1, 0.0, None, stream=0)
+    assert e.value.status == m.ERR_MISALIGNED
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_bias_act_bwd(4, 4, FAKE, None, 1, None, FAKE, 1, stream=0)   # ReLU needs y
+    assert e.value.status == m.ERR_NULL
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_maxpool2_bwd(1, 4, 4, 2, None, None, FAKE, 1, stream=0)
+    assert e.value.status == m.ERR_NULL
+
+
+def test_net_create_validates_the_chain(m):
+    import workloads as W
+    L = m.LayerDesc
+    cfg = m.TrainCfg(m.BF16, m.LOSS_XENT, 0.01, 0.0, 0, 10)
+    good = [L(m.LAYER_CONV, 1, 1, 28, 28, 32, 5, 5, 2), L(m.LAYER_MAXPOOL2, 0, 32, 28, 28, 32, 0, 0, 0),
+            L(m.LAYER_FC, 1, 14 * 14 * 32, 1, 1, 64, 0, 0, 0), L(m.LAYER_FC, 0, 64, 1, 1, 10, 0, 0, 0)]
+    h = m.mdnn_net_create(good, 8, cfg)
+    n, ws = m.mdnn_net_sizes(h)
+    assert n == 32 * 25 + 32 + 6272 * 64 + 64 + 640 + 10 and ws > 0
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_net_bind(h, FAKE, FAKE, None, None, FAKE, ws, None)       # bf16 net needs lowp_w
+    assert e.value.status == m.ERR_NULL
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_train_step(h, FAKE, FAKE, FAKE, stream=0)                 # not bound
+    assert e.value.status == m.ERR_STATE
+    m.mdnn_net_destroy(h)
+    bad = list(good)
+    bad[2] = L(m.LAYER_FC, 1, 100, 1, 1, 64, 0, 0, 0)                     # size mismatch
+    with pytest.raises(m.MdnnError):
+        m.mdnn_net_create(bad, 8, cfg)
+    bad = list(good)
+    bad[3] = L(m.LAYER_FC, 1, 64, 1, 1, 10, 0, 0, 0)                      # last layer with ReLU
+    with pytest.raises(m.MdnnError):
+        m.mdnn_net_create(bad, 8, cfg)
+    # the three workloads' chains are accepted and match the flat parameter counts
+    for f in (W.mlp784_fp32, W.lenet_bf16, W.wide_mlp_fp16):
+        c = f()
+        descs = [L(l.kind, l.act, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.pad) for l in c.layers]
+        tc = m.TrainCfg(DT_CODE[c.dtype], c.loss, c.lr, c.momentum, int(c.loss_scaling), c.n_classes)
+        h = m.mdnn_net_create(descs, c.batch, tc)
+        assert m.mdnn_net_sizes(h)[0] == c.n_params
+        m.mdnn_net_destroy(h)
+
+
+DT_CODE = {"f32": 0, "f16": 1, "bf16": 2}

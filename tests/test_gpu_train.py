@@ -1,0 +1,170 @@
+"""GPU parity of mdnn_train_step (forward, loss, backpropagation, SGD update)
+against the oracle's step on the same seeded inputs.
+
+The gate: the loss of every step (the forward loss before that step's
+update) within 1e-3 relative of the oracle's, over 10 steps (MLP fp32 and
+LeNet bf16 at their full sizes; the loss-scaled fp16 wide MLP at reduced width
+for 10 steps and at full size for 2 steps).  Also: every layer's stored
+output inside the step, reproducibility (bitwise-identical reruns), dynamic loss scaling
+through a forced overflow, and master weights after the run.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import train
+from tests.helpers import DT, dev, norm_max_err
+
+pytestmark = pytest.mark.gpu
+REL = 1e-3
+
+
+def _gpu_net(mdnn, cfg, params=None):
+    net = mdnn.Net(cfg.layers, cfg.batch, DT[cfg.dtype], cfg.loss, cfg.lr, cfg.momentum,
+                   cfg.loss_scaling, cfg.init_scale, cfg.n_classes)
+    net.set_params(W.init_params(cfg) if params is None else params)
+    return net
+
+
+def _target(cfg, t):
+    return dev(t, "f32") if cfg.loss == W.LOSS_MSE else dev(t, "i32")
+
+
+def _trajectory(mdnn, cfg, steps, params=None):
+    net = _gpu_net(mdnn, cfg, params)
+    losses = []
+    for s in range(steps):
+        x, t = W.batch_inputs(cfg, s)
+        losses.append(float(net.step(dev(x, "f32"), _target(cfg, t)).item()))
+    return losses, net
+
+
+def _oracle_trajectory(cfg, steps, params=None):
+    orc = train.from_config(cfg, W.init_params(cfg) if params is None else params)
+    losses = []
+    for s in range(steps):
+        x, t = W.batch_inputs(cfg, s)
+        losses.append(orc.step(x, t))
+    return losses, orc
+
+
+def _check(gl, ol):
+    for s, (g, o) in enumerate(zip(gl, ol)):
+        assert abs(g - o) <= REL * abs(o), f"step {s}: gpu {g} oracle {o} (all: {gl} vs {ol})"
+
+
+def test_mlp784_fp32_ten_steps(mdnn):
+    cfg = W.mlp784_fp32()
+    gl, net = _trajectory(mdnn, cfg, 10)
+    ol, orc = _oracle_trajectory(cfg, 10)
+    _check(gl, ol)
+    w = net.master.cpu().numpy().astype(np.float64)
+    assert norm_max_err(w, orc.w32) <= 1e-4
+
+
+@pytest.mark.timeout(300)
+def test_lenet_bf16_ten_steps(mdnn):
+    cfg = W.lenet_bf16()
+    gl, net = _trajectory(mdnn, cfg, 10)
+    ol, orc = _oracle_trajectory(cfg, 10)
+    _check(gl, ol)
+    assert gl[-1] < gl[0]
+    w = net.master.cpu().numpy().astype(np.float64)
+    assert norm_max_err(w, orc.w32) <= 1e-3
+
+
+@pytest.mark.timeout(300)
+def test_wide_mlp_fp16_reduced_ten_steps(mdnn):
+    cfg = W.wide_mlp_fp16(batch=512, width=1024)
+    gl, net = _trajectory(mdnn, cfg, 10)
+    ol, orc = _oracle_trajectory(cfg, 10)
+    _check(gl, ol)
+    s = mdnn.read_scaler(net.scaler)
+    assert s["scale"] == orc.scaler["scale"] and s["good_steps"] == orc.scaler["good_steps"]
+    w = net.master.cpu().numpy().astype(np.float64)
+    assert norm_max_err(w, orc.w32) <= 1e-3
+
+
+@pytest.mark.timeout(300)
+def test_wide_mlp_fp16_full_size_two_steps(mdnn):
+    """The full wide MLP (batch 4096, 4 x 4096 hidden), as the benchmark runs it."""
+    cfg = W.wide_mlp_fp16()
+    gl, _ = _trajectory(mdnn, cfg, 2)
+    ol, _ = _oracle_trajectory(cfg, 2)
+    _check(gl, ol)
+
+
+def test_forced_overflow_skips_steps(mdnn):
+    """Initial loss scale 2^40: the scaled fp16 loss gradient overflows, the
+    update is skipped and the scale halves until it fits; the trajectory
+    (skipped steps included) matches the oracle's."""
+    cfg = W.wide_mlp_fp16(batch=256, width=256, init_scale=2.0 ** 40)
+    gl, net = _trajectory(mdnn, cfg, 6)
+    ol, orc = _oracle_trajectory(cfg, 6)
+    _check(gl, ol)
+    s = mdnn.read_scaler(net.scaler)
+    assert s["scale"] == orc.scaler["scale"] < 2.0 ** 40
+    assert s["good_steps"] == orc.scaler["good_steps"]
+
+
+def _stored(net, i, n, dt):
+    """Activation i of the last forward pass, read from the bound workspace."""
+    import torch
+    nbytes = n * (4 if dt == torch.float32 else 2)
+    off = net.activation_ptr(i) - net.ws.data_ptr()
+    return net.ws[off:off + nbytes].clone().view(dt)
+
+
+def test_layer_outputs_inside_the_step(mdnn):
+    """Each stored activation of the first forward pass of the LeNet chain
+    against the oracle's layer applied to the GPU's own stored input of that
+    layer (same bits in, so the per-op bar applies inside the chain)."""
+    import torch
+    from oracle import ops
+    from oracle.rounding import round_to
+    from tests.helpers import accum_bound, lowp_close
+    cfg = W.lenet_bf16()
+    p = W.init_params(cfg)
+    net = _gpu_net(mdnn, cfg, p)
+    x, t = W.batch_inputs(cfg, 0)
+    net.step(dev(x, "f32"), _target(cfg, t))
+    torch.cuda.synchronize()
+    B = cfg.batch
+    wl = round_to(p.astype(np.float64), "bf16")
+    a0 = _stored(net, 0, B * cfg.in_features, torch.bfloat16).float().cpu().numpy().astype(np.float64)
+    assert np.array_equal(a0, round_to(x.astype(np.float64), "bf16").reshape(-1))
+    for i, (l, (wo, bo)) in enumerate(zip(cfg.layers, cfg.param_offsets())):
+        last = i == len(cfg.layers) - 1
+        dt = torch.float32 if last else torch.bfloat16
+        a_in = _stored(net, i, B * l.c_in * l.h * l.w, torch.bfloat16).float().cpu().numpy().astype(np.float64)
+        got = _stored(net, i + 1, B * l.out_features(), dt).float().cpu().numpy().astype(np.float64)
+        b = p[bo:bo + l.n_bias].astype(np.float64)
+        if l.kind == W.FC:
+            w = wl[wo:wo + l.n_weight].reshape(l.c_in, l.c_out)
+            a2 = a_in.reshape(B, -1)
+            z = a2 @ w + b
+            bound = accum_bound(np.abs(a2) @ np.abs(w) + np.abs(b), l.c_in + 1)
+        elif l.kind == W.CONV:
+            w = wl[wo:wo + l.n_weight].reshape(l.c_out, l.r, l.s, l.c_in)
+            a4 = a_in.reshape(B, l.h, l.w, l.c_in)
+            z = ops.conv2d_fwd(a4, w, l.pad) + b
+            bound = accum_bound(ops.conv2d_fwd(np.abs(a4), np.abs(w), l.pad) + np.abs(b),
+                                l.r * l.s * l.c_in + 1)
+        else:
+            y, _ = ops.maxpool2_fwd(a_in.reshape(B, l.h, l.w, l.c_in))
+            assert np.array_equal(got, y.reshape(-1)), i
+            continue
+        if l.act == W.ACT_RELU:
+            z = ops.relu(z)
+        if last:
+            assert norm_max_err(got, z.reshape(-1)) <= 1e-4, i
+        else:
+            assert lowp_close(got, z.reshape(-1), "bf16", bound.reshape(-1)), i
+
+
+def test_train_step_reproducible(mdnn):
+    cfg = W.lenet_bf16()
+    gl1, n1 = _trajectory(mdnn, cfg, 3)
+    gl2, n2 = _trajectory(mdnn, cfg, 3)
+    assert gl1 == gl2
+    assert bool((n1.master == n2.master).all()) and bool((n1.lowp == n2.lowp).all())

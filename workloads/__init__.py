@@ -181,17 +181,19 @@ def lenet_bf16() -> TrainConfig:
         batch=256, in_features=784, dtype="bf16", loss=LOSS_XENT, lr=0.01)
 
 
-def wide_mlp_fp16(batch: int = 4096) -> TrainConfig:
+def wide_mlp_fp16(batch: int = 4096, width: int = 4096, init_scale: float = 2.0 ** 16) -> TrainConfig:
     """Wide regression MLP 1024->4x4096(ReLU)->1, MSE, fp16 storage with dynamic
     loss scaling (initial scale 2^16), fp32 master weights, SGD momentum 0.9.
-    The learning rate is not given by the workload; 1e-3 is used."""
-    layers = [Layer(FC, 1024, c_out=4096, act=ACT_RELU)]
-    layers += [Layer(FC, 4096, c_out=4096, act=ACT_RELU) for _ in range(3)]
-    layers += [Layer(FC, 4096, c_out=1)]
+    The learning rate is not given by the workload; 1e-3 is used.  ``width``
+    shrinks the hidden layers for quick multi-step checks."""
+    layers = [Layer(FC, 1024, c_out=width, act=ACT_RELU)]
+    layers += [Layer(FC, width, c_out=width, act=ACT_RELU) for _ in range(3)]
+    layers += [Layer(FC, width, c_out=1)]
+    suffix = "" if width == 4096 else f"_w{width}"
     return TrainConfig(
-        name=f"wide_mlp_fp16_b{batch}", base_seed=1188 + 5, layers=tuple(layers),
+        name=f"wide_mlp_fp16_b{batch}{suffix}", base_seed=1188 + 5, layers=tuple(layers),
         batch=batch, in_features=1024, dtype="f16", loss=LOSS_MSE, lr=1e-3,
-        momentum=0.9, loss_scaling=True, init_scale=2.0 ** 16, x_dist="normal")
+        momentum=0.9, loss_scaling=True, init_scale=init_scale, x_dist="normal")
 
 
 TRAIN_CONFIGS = {
