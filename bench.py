@@ -100,14 +100,18 @@ def _step_gemms(cfg):
     return out
 
 
-def _tile(m: int, n: int) -> str:
-    """The GEMM engine's automatic tile choice (a fixed table keyed on M, N)."""
+def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
+    """The GEMM engine's automatic kernel choice for the step's plain,
+    aligned operands (mirrors the library's fixed table)."""
     cd = lambda a, b: -(-a // b)  # noqa: E731
+    mn_contig = {"NN": [n], "NT": [], "TN": [m, n]}[layout]
+    if k % 64 == 0 and all(d % 8 == 0 for d in mn_contig) and cd(m, 256) * cd(n, 256) >= 128:
+        return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
     if cd(m, 256) * cd(n, 256) >= 256:
-        return "256x256"
+        return "gemm_mfma_kernel 256x256"
     if cd(m, 128) * cd(n, 128) >= 160:
-        return "128x128"
-    return "64x64"
+        return "gemm_mfma_kernel 128x128"
+    return "gemm_mfma_kernel 64x64"
 
 
 def _replay_group(mdnn, net, cfg, group, reps):
@@ -266,7 +270,7 @@ def main():
     gemms = _step_gemms(cfg)
     groups = {}
     for g in gemms:
-        groups.setdefault((g[0], g[4], _tile(g[1], g[2])), []).append(g)
+        groups.setdefault((g[0], g[4], _kernel_choice(g[0], g[1], g[2], g[3])), []).append(g)
     best = None
     for key, grp in groups.items():
         mpl, fpl = _replay_group(mdnn, net, cfg, grp, reps=max(5, args.steps // 2))
@@ -277,8 +281,7 @@ def main():
     achieved = fpl / (mpl * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_F16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_F16_TFLOPS, 4), "traffic": None,
-                "kernel": f"gemm_mfma_kernel {key[0]} f16 -> {key[1]}, tile {key[2]}, "
-                          f"{nl} launches per step",
+                "kernel": f"{key[2]}, {key[0]} f16 -> {key[1]}, {nl} launches per step",
                 "avg_launch_ms": round(mpl, 4), "flop_per_launch": fpl}
     print(f"[bench] dominant kernel {roofline['kernel']}: {mpl:.4f} ms/launch, "
           f"{achieved:.1f} TFLOP/s", file=sys.stderr, flush=True)

@@ -101,10 +101,14 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
                               const float* bias, mdnn_act_t act, const void* mask_src,
                               int64_t ldm, mdnn_stream_t stream);
 
-/* Tuning knob for measurements (process-wide): force the MFMA tile shape of
- * the GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128,
- * 3 = 64x64.  Returns 0, or -1 for an unknown code.  Results do not depend on
- * the tile shape except through the fp32 summation order of split-K. */
+/* Tuning knob for measurements (process-wide): force the MFMA kernel of the
+ * GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128, 3 = 64x64
+ * general kernels, 4 = the 256x256 direct-to-LDS pipelined kernel wherever its
+ * preconditions hold (K % 64 == 0, 16-byte aligned operands with leading
+ * dimensions multiple of 8, MN-contiguous extents multiple of 8), the
+ * automatic choice elsewhere.  Returns 0, or -1 for an unknown code.  Results
+ * do not depend on the kernel except through the fp32 summation order of
+ * split-K. */
 int mdnn_set_gemm_tile(int code);
 
 /* ---------------------------------------------------------------------------
@@ -135,12 +139,13 @@ mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, const void* d
                                    mdnn_dtype_t dx_type, mdnn_stream_t stream);
 
 /* Bytes of device workspace mdnn_conv2d_bwd_filter needs for this shape
- * (fp32 split-K partial sums reduced in a fixed order); 0 on a bad shape. */
+ * (fp32 split-K partial sums of dw and partial column sums of db, each
+ * reduced in a fixed order); 0 on a bad shape. */
 size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape, mdnn_dtype_t io_type);
 
 /* dw: fp32 [c_out, r, s, c_in] (overwritten).  db: NULL or fp32 [c_out]
- * (overwritten).  workspace: device memory of at least the size above (may be
- * NULL when that size is 0).  Deterministic. */
+ * (overwritten).  workspace: device memory of at least the size above,
+ * 256-byte aligned (may be NULL when that size is 0).  Deterministic. */
 mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x, const void* dy,
                                      mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
                                      size_t ws_bytes, mdnn_stream_t stream);
@@ -154,13 +159,18 @@ mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void*
  *        (dz may be NULL, may alias dy); db = column sums of dz in fp32
  *        (db may be NULL), summed in a fixed order (deterministic).
  *        dy, y, dz are `dtype` [rows, cols]; y may be NULL when act is NONE.
+ *        workspace: NULL, or device memory of mdnn_bias_act_bwd_workspace()
+ *        bytes (16-byte aligned) that lets db use a two-pass reduction spread
+ *        over the whole GPU; without it db is summed by one pass per column
+ *        group (same result, much slower for tall matrices).
  * ------------------------------------------------------------------------- */
 mdnn_status_t mdnn_bias_act_fwd(int64_t rows, int64_t cols, const float* x, const float* bias,
                                 mdnn_act_t act, void* y, mdnn_dtype_t y_type,
                                 mdnn_stream_t stream);
+size_t mdnn_bias_act_bwd_workspace(int64_t rows, int64_t cols);
 mdnn_status_t mdnn_bias_act_bwd(int64_t rows, int64_t cols, const void* dy, const void* y,
                                 mdnn_act_t act, void* dz, float* db, mdnn_dtype_t dtype,
-                                mdnn_stream_t stream);
+                                void* workspace, size_t ws_bytes, mdnn_stream_t stream);
 
 /* ---------------------------------------------------------------------------
  * 2x2 stride-2 max pooling, NHWC (the LeNet-style workload's pooling layers).

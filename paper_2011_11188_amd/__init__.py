@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libmdnn.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
-        f"{LIB_PATH} is missing: build it with `python -m paper_2011_11188_amd.build` "
+        f"{LIB_PATH} is missing: build it with `python paper_2011_11188_amd/build.py` "
         "(the HIP path has no fallback)")
 
 _lib = C.CDLL(LIB_PATH)
@@ -74,7 +74,7 @@ _SIGS = {
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
     "mdnn_bias_act_fwd": [_i64, _i64, _vp, _vp, _i, _vp, _i, _vp],
-    "mdnn_bias_act_bwd": [_i64, _i64, _vp, _vp, _i, _vp, _vp, _i, _vp],
+    "mdnn_bias_act_bwd": [_i64, _i64, _vp, _vp, _i, _vp, _vp, _i, _vp, C.c_size_t, _vp],
     "mdnn_maxpool2_fwd": [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _i, _vp],
     "mdnn_maxpool2_bwd": [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _i, _vp],
     "mdnn_softmax_xent": [_i64, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _i64, _i, _vp],
@@ -93,6 +93,8 @@ for _name, _args in _SIGS.items():
     _fn.restype = C.c_int
 _lib.mdnn_conv2d_bwd_filter_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_bwd_filter_workspace.restype = C.c_size_t
+_lib.mdnn_bias_act_bwd_workspace.argtypes = [_i64, _i64]
+_lib.mdnn_bias_act_bwd_workspace.restype = C.c_size_t
 _lib.mdnn_last_error.restype = C.c_char_p
 _lib.mdnn_version.restype = C.c_char_p
 _lib.mdnn_net_activation.argtypes = [_vp, C.c_int32]
@@ -146,7 +148,8 @@ def last_error() -> str:
 
 
 def exported_symbols():
-    return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_last_error",
+    return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
+                                 "mdnn_last_error",
                                  "mdnn_version", "mdnn_net_activation", "mdnn_net_destroy",
                                  "mdnn_set_gemm_tile"])
 
@@ -189,9 +192,14 @@ def mdnn_bias_act_fwd(rows, cols, x, bias, act, y, y_type, stream=None):
     return _call("mdnn_bias_act_fwd", rows, cols, _p(x), _p(bias), act, _p(y), y_type, _s(stream))
 
 
-def mdnn_bias_act_bwd(rows, cols, dy, y, act, dz, db, dtype, stream=None):
+def mdnn_bias_act_bwd_workspace(rows, cols) -> int:
+    return _lib.mdnn_bias_act_bwd_workspace(rows, cols)
+
+
+def mdnn_bias_act_bwd(rows, cols, dy, y, act, dz, db, dtype, workspace=None, ws_bytes=0,
+                      stream=None):
     return _call("mdnn_bias_act_bwd", rows, cols, _p(dy), _p(y), act, _p(dz), _p(db), dtype,
-                 _s(stream))
+                 _p(workspace), ws_bytes, _s(stream))
 
 
 def mdnn_maxpool2_fwd(n, h, w, c, x, y, argmax, dtype, stream=None):

@@ -1,6 +1,7 @@
 """Build libmdnn.so (gfx950) in-tree with hipcc.
 
-    python -m paper_2011_11188_amd.build      # or build() from Python
+    python paper_2011_11188_amd/build.py      # (not -m: that imports the package,
+                                              #  which loads the library being rebuilt)
 
 Every source under csrc/ is compiled to an object in _build/ (in parallel),
 then linked into paper_2011_11188_amd/libmdnn.so.
@@ -23,8 +24,10 @@ ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           f"-I{os.path.join(os.path.dirname(PKG), 'include')}"]
-# Packed fp32 instructions are disabled for all device code.
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 instructions are disabled for all device code.  MFMA results
+# are kept in VGPRs (in-place accumulation), which the kernels are sized for.
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def _compile(src: str) -> str:

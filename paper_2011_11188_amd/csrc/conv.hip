@@ -153,13 +153,19 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
   }
 }
 
+// Workspace: split-K partials of dw, then (256-byte aligned) the partial
+// column sums of db.
+static size_t filter_ws_split_bytes(const ConvGeom& g) {
+  SplitPlan p = filter_plan(g);
+  if (p.splits <= 1) return 0;
+  return ((size_t)p.splits * g.k * ((size_t)g.r * g.s * g.c) * sizeof(float) + 255) & ~(size_t)255;
+}
+
 extern "C" size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape,
                                                    mdnn_dtype_t io_type) {
   ConvGeom g;
   if (check_shape(shape, g) != MDNN_SUCCESS || !dtype_ok(io_type)) return 0;
-  SplitPlan p = filter_plan(g);
-  if (p.splits <= 1) return 0;
-  return (size_t)p.splits * g.k * ((size_t)g.r * g.s * g.c) * sizeof(float);
+  return filter_ws_split_bytes(g) + column_sums_ws_bytes((int64_t)g.n * g.ho * g.wo, g.k);
 }
 
 extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x,
@@ -175,8 +181,8 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
   if ((x && !aligned(x, es)) || (dy && !aligned(dy, es)) || !aligned(dw, 4) || (db && !aligned(db, 4)))
     return fail(MDNN_ERR_MISALIGNED, "conv bwd_filter: misaligned base pointer");
   const size_t need = mdnn_conv2d_bwd_filter_workspace(shape, io_type);
-  if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 16)))
-    return fail(MDNN_ERR_WORKSPACE, "conv bwd_filter: needs %zu bytes of 16-byte aligned workspace",
+  if (need > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
+    return fail(MDNN_ERR_WORKSPACE, "conv bwd_filter: needs %zu bytes of 256-byte aligned workspace",
                 need);
   clear_error();
   hipStream_t st = as_stream(stream);
@@ -190,6 +196,11 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
     case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st)); break;
     default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st)); break;
   }
-  if (db) return column_sums(dy, io_type, (int64_t)g.n * g.ho * g.wo, g.k, db, st);
+  if (db) {
+    const size_t off = filter_ws_split_bytes(g);
+    const size_t cs = column_sums_ws_bytes((int64_t)g.n * g.ho * g.wo, g.k);
+    return column_sums(dy, nullptr, io_type, (int64_t)g.n * g.ho * g.wo, g.k, db,
+                       cs ? (char*)workspace + off : nullptr, cs, st);
+  }
   return MDNN_SUCCESS;
 }

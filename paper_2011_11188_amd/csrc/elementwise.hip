@@ -113,32 +113,6 @@ __global__ void relu_mask_kernel(const typename T::storage* __restrict__ dy,
   }
 }
 
-// Column sums of dy (masked by [y > 0] when y != null); 32 columns per block,
-// 8 row lanes each summing rows in order, combined in a fixed order.
-template <class T>
-__global__ void __launch_bounds__(256)
-masked_column_sums_kernel(const typename T::storage* __restrict__ dy,
-                          const typename T::storage* __restrict__ y, int64_t rows, int64_t cols,
-                          float* __restrict__ out) {
-  __shared__ float part[8][33];
-  const int cx = threadIdx.x & 31, ry = threadIdx.x >> 5;
-  const int64_t col = (int64_t)blockIdx.x * 32 + cx;
-  float s = 0.0f;
-  if (col < cols)
-    for (int64_t r = ry; r < rows; r += 8) {
-      const int64_t i = r * cols + col;
-      if (y == nullptr || to_f<T>(y[i]) > 0.0f) s += to_f<T>(dy[i]);
-    }
-  part[ry][cx] = s;
-  __syncthreads();
-  if (ry == 0 && col < cols) {
-    float t = part[0][cx];
-#pragma unroll
-    for (int k = 1; k < 8; ++k) t += part[k][cx];
-    out[col] = t;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // 2x2 / stride 2 max pooling, NHWC
 // ---------------------------------------------------------------------------
@@ -396,13 +370,9 @@ extern "C" mdnn_status_t mdnn_bias_act_fwd(int64_t rows, int64_t cols, const flo
 
 template <class T>
 static mdnn_status_t bias_act_bwd_t(int64_t rows, int64_t cols, const void* dy, const void* y,
-                                    void* dz, float* db, hipStream_t st) {
+                                    void* dz, float* db, void* ws, size_t ws_bytes, hipStream_t st) {
   typedef typename T::storage S;
-  if (db) {
-    hipLaunchKernelGGL(masked_column_sums_kernel<T>, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
-                       (const S*)dy, (const S*)y, rows, cols, db);
-    MDNN_TRY(check_launch("masked_column_sums_kernel"));
-  }
+  if (db) MDNN_TRY(column_sums(dy, y, T::id, rows, cols, db, ws, ws_bytes, st));
   if (dz) {
     unsigned g = grid_for(rows * cols, 256);
     if (g > 8192) g = 8192;
@@ -413,9 +383,15 @@ static mdnn_status_t bias_act_bwd_t(int64_t rows, int64_t cols, const void* dy, 
   return MDNN_SUCCESS;
 }
 
+extern "C" size_t mdnn_bias_act_bwd_workspace(int64_t rows, int64_t cols) {
+  if (rows < 0 || cols < 0) return 0;
+  return column_sums_ws_bytes(rows, cols);
+}
+
 extern "C" mdnn_status_t mdnn_bias_act_bwd(int64_t rows, int64_t cols, const void* dy,
                                            const void* y, mdnn_act_t act, void* dz, float* db,
-                                           mdnn_dtype_t dtype, mdnn_stream_t stream) {
+                                           mdnn_dtype_t dtype, void* workspace, size_t ws_bytes,
+                                           mdnn_stream_t stream) {
   if (rows < 0 || cols < 0) return fail(MDNN_ERR_SHAPE, "bias_act_bwd: negative size");
   if (!dtype_ok(dtype)) return fail(MDNN_ERR_DTYPE, "bias_act_bwd: unknown dtype");
   if (act != MDNN_ACT_NONE && act != MDNN_ACT_RELU) return fail(MDNN_ERR_DTYPE, "bias_act_bwd: unknown act");
@@ -428,16 +404,17 @@ extern "C" mdnn_status_t mdnn_bias_act_bwd(int64_t rows, int64_t cols, const voi
   if (!dy) return fail(MDNN_ERR_NULL, "bias_act_bwd: dy is NULL");
   if (act == MDNN_ACT_RELU && !y) return fail(MDNN_ERR_NULL, "bias_act_bwd: ReLU needs y");
   const size_t es = dtype_size(dtype);
-  if (!aligned(dy, es) || (y && !aligned(y, es)) || (dz && !aligned(dz, es)) || (db && !aligned(db, 4)))
+  if (!aligned(dy, es) || (y && !aligned(y, es)) || (dz && !aligned(dz, es)) || (db && !aligned(db, 4)) ||
+      (workspace && !aligned(workspace, 16)))
     return fail(MDNN_ERR_MISALIGNED, "bias_act_bwd: misaligned buffer");
   const void* ym = act == MDNN_ACT_RELU ? y : nullptr;
   if (dz == dy && act == MDNN_ACT_NONE) dz = nullptr;  // nothing to write
   clear_error();
   hipStream_t st = as_stream(stream);
   switch (dtype) {
-    case MDNN_F32: return bias_act_bwd_t<F32>(rows, cols, dy, ym, dz, db, st);
-    case MDNN_F16: return bias_act_bwd_t<F16>(rows, cols, dy, ym, dz, db, st);
-    default: return bias_act_bwd_t<BF16>(rows, cols, dy, ym, dz, db, st);
+    case MDNN_F32: return bias_act_bwd_t<F32>(rows, cols, dy, ym, dz, db, workspace, ws_bytes, st);
+    case MDNN_F16: return bias_act_bwd_t<F16>(rows, cols, dy, ym, dz, db, workspace, ws_bytes, st);
+    default: return bias_act_bwd_t<BF16>(rows, cols, dy, ym, dz, db, workspace, ws_bytes, st);
   }
 }
 

@@ -42,18 +42,94 @@ mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int6
   return check_launch("reduce_splits_kernel");
 }
 
-// Column sums: a block owns 32 columns; 8 row lanes stride over the rows in
-// order and are combined in a fixed order through LDS.
+// Column sums of a [rows, cols] matrix (optionally masked by [y > 0]), in a
+// fixed order so the result is bitwise reproducible.
+//
+// With a workspace (two passes): pass 1 splits the rows into chunks of
+// COLSUM_ROWS; a block reduces one chunk x 64 columns (8 column groups of 8
+// read as 16-byte vectors, 32 row lanes, then a fixed-order combine in LDS)
+// into partial[chunk][col].  Pass 2 sums the partials of each column in chunk
+// order (8 lanes per column, strided, then a fixed-order combine).
+// Without a workspace: one block per 32 columns walks all rows (slow for very
+// tall matrices; kept for callers that cannot provide memory).
+constexpr int64_t COLSUM_ROWS = 256;
+
+template <class T>
+__device__ __forceinline__ float masked_val(const typename T::storage* x, const typename T::storage* y,
+                                            int64_t i) {
+  return (y == nullptr || to_f<T>(y[i]) > 0.0f) ? to_f<T>(x[i]) : 0.0f;
+}
+
 template <class T>
 __global__ void __launch_bounds__(256)
-column_sums_kernel(const typename T::storage* __restrict__ x, int64_t rows, int64_t cols,
-                   float* __restrict__ out) {
+colsum_partial_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ y,
+                      int64_t rows, int64_t cols, bool vec, float* __restrict__ partial) {
+  __shared__ float red[32][65];
+  const int cg = threadIdx.x & 7, rl = threadIdx.x >> 3;
+  const int64_t c0 = (int64_t)blockIdx.x * 64 + cg * 8;
+  const int64_t r0 = (int64_t)blockIdx.y * COLSUM_ROWS;
+  const int64_t r1 = r0 + COLSUM_ROWS < rows ? r0 + COLSUM_ROWS : rows;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (vec && sizeof(typename T::storage) == 2 && c0 + 8 <= cols) {
+    for (int64_t r = r0 + rl; r < r1; r += 32) {
+      const uint4 v = *(const uint4*)(x + r * cols + c0);
+      uint4 m = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
+      if (y) m = *(const uint4*)(y + r * cols + c0);
+      const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+      const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint16_t xv = (uint16_t)(vw[e >> 1] >> ((e & 1) * 16));
+        const uint16_t yv = (uint16_t)(mw[e >> 1] >> ((e & 1) * 16));
+        if (y == nullptr || to_f<T>((typename T::storage)yv) > 0.0f) s[e] += to_f<T>((typename T::storage)xv);
+      }
+    }
+  } else {
+    for (int64_t r = r0 + rl; r < r1; r += 32)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (c0 + e < cols) s[e] += masked_val<T>(x, y, r * cols + c0 + e);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rl][cg * 8 + e] = s[e];
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int64_t c = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    float t = red[0][threadIdx.x];
+    for (int k = 1; k < 32; ++k) t += red[k][threadIdx.x];
+    if (c < cols) partial[(int64_t)blockIdx.y * cols + c] = t;
+  }
+}
+
+__global__ void __launch_bounds__(256)
+colsum_final_kernel(const float* __restrict__ partial, int64_t chunks, int64_t cols,
+                    float* __restrict__ out) {
+  __shared__ float red[8][33];
+  const int cx = threadIdx.x & 31, ln = threadIdx.x >> 5;
+  const int64_t c = (int64_t)blockIdx.x * 32 + cx;
+  float s = 0.0f;
+  if (c < cols)
+    for (int64_t k = ln; k < chunks; k += 8) s += partial[k * cols + c];
+  red[ln][cx] = s;
+  __syncthreads();
+  if (ln == 0 && c < cols) {
+    float t = red[0][cx];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += red[k][cx];
+    out[c] = t;
+  }
+}
+
+template <class T>
+__global__ void __launch_bounds__(256)
+colsum_single_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ y,
+                     int64_t rows, int64_t cols, float* __restrict__ out) {
   __shared__ float part[8][33];
   const int cx = threadIdx.x & 31, ry = threadIdx.x >> 5;
   const int64_t col = (int64_t)blockIdx.x * 32 + cx;
   float s = 0.0f;
   if (col < cols)
-    for (int64_t r = ry; r < rows; r += 8) s += to_f<T>(x[r * cols + col]);
+    for (int64_t r = ry; r < rows; r += 8) s += masked_val<T>(x, y, r * cols + col);
   part[ry][cx] = s;
   __syncthreads();
   if (ry == 0 && col < cols) {
@@ -64,22 +140,39 @@ column_sums_kernel(const typename T::storage* __restrict__ x, int64_t rows, int6
   }
 }
 
-mdnn_status_t column_sums(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* out,
-                          hipStream_t stream) {
-  if (cols == 0) return MDNN_SUCCESS;
-  dim3 grid((unsigned)ceil_div(cols, 32));
-  switch (t) {
-    case MDNN_F32:
-      hipLaunchKernelGGL(column_sums_kernel<F32>, grid, dim3(256), 0, stream, (const float*)x, rows, cols, out);
-      break;
-    case MDNN_F16:
-      hipLaunchKernelGGL(column_sums_kernel<F16>, grid, dim3(256), 0, stream, (const uint16_t*)x, rows, cols, out);
-      break;
-    default:
-      hipLaunchKernelGGL(column_sums_kernel<BF16>, grid, dim3(256), 0, stream, (const uint16_t*)x, rows, cols, out);
-      break;
+size_t column_sums_ws_bytes(int64_t rows, int64_t cols) {
+  if (rows <= COLSUM_ROWS) return 0;
+  return (size_t)ceil_div(rows, COLSUM_ROWS) * (size_t)cols * sizeof(float);
+}
+
+template <class T>
+static void colsum_launch(const void* x, const void* y, int64_t rows, int64_t cols, float* out,
+                          void* ws, size_t ws_bytes, hipStream_t st) {
+  typedef typename T::storage S;
+  const size_t need = column_sums_ws_bytes(rows, cols);
+  if (need > 0 && ws && ws_bytes >= need && aligned(ws, 4)) {
+    const int64_t chunks = ceil_div(rows, COLSUM_ROWS);
+    const bool vec = aligned(x, 16) && (!y || aligned(y, 16)) && cols % 8 == 0;
+    hipLaunchKernelGGL(colsum_partial_kernel<T>, dim3((unsigned)ceil_div(cols, 64), (unsigned)chunks), dim3(256),
+                       0, st, (const S*)x, (const S*)y, rows, cols, vec, (float*)ws);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
+                       (const float*)ws, chunks, cols, out);
+  } else {
+    hipLaunchKernelGGL(colsum_single_kernel<T>, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
+                       (const S*)x, (const S*)y, rows, cols, out);
   }
-  return check_launch("column_sums_kernel");
+}
+
+mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
+                          float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (cols == 0) return MDNN_SUCCESS;
+  if (ceil_div(rows, COLSUM_ROWS) > 65535) ws = nullptr;  // grid limit: single pass
+  switch (t) {
+    case MDNN_F32: colsum_launch<F32>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
+    case MDNN_F16: colsum_launch<F16>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
+    default: colsum_launch<BF16>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
+  }
+  return check_launch("column sums");
 }
 
 // ---------------------------------------------------------------------------
@@ -91,6 +184,14 @@ static mdnn_status_t gemm_dispatch16(mdnn_layout_t layout, int64_t M, int64_t N,
                                      int64_t ldb, bool vb, const Epilogue& ep, hipStream_t st) {
   const uint16_t* a = (const uint16_t*)A;
   const uint16_t* b = (const uint16_t*)B;
+  const LdsOperand la{A, lda, M, layout != MDNN_TN}, lb{B, ldb, N, layout == MDNN_NT};
+  if (lds_pipe_eligible(la, lb, M, N, K, K, 1)) {
+    switch (layout) {
+      case MDNN_NN: return run_gemm_lds<T, OutT, true, false>(la, lb, M, N, K, ep, 1, st);
+      case MDNN_NT: return run_gemm_lds<T, OutT, true, true>(la, lb, M, N, K, ep, 1, st);
+      default: return run_gemm_lds<T, OutT, false, false>(la, lb, M, N, K, ep, 1, st);
+    }
+  }
   switch (layout) {
     case MDNN_NN:
       return run_gemm16<T, OutT>(SrcMatK<uint16_t>{a, lda, M, K, va},
@@ -187,7 +288,7 @@ extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_
 }
 
 extern "C" int mdnn_set_gemm_tile(int code) {
-  if (code < 0 || code > 3) return -1;
+  if (code < 0 || code > 4) return -1;
   g_tile_override.store(code, std::memory_order_relaxed);
   return 0;
 }

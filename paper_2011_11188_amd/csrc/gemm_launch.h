@@ -3,6 +3,7 @@
 #pragma once
 
 #include "gemm_core.h"
+#include "gemm_lds.h"
 #include "internal.h"
 
 namespace mdnn {
@@ -62,14 +63,17 @@ gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
   }
 }
 
-// Tile configurations of the MFMA kernel.
-enum TileCfg { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2, TILE_64x64 = 3 };
+// Tile configurations of the MFMA kernels.  TILE_LDS_PIPE is the 256 x 256
+// direct-to-LDS pipelined mainloop (gemm_lds.h), used for plain matrices that
+// meet its preconditions.
+enum TileCfg { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2, TILE_64x64 = 3, TILE_LDS_PIPE = 4 };
 
 int gemm_tile_override();
 
 inline TileCfg choose_tile(int64_t M, int64_t N, int splits) {
   int o = gemm_tile_override();
   if (o >= TILE_256x256 && o <= TILE_64x64) return (TileCfg)o;
+  if (o == TILE_LDS_PIPE) return TILE_256x256;  // this path has no pipelined kernel
   const int64_t t256 = ceil_div(M, 256) * ceil_div(N, 256) * splits;
   if (t256 >= 256) return TILE_256x256;
   const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128) * splits;
@@ -97,6 +101,39 @@ inline mdnn_status_t run_gemm16(const SrcA& a, const SrcB& b, int64_t M, int64_t
     default:           launch_mfma<T, OutT, SrcA, SrcB, 64, 64, 1, 2>(a, b, M, N, K, ep, splits, stream); break;
   }
   return check_launch("gemm_mfma_kernel");
+}
+
+// Plain-matrix operand of the pipelined kernel: `kc` = K-contiguous.
+struct LdsOperand {
+  const void* p;
+  int64_t ld, MN;
+  bool kc;
+};
+
+// Whether the pipelined kernel can run this problem (see gemm_lds.h).
+inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
+                              int64_t K, int64_t k_per_split, int splits) {
+  const int o = gemm_tile_override();
+  if (o >= TILE_256x256 && o <= TILE_64x64) return false;
+  if (K <= 0 || K % lds::BK != 0 || k_per_split % lds::BK != 0) return false;
+  if (o != TILE_LDS_PIPE && ceil_div(M, 256) * ceil_div(N, 256) * splits < 128) return false;
+  for (const LdsOperand* op : {&a, &b}) {
+    if (!aligned(op->p, 16) || op->ld % 8 != 0) return false;
+    const int64_t reach = op->kc ? (op->MN - 1) * op->ld + K : (int64_t)lds::BK * op->ld + op->MN;
+    if (reach * 2 >= (int64_t)1 << 32) return false;
+    if (!op->kc && (op->MN % 8 != 0 || op->MN < 8)) return false;
+  }
+  return true;
+}
+
+template <class T, class OutT, bool A_KC, bool B_KC>
+inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
+                                  int64_t K, const Epilogue& ep, int splits, hipStream_t stream) {
+  dim3 grid((unsigned)(ceil_div(M, lds::BM) * ceil_div(N, lds::BN)), (unsigned)splits, 1);
+  lds::Operand oa{(const uint16_t*)a.p, a.ld, a.MN}, ob{(const uint16_t*)b.p, b.ld, b.MN};
+  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, A_KC, B_KC>), grid, dim3(lds::NT), 0, stream, oa,
+                     ob, M, N, K, ep);
+  return check_launch("gemm_lds_kernel");
 }
 
 template <class SrcA, class SrcB>

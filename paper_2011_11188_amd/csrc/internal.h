@@ -43,8 +43,12 @@ mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t stream);
 // Element-wise conversion between any two storage types (RNE when narrowing).
 mdnn_status_t cast_any(int64_t n, const void* src, mdnn_dtype_t s, void* dst, mdnn_dtype_t d,
                        hipStream_t stream);
-// Deterministic column sums of a [rows, cols] matrix of type t into fp32.
-mdnn_status_t column_sums(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols,
-                          float* out, hipStream_t stream);
+// Deterministic column sums of a [rows, cols] matrix x of type t (entries
+// where y <= 0 skipped when y != NULL) into fp32 out[cols].  Uses a two-pass
+// reduction when a workspace of column_sums_ws_bytes(rows, cols) bytes is
+// given, a single (slower) pass otherwise.
+size_t column_sums_ws_bytes(int64_t rows, int64_t cols);
+mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
+                          float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 }  // namespace mdnn

@@ -11,7 +11,8 @@
 //   act[i+1]        stored output of layer i (fp32 for the last layer)
 //   argmax[i]       window index of each max-pool output
 //   grad0, grad1    ping-pong buffers for activation gradients (low precision)
-//   filter_ws       split-K partials of the convolution backward-filter
+//   reduce_ws       split-K partials of the convolution backward-filter and
+//                   partial column sums of the bias gradients
 #include <new>
 #include <vector>
 
@@ -151,6 +152,10 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
       size_t need = mdnn_conv2d_bwd_filter_workspace(&cs, net->lp);
       if (need > fws) fws = need;
     }
+    if (p.L.kind == MDNN_LAYER_FC) {
+      size_t need = mdnn_bias_act_bwd_workspace(batch, p.L.c_out);
+      if (need > fws) fws = need;
+    }
     if (p.in_feat > max_feat) max_feat = p.in_feat;
     if (p.out_feat > max_feat) max_feat = p.out_feat;
   }
@@ -278,7 +283,8 @@ extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const 
       // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
       MDNN_TRY(mdnn_gemm_mixed(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o,
                                MDNN_F32, nullptr, MDNN_ACT_NONE, nullptr, 0, stream));
-      MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, stream));
+      MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp,
+                                 ws + net->fws_off, net->fws_bytes, stream));
       if (ii > 0) {
         // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
         MDNN_TRY(mdnn_gemm_mixed(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0,

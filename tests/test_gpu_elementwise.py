@@ -69,6 +69,10 @@ def test_bias_act_fwd_bwd(mdnn, dt):
     dz = empty((rows, cols), dt)
     db = torch.empty(cols, dtype=torch.float32, device="cuda")
     mdnn.mdnn_bias_act_bwd(rows, cols, dev(dy, dt), y, mdnn.ACT_RELU, dz, db, DT[dt])
+    db2 = torch.empty(cols, dtype=torch.float32, device="cuda")
+    nws = mdnn.mdnn_bias_act_bwd_workspace(rows, cols)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    mdnn.mdnn_bias_act_bwd(rows, cols, dev(dy, dt), y, mdnn.ACT_RELU, None, db2, DT[dt], ws, nws)
     torch.cuda.synchronize()
     exact = ops.bias_act(x.astype(np.float64), b.astype(np.float64), "relu")
     # x + b is rounded to fp32 before the storage rounding
@@ -78,6 +82,26 @@ def test_bias_act_fwd_bwd(mdnn, dt):
     dzw, dbw = ops.bias_act_bwd(decode(dy, dt), host64(y), "relu")
     assert np.array_equal(host64(dz), dzw)
     assert norm_max_err(host64(db), dbw) <= 1e-5
+    assert norm_max_err(host64(db2), dbw) <= 1e-5      # two-pass reduction with a workspace
+
+
+@pytest.mark.parametrize("shape", [(200704, 32), (4096, 4096), (1000, 10), (513, 72)])
+def test_column_sums_tall_and_wide(mdnn, shape):
+    """Bias gradients of the workloads' layer shapes (conv1 of the LeNet-style
+    net: 200704 x 32; a wide FC layer: 4096 x 4096), two-pass, deterministic."""
+    import torch
+    rows, cols = shape
+    dy = W.normal((rows, cols), 29, 1, "f16", 0.01)
+    DY = dev(dy, "f16")
+    nws = mdnn.mdnn_bias_act_bwd_workspace(rows, cols)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    db = torch.empty(cols, dtype=torch.float32, device="cuda")
+    db2 = torch.empty(cols, dtype=torch.float32, device="cuda")
+    mdnn.mdnn_bias_act_bwd(rows, cols, DY, None, mdnn.ACT_NONE, None, db, DT["f16"], ws, nws)
+    mdnn.mdnn_bias_act_bwd(rows, cols, DY, None, mdnn.ACT_NONE, None, db2, DT["f16"], ws, nws)
+    torch.cuda.synchronize()
+    assert norm_max_err(host64(db), dy.astype(np.float64).sum(axis=0)) <= 1e-5
+    assert torch.equal(db, db2)
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16", "f32"])

@@ -63,6 +63,45 @@ def test_gemm_ragged_all_tiles(mdnn, tile, dt, layout):
         mdnn.mdnn_set_gemm_tile(0)
 
 
+# shapes the direct-to-LDS pipelined kernel accepts (K % 64 == 0, M and N
+# multiples of 8) but that are ragged with respect to its 256 x 256 tiles
+PIPE = [(312, 264, 192), (520, 776, 320), (1000, 1032, 448), (8, 8, 64), (64, 2056, 128),
+        (264, 8, 1024)]
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_gemm_pipelined_kernel_ragged(mdnn, dt, layout):
+    mdnn.mdnn_set_gemm_tile(4)
+    try:
+        for i, (m, n, k) in enumerate(PIPE):
+            sa, sb = _shapes(layout, m, n, k)
+            a = W.normal(sa, 9, 10 * i + 1, dt, 1 / np.sqrt(k))
+            b = W.normal(sb, 9, 10 * i + 2, dt, 1 / np.sqrt(k))
+            got = _run(mdnn, layout, dev(a, dt), dev(b, dt), "f32", m, n, k)
+            want = ops.gemm(layout, decode(a, dt), decode(b, dt))
+            assert norm_max_err(got, want) <= TOL, (layout, dt, (m, n, k))
+        # epilogues on the pipelined kernel: bias + ReLU to the storage type
+        m, n, k = 520, 776, 320
+        sa, sb = _shapes(layout, m, n, k)
+        a = W.normal(sa, 9, 101, dt, 1 / np.sqrt(k))
+        b = W.normal(sb, 9, 102, dt)
+        bias = W.normal((n,), 9, 103, "f32", 0.5)
+        got = _run(mdnn, layout, dev(a, dt), dev(b, dt), dt, m, n, k, bias=dev(bias, "f32"), act=1)
+        a64, b64 = decode(a, dt), decode(b, dt)
+        exact = ops.bias_act(ops.gemm(layout, a64, b64), bias.astype(np.float64), "relu")
+        err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)) + np.abs(bias), k + 1)
+        assert lowp_close(got, exact, dt, err)
+        # and the ReLU mask of a backward-data product
+        y_in = W.normal((m, n), 9, 104, dt)
+        got = _run(mdnn, layout, dev(a, dt), dev(b, dt), dt, m, n, k, mask=dev(y_in, dt))
+        exact = np.where(decode(y_in, dt) > 0, ops.gemm(layout, a64, b64), 0.0)
+        err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)), k)
+        assert lowp_close(got, exact, dt, err)
+    finally:
+        mdnn.mdnn_set_gemm_tile(0)
+
+
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 def test_gemm_small_integers_bit_exact(mdnn, dt, layout):
