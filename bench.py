@@ -10,8 +10,10 @@ is train samples per second.
 
 Also on the same JSON line:
   roofline      the step's dominant kernel: its average launch duration from
-                HIP events over a replay of exactly its launches in the step
-                (same shapes and buffers), against the fp16 MFMA peak;
+                HIP events around each launch of a replay of exactly its
+                launches in the step (same shapes and buffers), against the
+                fp16 MFMA peak; HBM traffic per launch from rocprofv3 counters
+                (profiles/) while the kernel source is unchanged;
   cpu_baseline  the fp64 oracle's step on this host on one full batch;
   gemm_sweep    the fp16 GEMM sweep (M = N = K in 1024/4096/8192, NN/NT/TN);
   conv          the ResNet-style 3x3 layers (batch 128) fwd / bwd-data /
@@ -147,12 +149,22 @@ def _replay_group(mdnn, net, cfg, group, reps):
     for c in calls:  # warm
         mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0, None, 0,
                              c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    with _Timer() as tm:
-        for _ in range(reps):
-            for c in calls:
-                mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
-                                     None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    return tm.ms / (reps * len(calls)), flops
+    # one event pair around every launch: the sum is the kernels' own time,
+    # without the gaps between back-to-back launches
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps * len(calls))]
+    _sync()
+    i = 0
+    for _ in range(reps):
+        for c in calls:
+            evs[i][0].record()
+            mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
+                                 None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
+            evs[i][1].record()
+            i += 1
+    _sync()
+    total = sum(a.elapsed_time(b) for a, b in evs)
+    return total / len(evs), flops
 
 
 def _gemm_sweep(mdnn, reps_scale=1.0):
@@ -212,6 +224,25 @@ def _conv_bench(mdnn, reps=20):
             res[f"L{li + 1}_{sh.c_in}x{sh.h}_{op}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
                                                        "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
     return res
+
+
+def _traffic_record(kernel_desc: str):
+    """HBM bytes per launch of the dominant kernel measured with rocprofv3
+    counters (profiles/), used only while the kernel source is unchanged."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_lds_kernel_traffic.txt")
+    src = os.path.join(ROOT, "paper_2011_11188_amd", "csrc", "gemm_lds.h")
+    if not os.path.exists(path) or "gemm_lds_kernel" not in kernel_desc:
+        return None
+    rec = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            rec[k.strip()] = v.strip()
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if rec.get("source_sha256") != digest or "bytes_per_launch" not in rec:
+        return None
+    return float(rec["bytes_per_launch"])
 
 
 def _cpu_baseline(cfg):
@@ -285,6 +316,19 @@ def main():
                 "avg_launch_ms": round(mpl, 4), "flop_per_launch": fpl}
     print(f"[bench] dominant kernel {roofline['kernel']}: {mpl:.4f} ms/launch, "
           f"{achieved:.1f} TFLOP/s", file=sys.stderr, flush=True)
+
+    # calibration for HBM-traffic counters: a plain fp32 copy of known size
+    # (256 MiB read + 256 MiB written per launch)
+    ncopy = 64 << 20
+    csrc = torch.empty(ncopy, dtype=torch.float32, device="cuda").normal_()
+    cdst = torch.empty_like(csrc)
+    for _ in range(3):
+        mdnn.mdnn_cast(ncopy, csrc, mdnn.F32, cdst, mdnn.F32)
+    _sync()
+    del csrc, cdst
+    traffic = _traffic_record(roofline["kernel"])
+    if traffic is not None:
+        roofline["traffic"] = traffic
 
     line = {
         "metric": METRIC, "value": round(samples, 1), "unit": "samples/s", "n_gpus": 1,
