@@ -3,6 +3,7 @@
 //   bwd_data:   M = n*h*w,   N = c_in,  K = r*s*c_out  (A = im2col of dy with flipped taps, B = w)
 //   bwd_filter: M = c_out,   N = r*s*c_in, K = n*Ho*Wo (A = dy^T, B = shifted x), split over K
 // No im2col buffer is materialised: the operand sources compute addresses.
+#include "conv_pipe.h"
 #include "gemm_launch.h"
 
 namespace mdnn {
@@ -21,6 +22,13 @@ static mdnn_status_t check_shape(const mdnn_conv_shape_t* s, ConvGeom& g) {
   g = ConvGeom{(int32_t)s->n, (int32_t)s->h, (int32_t)s->w, (int32_t)s->c_in, (int32_t)s->c_out,
                (int32_t)s->r, (int32_t)s->s, (int32_t)s->pad, (int32_t)ho, (int32_t)wo};
   return MDNN_SUCCESS;
+}
+
+// The pipelined kernels run unless a general tile is forced (tests of the
+// general path).
+static bool pipe_allowed() {
+  const int o = gemm_tile_override();
+  return !(o >= TILE_256x256 && o <= TILE_64x64);
 }
 
 static Epilogue plain_epilogue(void* D, int64_t ldd, mdnn_dtype_t d_type) {
@@ -120,6 +128,11 @@ extern "C" mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const v
   ep.act = act;
   clear_error();
   hipStream_t st = as_stream(stream);
+  if (pipe_allowed()) {
+    bool done = false;
+    MDNN_TRY(conv_pipe_fwd(g, x, w, ep, io_type, y_type, st, &done));
+    if (done) return MDNN_SUCCESS;
+  }
   switch (io_type) {
     case MDNN_F16: return fwd_impl<F16>(g, x, w, ep, y_type, st);
     case MDNN_BF16: return fwd_impl<BF16>(g, x, w, ep, y_type, st);
@@ -146,6 +159,11 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
   ep.ldm = g.c;
   clear_error();
   hipStream_t st = as_stream(stream);
+  if (pipe_allowed()) {
+    bool done = false;
+    MDNN_TRY(conv_pipe_bwd_data(g, dy, w, ep, io_type, dx_type, st, &done));
+    if (done) return MDNN_SUCCESS;
+  }
   switch (io_type) {
     case MDNN_F16: return bwd_data_impl<F16>(g, dy, w, ep, dx_type, st);
     case MDNN_BF16: return bwd_data_impl<BF16>(g, dy, w, ep, dx_type, st);
@@ -153,13 +171,17 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
   }
 }
 
-// Workspace: split-K partials of dw, then (256-byte aligned) the partial
+// Workspace: split-K partials of dw (room for the pipelined kernel's plan and
+// the general kernel's, whichever runs), then (256-byte aligned) the partial
 // column sums of db.
 static size_t filter_ws_split_bytes(const ConvGeom& g) {
-  SplitPlan p = filter_plan(g);
-  if (p.splits <= 1) return 0;
-  return ((size_t)p.splits * g.k * ((size_t)g.r * g.s * g.c) * sizeof(float) + 255) & ~(size_t)255;
+  const size_t mn = (size_t)g.k * ((size_t)g.r * g.s * g.c) * sizeof(float);
+  const SplitPlan p = filter_plan(g), q = conv_pipe_filter_plan(g);
+  size_t splits = p.splits > 1 ? (size_t)p.splits : 0;
+  if (q.splits > 1 && (size_t)q.splits > splits) splits = (size_t)q.splits;
+  return (splits * mn + 255) & ~(size_t)255;
 }
+
 
 extern "C" size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape,
                                                    mdnn_dtype_t io_type) {
@@ -191,10 +213,14 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
     MDNN_TRY(fill_zero(dw, (size_t)g.k * g.r * g.s * g.c * 4, st));
     return db ? fill_zero(db, (size_t)g.k * 4, st) : MDNN_SUCCESS;
   }
-  switch (io_type) {
-    case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st)); break;
-    case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st)); break;
-    default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st)); break;
+  bool done = false;
+  if (pipe_allowed()) MDNN_TRY(conv_pipe_bwd_filter(g, x, dy, dw, workspace, io_type, st, &done));
+  if (!done) {
+    switch (io_type) {
+      case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st)); break;
+      case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st)); break;
+      default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st)); break;
+    }
   }
   if (db) {
     const size_t off = filter_ws_split_bytes(g);

@@ -1,0 +1,157 @@
+// Implicit-GEMM convolutions (section 3.1's convolution layers, stride 1,
+// zero padding) on the pipelined mainloop of gemm_lds.h.  The im2col
+// operands are gathered straight into LDS by the convolution loaders; no
+// im2col buffer exists.
+//
+// Tiles (all 8 waves, 64 x 32 wave tiles):
+//   forward / backward data: 256 x 64 when N <= 64, else 128 x 128; 2 stages.
+//   backward filter: 64 x 256 when M <= 64, else 128 x 128; 3 stages and a
+//   split over K (output pixels) sized to fill the chip, reduced in split
+//   order (deterministic).
+#include "conv_pipe.h"
+#include "gemm_launch.h"
+
+namespace mdnn {
+
+namespace {
+
+typedef lds::Tile<256, 64, 4, 2, 4> TileTall;
+typedef lds::Tile<128, 128, 2, 4, 4> TileSquare;
+// backward filter: 3 stages leave room for one workgroup per CU
+typedef lds::Tile<64, 256, 2, 4, 2> TileWide;
+typedef lds::Tile<128, 128, 2, 4, 2> TileSquareF;
+constexpr int FILTER_STAGES = 3;
+constexpr size_t FILTER_WS_MAX = 64ull << 20;
+constexpr int64_t BUF_MAX = 0x7fffffffLL;  // range-checked buffers: offsets below 2^31
+
+uint32_t magic_of(uint32_t d) { return d == 1 ? 0u : (uint32_t)(((1ull << 32) + d - 1) / d); }
+
+template <class T, class OutT, class TL, class LB>
+mdnn_status_t run_rows(const lds::ConvRowsArgs& a, const typename LB::Args& b, int64_t M, int64_t N, int64_t K,
+                       const Epilogue& ep, hipStream_t st) {
+  return run_pipe<T, OutT, TL, 2, lds::ConvRowsLoader<TL::BM, TL::LA>, LB>(a, b, M, N, K, ep, 1, st);
+}
+
+// fwd (B = filter as a K-contiguous matrix) or bwd_data (B = TapWeightLoader)
+template <class T, class OutT, bool BWD>
+mdnn_status_t rows_dispatch(const lds::ConvRowsArgs& a, const void* w, int32_t ldw, const ConvGeom& g, int64_t M,
+                            int64_t N, int64_t K, const Epilogue& ep, hipStream_t st) {
+  if constexpr (!BWD) {
+    const lds::MatArgs b{w, ldw, N};
+    if (N <= 64) return run_rows<T, OutT, TileTall, lds::MatLoader<true, 64, TileTall::LB>>(a, b, M, N, K, ep, st);
+    return run_rows<T, OutT, TileSquare, lds::MatLoader<true, 128, TileSquare::LB>>(a, b, M, N, K, ep, st);
+  } else {
+    const lds::TapWeightArgs b{w, g.k, g.r * g.s, g.c};
+    if (N <= 64) return run_rows<T, OutT, TileTall, lds::TapWeightLoader<64, TileTall::LB>>(a, b, M, N, K, ep, st);
+    return run_rows<T, OutT, TileSquare, lds::TapWeightLoader<128, TileSquare::LB>>(a, b, M, N, K, ep, st);
+  }
+}
+
+template <bool BWD>
+mdnn_status_t rows_typed(const lds::ConvRowsArgs& a, const void* w, int32_t ldw, const ConvGeom& g, int64_t M,
+                         int64_t N, int64_t K, const Epilogue& ep, mdnn_dtype_t io, mdnn_dtype_t out,
+                         hipStream_t st) {
+  if (io == MDNN_F16)
+    return out == MDNN_F32 ? rows_dispatch<F16, F32, BWD>(a, w, ldw, g, M, N, K, ep, st)
+                           : rows_dispatch<F16, F16, BWD>(a, w, ldw, g, M, N, K, ep, st);
+  return out == MDNN_F32 ? rows_dispatch<BF16, F32, BWD>(a, w, ldw, g, M, N, K, ep, st)
+                         : rows_dispatch<BF16, BF16, BWD>(a, w, ldw, g, M, N, K, ep, st);
+}
+
+}  // namespace
+
+mdnn_status_t conv_pipe_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep,
+                            mdnn_dtype_t io, mdnn_dtype_t out, hipStream_t st, bool* done) {
+  *done = false;
+  const int64_t M = (int64_t)g.n * g.ho * g.wo, N = g.k, K = (int64_t)g.r * g.s * g.c;
+  const int64_t x_bytes = (int64_t)g.n * g.h * g.w * g.c * 2;
+  if (io == MDNN_F32 || g.c % 64 != 0 || !aligned(x, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
+  if (x_bytes > BUF_MAX || M > BUF_MAX || N * K * 2 >= ((int64_t)1 << 32)) return MDNN_SUCCESS;
+  const lds::ConvRowsArgs a{x, (uint32_t)x_bytes, g.h, g.w, g.c, g.ho, g.wo, g.s, g.pad, 0, M};
+  MDNN_TRY(rows_typed<false>(a, w, (int32_t)K, g, M, N, K, ep, io, out, st));
+  *done = true;
+  return MDNN_SUCCESS;
+}
+
+mdnn_status_t conv_pipe_bwd_data(const ConvGeom& g, const void* dy, const void* w, const Epilogue& ep,
+                                 mdnn_dtype_t io, mdnn_dtype_t out, hipStream_t st, bool* done) {
+  *done = false;
+  const int64_t M = (int64_t)g.n * g.h * g.w, N = g.c, K = (int64_t)g.r * g.s * g.k;
+  const int64_t dy_bytes = (int64_t)g.n * g.ho * g.wo * g.k * 2;
+  if (io == MDNN_F32 || g.k % 64 != 0 || g.c % 8 != 0 || !aligned(dy, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
+  const int64_t ldw = (int64_t)g.r * g.s * g.c;  // filter elements between consecutive c_out
+  if (dy_bytes > BUF_MAX || M > BUF_MAX || (64 * ldw + N) * 2 >= ((int64_t)1 << 32)) return MDNN_SUCCESS;
+  // rows over the h x w input grid, gathered from the ho x wo grid of dy
+  const lds::ConvRowsArgs a{dy, (uint32_t)dy_bytes, g.ho, g.wo, g.k, g.h, g.w, g.s, g.pad, 1, M};
+  MDNN_TRY(rows_typed<true>(a, w, 0, g, M, N, K, ep, io, out, st));
+  *done = true;
+  return MDNN_SUCCESS;
+}
+
+SplitPlan conv_pipe_filter_plan(const ConvGeom& g) {
+  SplitPlan p{0, 0};
+  const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
+  const int64_t x_bytes = (int64_t)g.n * g.h * g.w * g.c * 2;
+  if (g.ho != g.h || g.wo != g.w || g.c % 8 != 0 || g.k % 8 != 0 || K % lds::BK != 0 || K == 0) return p;
+  if (x_bytes > BUF_MAX || K * (g.w - 1) >= ((int64_t)1 << 32) || (K / g.w) * (g.h - 1) >= ((int64_t)1 << 32))
+    return p;
+  if (N > BUF_MAX / 4 || M * N > BUF_MAX / 4) return p;
+  // one workgroup per CU (3 stages), so aim at 256 workgroups; each split
+  // keeps at least 4 K steps and the partials stay within the cap
+  const int64_t tiles = M <= 64 ? ceil_div(N, TileWide::BN) : ceil_div(M, 128) * ceil_div(N, 128);
+  const int64_t steps = K / lds::BK;
+  int64_t s = ceil_div(256, tiles);
+  if (s > steps / 4) s = steps / 4;
+  while (s > 1 && (size_t)s * M * N * 4 > FILTER_WS_MAX) --s;
+  if (s < 1) s = 1;
+  const int64_t kps = ceil_div(steps, s) * lds::BK;
+  p.splits = (int)ceil_div(K, kps);
+  p.k_per_split = kps;
+  return p;
+}
+
+namespace {
+
+template <class T, class TL>
+mdnn_status_t filter_run(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws, const SplitPlan& p,
+                         hipStream_t st) {
+  const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
+  const lds::MatArgs a{dy, g.k, g.k};
+  const lds::ConvColsArgs b{x, (uint32_t)((int64_t)g.n * g.h * g.w * g.c * 2), g.h, g.w, g.c, g.s, g.pad,
+                            magic_of((uint32_t)g.w), magic_of((uint32_t)g.h), N};
+  Epilogue ep{};
+  ep.alpha = 1.0f;
+  ep.D = dw;
+  ep.ldd = N;
+  ep.act = MDNN_ACT_NONE;
+  ep.vec4 = (N % 4 == 0) && aligned(dw, 16);
+  ep.k_per_split = K;
+  if (p.splits > 1) {
+    ep.partial = (float*)ws;
+    ep.k_per_split = p.k_per_split;
+  }
+  MDNN_TRY((run_pipe<T, F32, TL, FILTER_STAGES, lds::MatLoader<false, TL::BM, TL::LA>,
+                     lds::ConvColsLoader<TL::BN, TL::LB>>(a, b, M, N, K, ep, p.splits, st)));
+  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st);
+  return MDNN_SUCCESS;
+}
+
+}  // namespace
+
+mdnn_status_t conv_pipe_bwd_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
+                                   mdnn_dtype_t io, hipStream_t st, bool* done) {
+  *done = false;
+  const SplitPlan p = conv_pipe_filter_plan(g);
+  if (io == MDNN_F32 || p.splits == 0 || !aligned(x, 16) || !aligned(dy, 16)) return MDNN_SUCCESS;
+  if (p.splits > 1 && (!ws || !aligned(ws, 16))) return MDNN_SUCCESS;
+  if (g.k <= 64)
+    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileWide>(g, x, dy, dw, ws, p, st)
+                             : filter_run<BF16, TileWide>(g, x, dy, dw, ws, p, st)));
+  else
+    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileSquareF>(g, x, dy, dw, ws, p, st)
+                             : filter_run<BF16, TileSquareF>(g, x, dy, dw, ws, p, st)));
+  *done = true;
+  return MDNN_SUCCESS;
+}
+
+}  // namespace mdnn

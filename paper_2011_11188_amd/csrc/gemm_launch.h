@@ -129,10 +129,24 @@ inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t 
 template <class T, class OutT, bool A_KC, bool B_KC>
 inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
                                   int64_t K, const Epilogue& ep, int splits, hipStream_t stream) {
-  dim3 grid((unsigned)(ceil_div(M, lds::BM) * ceil_div(N, lds::BN)), (unsigned)splits, 1);
-  lds::Operand oa{(const uint16_t*)a.p, a.ld, a.MN}, ob{(const uint16_t*)b.p, b.ld, b.MN};
-  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, A_KC, B_KC>), grid, dim3(lds::NT), 0, stream, oa,
-                     ob, M, N, K, ep);
+  typedef lds::Tile256 TL;
+  dim3 grid((unsigned)(ceil_div(M, TL::BM) * ceil_div(N, TL::BN)), (unsigned)splits, 1);
+  lds::MatArgs oa{a.p, a.ld, a.MN}, ob{b.p, b.ld, b.MN};
+  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, 2, lds::Mat256<A_KC>, lds::Mat256<B_KC>>), grid,
+                     dim3(TL::NT), 0, stream, oa, ob, M, N, K, ep);
+  return check_launch("gemm_lds_kernel");
+}
+
+// Pipelined kernel with explicit tile and loaders (the convolutions).
+template <class T, class OutT, class TL, int NS, class LA, class LB>
+inline mdnn_status_t run_pipe(const typename LA::Args& a, const typename LB::Args& b, int64_t M, int64_t N,
+                              int64_t K, const Epilogue& ep, int splits, hipStream_t stream) {
+  const int64_t tiles = ceil_div(M, TL::BM) * ceil_div(N, TL::BN);
+  if (tiles > 0x7fffffffLL || splits > 65535)
+    return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the launch grid");
+  dim3 grid((unsigned)tiles, (unsigned)splits, 1);
+  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, NS, LA, LB>), grid, dim3(TL::NT), 0, stream, a, b, M, N,
+                     K, ep);
   return check_launch("gemm_lds_kernel");
 }
 

@@ -4,7 +4,8 @@ definitions (fwd, bwd-data, bwd-filter; stride 1, zero padding, NHWC x KRSC).
 fp32 outputs: normalized max error <= 1e-4.  Low-precision outputs (with the
 bias+ReLU epilogue or the ReLU mask): one storage ulp plus the fp32
 accumulation bound.  Covers channel counts that are and are not multiples of
-8 (vector and element-wise operand paths), non-"same" padding, the LeNet-style
+8 (vector and element-wise operand paths), the pipelined kernels (c_in or
+c_out multiples of 64) next to the general ones, non-"same" padding, the LeNet-style
 layers (Cin = 1 and 32, 5x5) and the three ResNet-style 3x3 layers at their
 full size (batch 128), as launched by the benchmark.
 """
@@ -54,6 +55,75 @@ def test_conv_small_against_oracle(mdnn, shape, dt):
     assert norm_max_err(dx, ops.conv2d_bwd_data(dy, wt, pad, h, w)) <= TOL
     assert norm_max_err(dw, ops.conv2d_bwd_filter(x, dy, pad, r, s)) <= TOL
     assert norm_max_err(db, dy.sum(axis=(0, 1, 2))) <= TOL
+
+
+# Shapes on the pipelined kernels (forward: c_in % 64 == 0; backward data:
+# c_out % 64 == 0 and c_in % 8 == 0; backward filter: size-preserving, channels
+# multiples of 8, n*h*w % 64 == 0), with ragged M and N, non-square grids,
+# padding that changes the output size, 1x1 and 5x5 taps and split-K.
+PIPE = [  # n, h, w, c_in, c_out, r, s, pad
+    (2, 7, 9, 64, 72, 3, 3, 1),      # fwd, N = 72 (128 x 128 tile, ragged)
+    (3, 5, 6, 128, 64, 3, 3, 0),     # fwd + bwd_data with ho != h (valid conv)
+    (2, 8, 8, 64, 128, 5, 5, 2),     # all three; filter single split
+    (4, 16, 16, 64, 64, 1, 1, 0),    # 1x1; filter split-K on the 64-row tile
+    (2, 12, 10, 192, 40, 3, 3, 1),   # fwd, N = 40 (256 x 64 tile)
+    (5, 11, 13, 64, 64, 3, 3, 1),    # ragged M = 715
+    (8, 16, 16, 64, 256, 3, 3, 1),   # filter split-K on the 128 x 128 tile
+    (2, 8, 8, 16, 8, 3, 3, 1),       # filter with c_out = 8
+]
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("shape", PIPE)
+def test_conv_pipelined_against_oracle(mdnn, shape, dt):
+    n, h, w, ci, co, r, s, pad = shape
+    (x, wt, dy), (y, dx, dw, db) = _ops(mdnn, shape, dt, 17)
+    assert norm_max_err(y, ops.conv2d_fwd(x, wt, pad)) <= TOL
+    assert norm_max_err(dx, ops.conv2d_bwd_data(dy, wt, pad, h, w)) <= TOL
+    assert norm_max_err(dw, ops.conv2d_bwd_filter(x, dy, pad, r, s)) <= TOL
+    assert norm_max_err(db, dy.sum(axis=(0, 1, 2))) <= TOL
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_conv_pipelined_epilogues_lowp(mdnn, dt):
+    """Pipelined forward with bias+ReLU stored in the storage type, pipelined
+    backward-data with the ReLU mask, both with ragged M."""
+    import torch
+    n, h, w, ci, co, r, s, pad = 3, 7, 5, 64, 64, 3, 3, 1
+    x = W.normal((n, h, w, ci), 18, 1, dt, 0.3)
+    wt = W.normal((co, r, s, ci), 18, 2, dt, 0.1)
+    b = W.normal((co,), 18, 3, "f32", 0.2)
+    dy = W.normal((n, h, w, co), 18, 4, dt)
+    X, Wt = dev(x, dt), dev(wt, dt)
+    y = mdnn.conv2d_fwd(X, Wt, pad, bias=dev(b, "f32"), act=mdnn.ACT_RELU)
+    dx = mdnn.conv2d_bwd_data(dev(dy, dt), Wt, pad, h, w, mask=X)
+    torch.cuda.synchronize()
+    x64, w64, dy64 = decode(x, dt), decode(wt, dt), decode(dy, dt)
+    exact = ops.bias_act(ops.conv2d_fwd(x64, w64, pad), b.astype(np.float64), "relu")
+    err = accum_bound(ops.conv2d_fwd(np.abs(x64), np.abs(w64), pad) + np.abs(b), r * s * ci + 1)
+    assert lowp_close(host64(y), exact, dt, err)
+    exact_dx = np.where(x64 > 0, ops.conv2d_bwd_data(dy64, w64, pad, h, w), 0.0)
+    err = accum_bound(ops.conv2d_bwd_data(np.abs(dy64), np.abs(w64), pad, h, w), r * s * co)
+    assert lowp_close(host64(dx), exact_dx, dt, err)
+
+
+def test_conv_pipelined_integer_exact(mdnn):
+    """Small integers: every product and partial sum is exact in fp32, so the
+    pipelined kernels (padding zeros included) must match bit for bit."""
+    import torch
+    n, h, w, ci, co, r, s, pad = 2, 8, 8, 64, 64, 3, 3, 1
+    x = W.small_ints((n, h, w, ci), 19, 1, dtype="f16")
+    wt = W.small_ints((co, r, s, ci), 19, 2, dtype="f16")
+    dy = W.small_ints((n, h, w, co), 19, 3, dtype="f16")
+    X, Wt, DY = dev(x, "f16"), dev(wt, "f16"), dev(dy, "f16")
+    y = mdnn.conv2d_fwd(X, Wt, pad, out_dtype=torch.float32)
+    dx = mdnn.conv2d_bwd_data(DY, Wt, pad, h, w, out_dtype=torch.float32)
+    dwt, db = mdnn.conv2d_bwd_filter(X, DY, r, s, pad)
+    torch.cuda.synchronize()
+    x64, w64, dy64 = x.astype(np.float64), wt.astype(np.float64), dy.astype(np.float64)
+    assert np.array_equal(host64(y), ops.conv2d_fwd(x64, w64, pad))
+    assert np.array_equal(host64(dx), ops.conv2d_bwd_data(dy64, w64, pad, h, w))
+    assert np.array_equal(host64(dwt), ops.conv2d_bwd_filter(x64, dy64, pad, r, s))
 
 
 @pytest.mark.parametrize("tile", [1, 2, 3])
