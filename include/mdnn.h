@@ -103,7 +103,8 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
 
 /* Tuning knob for measurements (process-wide): force the MFMA kernel of the
  * GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128, 3 = 64x64
- * general kernels, 4 = the 256x256 direct-to-LDS pipelined kernel wherever its
+ * general kernels (convolutions then also use the general kernels), 4 / 5 =
+ * the 256x256 / 128x128 direct-to-LDS pipelined kernel wherever its
  * preconditions hold (K % 64 == 0, 16-byte aligned operands with leading
  * dimensions multiple of 8, MN-contiguous extents multiple of 8), the
  * automatic choice elsewhere.  Returns 0, or -1 for an unknown code.  Results

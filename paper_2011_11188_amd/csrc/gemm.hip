@@ -288,7 +288,7 @@ extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_
 }
 
 extern "C" int mdnn_set_gemm_tile(int code) {
-  if (code < 0 || code > 4) return -1;
+  if (code < 0 || code > TILE_LDS_PIPE128) return -1;
   g_tile_override.store(code, std::memory_order_relaxed);
   return 0;
 }

@@ -63,17 +63,25 @@ gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
   }
 }
 
-// Tile configurations of the MFMA kernels.  TILE_LDS_PIPE is the 256 x 256
-// direct-to-LDS pipelined mainloop (gemm_lds.h), used for plain matrices that
-// meet its preconditions.
-enum TileCfg { TILE_AUTO = 0, TILE_256x256 = 1, TILE_128x128 = 2, TILE_64x64 = 3, TILE_LDS_PIPE = 4 };
+// Tile configurations of the MFMA kernels.  TILE_LDS_PIPE / TILE_LDS_PIPE128
+// force the 256 x 256 / 128 x 128 direct-to-LDS pipelined mainloop
+// (gemm_lds.h) for plain matrices that meet its preconditions; TILE_AUTO
+// picks the tile by problem size.
+enum TileCfg {
+  TILE_AUTO = 0,
+  TILE_256x256 = 1,
+  TILE_128x128 = 2,
+  TILE_64x64 = 3,
+  TILE_LDS_PIPE = 4,
+  TILE_LDS_PIPE128 = 5
+};
 
 int gemm_tile_override();
 
 inline TileCfg choose_tile(int64_t M, int64_t N, int splits) {
   int o = gemm_tile_override();
   if (o >= TILE_256x256 && o <= TILE_64x64) return (TileCfg)o;
-  if (o == TILE_LDS_PIPE) return TILE_256x256;  // this path has no pipelined kernel
+  if (o >= TILE_LDS_PIPE) return TILE_256x256;  // this path has no pipelined kernel
   const int64_t t256 = ceil_div(M, 256) * ceil_div(N, 256) * splits;
   if (t256 >= 256) return TILE_256x256;
   const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128) * splits;
@@ -110,13 +118,15 @@ struct LdsOperand {
   bool kc;
 };
 
-// Whether the pipelined kernel can run this problem (see gemm_lds.h).
+// Whether the pipelined kernel can run this problem (see gemm_lds.h): the
+// 256 x 256 tile when it gives at least one tile per CU, else the 128 x 128
+// tile (8 waves of 64 x 32) when that gives at least 32 tiles.
 inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
                               int64_t K, int64_t k_per_split, int splits) {
   const int o = gemm_tile_override();
   if (o >= TILE_256x256 && o <= TILE_64x64) return false;
   if (K <= 0 || K % lds::BK != 0 || k_per_split % lds::BK != 0) return false;
-  if (o != TILE_LDS_PIPE && ceil_div(M, 256) * ceil_div(N, 256) * splits < 128) return false;
+  if (o < TILE_LDS_PIPE && ceil_div(M, 128) * ceil_div(N, 128) * splits < 32) return false;
   for (const LdsOperand* op : {&a, &b}) {
     if (!aligned(op->p, 16) || op->ld % 8 != 0) return false;
     const int64_t reach = op->kc ? (op->MN - 1) * op->ld + K : (int64_t)lds::BK * op->ld + op->MN;
@@ -126,14 +136,24 @@ inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t 
   return true;
 }
 
+template <class T, class OutT, class TL, bool A_KC, bool B_KC>
+inline void launch_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N, int64_t K,
+                            const Epilogue& ep, int splits, hipStream_t stream) {
+  dim3 grid((unsigned)(ceil_div(M, TL::BM) * ceil_div(N, TL::BN)), (unsigned)splits, 1);
+  lds::MatArgs oa{a.p, a.ld, a.MN}, ob{b.p, b.ld, b.MN};
+  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, 2, lds::MatLoader<A_KC, TL::BM, TL::LA>,
+                                           lds::MatLoader<B_KC, TL::BN, TL::LB>>),
+                     grid, dim3(TL::NT), 0, stream, oa, ob, M, N, K, ep);
+}
+
 template <class T, class OutT, bool A_KC, bool B_KC>
 inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
                                   int64_t K, const Epilogue& ep, int splits, hipStream_t stream) {
-  typedef lds::Tile256 TL;
-  dim3 grid((unsigned)(ceil_div(M, TL::BM) * ceil_div(N, TL::BN)), (unsigned)splits, 1);
-  lds::MatArgs oa{a.p, a.ld, a.MN}, ob{b.p, b.ld, b.MN};
-  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, 2, lds::Mat256<A_KC>, lds::Mat256<B_KC>>), grid,
-                     dim3(TL::NT), 0, stream, oa, ob, M, N, K, ep);
+  const int o = gemm_tile_override();
+  if (o == TILE_LDS_PIPE || (o != TILE_LDS_PIPE128 && ceil_div(M, 256) * ceil_div(N, 256) * splits >= 256))
+    launch_gemm_lds<T, OutT, lds::Tile256, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
+  else
+    launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
   return check_launch("gemm_lds_kernel");
 }
 

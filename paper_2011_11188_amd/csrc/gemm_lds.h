@@ -640,10 +640,10 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
     for (int j = 0; j < FN; ++j) epilogue_store4<T, OutT>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j]);
 }
 
-// The plain-GEMM configuration: 256 x 256 tile, 8 waves of 128 x 64.
+// Plain-GEMM configurations: 256 x 256 tile with 8 waves of 128 x 64, and
+// for problems with fewer tiles, 128 x 128 with 8 waves of 64 x 32.
 typedef Tile<256, 256, 2, 4> Tile256;
-template <bool KC>
-using Mat256 = MatLoader<KC, 256, Tile256::LA>;
+typedef Tile<128, 128, 2, 4, 4> Tile128;
 
 }  // namespace lds
 }  // namespace mdnn

@@ -145,3 +145,14 @@ def test_net_create_validates_the_chain(m):
 
 
 DT_CODE = {"f32": 0, "f16": 1, "bf16": 2}
+
+
+def test_gemm_tile_override_codes():
+    import paper_2011_11188_amd as m
+    try:
+        for code in range(6):
+            assert m.mdnn_set_gemm_tile(code) == 0
+        assert m.mdnn_set_gemm_tile(6) == -1
+        assert m.mdnn_set_gemm_tile(-1) == -1
+    finally:
+        m.mdnn_set_gemm_tile(0)

@@ -64,15 +64,17 @@ def test_gemm_ragged_all_tiles(mdnn, tile, dt, layout):
 
 
 # shapes the direct-to-LDS pipelined kernel accepts (K % 64 == 0, M and N
-# multiples of 8) but that are ragged with respect to its 256 x 256 tiles
+# multiples of 8) but that are ragged with respect to its 256 x 256 and
+# 128 x 128 tiles
 PIPE = [(312, 264, 192), (520, 776, 320), (1000, 1032, 448), (8, 8, 64), (64, 2056, 128),
         (264, 8, 1024)]
 
 
+@pytest.mark.parametrize("tile", [4, 5])
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
-def test_gemm_pipelined_kernel_ragged(mdnn, dt, layout):
-    mdnn.mdnn_set_gemm_tile(4)
+def test_gemm_pipelined_kernel_ragged(mdnn, dt, layout, tile):
+    mdnn.mdnn_set_gemm_tile(tile)
     try:
         for i, (m, n, k) in enumerate(PIPE):
             sa, sb = _shapes(layout, m, n, k)
