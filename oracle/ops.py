@@ -37,6 +37,45 @@ def gemm(layout: str, a: np.ndarray, b: np.ndarray, alpha: float = 1.0,
 
 
 # ---------------------------------------------------------------------------
+# fp32 products from fp16 matrix-core products: section 3.2's Eq. (1).  An
+# fp32 matrix is the scaled sum of two fp16 matrices, X ~ s1*X1 + s2*X2 with
+# s2 = 2^-11 * s1 (the well-scaled case the section spells out, for a
+# caller-chosen power of two s1): X1 = RNE16(X / s1) keeps the leading 11
+# significant bits, X2 = RNE16((X - s1*X1) / s2) the next 11.  The product
+# of two such matrices keeps three of the four fp16 products (the X2*Y2
+# term, 2^-22 below the leading one, is dropped).
+# ---------------------------------------------------------------------------
+
+SPLIT_SHIFT = 2.0 ** -11   # s2 / s1
+
+
+def split_f16(x: np.ndarray, scale: float) -> Tuple[np.ndarray, np.ndarray]:
+    """(X1, X2) of Eq. (1) as exact fp64 values of fp16 numbers."""
+    from .rounding import round_to
+    x = np.asarray(x, dtype=np.float64)
+    hi = round_to(x / scale, "f16")
+    with np.errstate(invalid="ignore"):
+        lo = round_to((x - scale * hi) / (scale * SPLIT_SHIFT), "f16")
+    return hi, lo
+
+
+def gemm_split3(layout: str, a: np.ndarray, b: np.ndarray, a_scale: float, b_scale: float,
+                alpha: float = 1.0, beta: float = 0.0, c: Optional[np.ndarray] = None) -> np.ndarray:
+    """alpha * (a1 b1 A1B1 + a1 b2 A1B2 + a2 b1 A2B1) + beta * C, exactly, for
+    the Eq. (1) splits of A (scale a1) and B (scale b1)."""
+    a1, a2 = split_f16(a, a_scale)
+    b1, b2 = split_f16(b, b_scale)
+    sa2, sb2 = a_scale * SPLIT_SHIFT, b_scale * SPLIT_SHIFT
+    prod = (a_scale * b_scale) * gemm(layout, a1, b1) + (a_scale * sb2) * gemm(layout, a1, b2) + \
+        (sa2 * b_scale) * gemm(layout, a2, b1)
+    return _axpby(alpha, prod, beta, c)
+
+
+def _axpby(alpha: float, x: np.ndarray, beta: float, c: Optional[np.ndarray]) -> np.ndarray:
+    return alpha * x + beta * c if beta != 0.0 else alpha * x
+
+
+# ---------------------------------------------------------------------------
 # Bias + ReLU epilogue and its backward (a fully connected / convolution
 # layer's activation; section 2.1 backpropagation).
 # ReLU keeps NaN (x < 0 is false for NaN); its derivative at 0 is 0 and the
