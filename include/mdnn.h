@@ -113,6 +113,40 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
 int mdnn_set_gemm_tile(int code);
 
 /* ---------------------------------------------------------------------------
+ * fp32 products on the fp16 matrix cores (section 3.2, Eq. (1)).
+ *
+ * mdnn_split_f16: the two-term fp16 split of an fp32 matrix at a power-of-two
+ * scale s,
+ *   hi = RNE16(x / s),   lo = RNE16((x / s - hi) * 2^11),
+ * so that x ~ s*hi + s*2^-11*lo to about 22 significant bits (the section's
+ * a2 = 2^-11 a1).  x is rows x cols fp32 with leading dimension ldx; hi and lo
+ * are fp16 with leading dimensions ldh, ldl (each >= cols).  |x| / s must stay
+ * below 65504 (larger values give inf / NaN); values below 2^-14 * s lose bits
+ * to fp16 subnormals.  Errors: MDNN_ERR_SHAPE for negative sizes or a scale
+ * that is not a positive power of two, MDNN_ERR_NULL, MDNN_ERR_LAYOUT,
+ * MDNN_ERR_MISALIGNED (x 4-byte, hi / lo 2-byte aligned).
+ */
+mdnn_status_t mdnn_split_f16(int64_t rows, int64_t cols, const float* x, int64_t ldx, float scale,
+                             void* hi, int64_t ldh, void* lo, int64_t ldl, mdnn_stream_t stream);
+
+/* D = alpha * op(A) op(B) + beta * C for fp32 A, B, C, D through three fp16
+ * MFMA products of the Eq. (1) splits of A (scale a_scale) and B (scale
+ * b_scale):  a b [A1 B1 + 2^-11 (A1 B2 + A2 B1)], each accumulated in fp32
+ * (the A2 B2 product, 2^-22 below the leading one, is dropped).  Layouts,
+ * leading dimensions and the beta == 0 rule as mdnn_gemm_mixed; scales are
+ * positive powers of two chosen so that |A| / a_scale and |B| / b_scale stay
+ * below 65504 (1 for data of moderate magnitude).  The caller provides
+ * mdnn_gemm_split3_workspace(M, N, K) bytes of 256-byte aligned device
+ * workspace (the split operands and one fp32 M x N product); C may alias D.
+ * Four or more launches on `stream`, no host synchronisation.
+ */
+size_t mdnn_gemm_split3_workspace(int64_t M, int64_t N, int64_t K);
+mdnn_status_t mdnn_gemm_split3(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, float alpha,
+                               const float* A, int64_t lda, float a_scale, const float* B, int64_t ldb,
+                               float b_scale, float beta, const float* C, int64_t ldc, float* D,
+                               int64_t ldd, void* workspace, size_t ws_bytes, mdnn_stream_t stream);
+
+/* ---------------------------------------------------------------------------
  * 2-D convolution as implicit GEMM (section 2.1: a convolution is an
  * interchangeable algorithm behind one operation).  Stride 1, zero padding
  * `pad`, output Ho = h + 2*pad - r + 1, Wo = w + 2*pad - s + 1 (both >= 1).

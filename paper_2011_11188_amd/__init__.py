@@ -81,6 +81,9 @@ _SIGS = {
     "mdnn_mse_loss": [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _i, _vp],
     "mdnn_sgd_update": [_i64, _vp, _vp, _vp, _vp, _i, _f, _f, _vp, _vp],
     "mdnn_cast": [_i64, _vp, _i, _vp, _i, _vp],
+    "mdnn_split_f16": [_i64, _i64, _vp, _i64, _f, _vp, _i64, _vp, _i64, _vp],
+    "mdnn_gemm_split3": [_i, _i64, _i64, _i64, _f, _vp, _i64, _f, _vp, _i64, _f, _f, _vp, _i64, _vp,
+                         _i64, _vp, C.c_size_t, _vp],
     "mdnn_net_create": [_vp, C.c_int32, _i64, _vp, _vp],
     "mdnn_net_sizes": [_vp, _vp, _vp],
     "mdnn_net_bind": [_vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp],
@@ -93,6 +96,8 @@ for _name, _args in _SIGS.items():
     _fn.restype = C.c_int
 _lib.mdnn_conv2d_bwd_filter_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_bwd_filter_workspace.restype = C.c_size_t
+_lib.mdnn_gemm_split3_workspace.argtypes = [_i64, _i64, _i64]
+_lib.mdnn_gemm_split3_workspace.restype = C.c_size_t
 _lib.mdnn_bias_act_bwd_workspace.argtypes = [_i64, _i64]
 _lib.mdnn_bias_act_bwd_workspace.restype = C.c_size_t
 _lib.mdnn_last_error.restype = C.c_char_p
@@ -149,6 +154,7 @@ def last_error() -> str:
 
 def exported_symbols():
     return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
+                                 "mdnn_gemm_split3_workspace",
                                  "mdnn_last_error",
                                  "mdnn_version", "mdnn_net_activation", "mdnn_net_destroy",
                                  "mdnn_set_gemm_tile"])
@@ -228,6 +234,20 @@ def mdnn_sgd_update(n, w32, g32, v32, w_lp, lp_type, lr, momentum, scaler, strea
 
 def mdnn_cast(n, src, src_type, dst, dst_type, stream=None):
     return _call("mdnn_cast", n, _p(src), src_type, _p(dst), dst_type, _s(stream))
+
+
+def mdnn_split_f16(rows, cols, x, ldx, scale, hi, ldh, lo, ldl, stream=None):
+    return _call("mdnn_split_f16", rows, cols, _p(x), ldx, scale, _p(hi), ldh, _p(lo), ldl, _s(stream))
+
+
+def mdnn_gemm_split3_workspace(M, N, K) -> int:
+    return _lib.mdnn_gemm_split3_workspace(M, N, K)
+
+
+def mdnn_gemm_split3(layout, M, N, K, alpha, A, lda, a_scale, B, ldb, b_scale, beta, Cm, ldc, D, ldd,
+                     workspace, ws_bytes, stream=None):
+    return _call("mdnn_gemm_split3", layout, M, N, K, alpha, _p(A), lda, a_scale, _p(B), ldb, b_scale,
+                 beta, _p(Cm), ldc, _p(D), ldd, _p(workspace), ws_bytes, _s(stream))
 
 
 def mdnn_net_create(layers, batch: int, cfg: TrainCfg) -> int:

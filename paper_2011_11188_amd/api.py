@@ -11,11 +11,12 @@ from typing import Optional, Sequence
 from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, LOSS_MSE, LOSS_XENT,
                NN, NT, TN, ConvShape, LayerDesc, Scaler, TrainCfg, dtype_of, mdnn_conv2d_bwd_data,
                mdnn_conv2d_bwd_filter, mdnn_conv2d_bwd_filter_workspace, mdnn_conv2d_fwd,
-               mdnn_gemm_mixed, mdnn_net_activation, mdnn_net_bind, mdnn_net_create,
-               mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp, mdnn_train_step)
+               mdnn_gemm_mixed, mdnn_gemm_split3, mdnn_gemm_split3_workspace, mdnn_net_activation,
+               mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
+               mdnn_split_f16, mdnn_train_step)
 
-__all__ = ["torch_dtype", "gemm", "conv_shape", "conv2d_fwd", "conv2d_bwd_data",
-           "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net"]
+__all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "pow2_scale", "conv_shape", "conv2d_fwd",
+           "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net"]
 
 
 def torch_dtype(code: int):
@@ -38,6 +39,45 @@ def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask
                     Cm.stride(0) if Cm is not None else 0, out, out.stride(0), dtype_of(out), bias,
                     act, mask, mask.stride(0) if mask is not None else 0, stream)
     return out
+
+
+def split_f16(x, scale: float = 1.0, stream=None):
+    """(hi, lo) fp16 tensors of the two-term split of a 2-D fp32 tensor."""
+    import torch
+    rows, cols = x.shape
+    hi = torch.empty((rows, cols), dtype=torch.float16, device=x.device)
+    lo = torch.empty_like(hi)
+    mdnn_split_f16(rows, cols, x, x.stride(0), scale, hi, cols, lo, cols, stream)
+    return hi, lo
+
+
+def gemm_split3(layout: int, A, B, a_scale: float = 1.0, b_scale: float = 1.0, alpha: float = 1.0,
+                beta: float = 0.0, Cm=None, out=None, stream=None):
+    """fp32 D = alpha op(A) op(B) + beta C through three fp16 MFMA products."""
+    import torch
+    if layout == TN:
+        K, M = A.shape
+    else:
+        M, K = A.shape
+    N = B.shape[0] if layout == NT else B.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    ws_bytes = mdnn_gemm_split3_workspace(M, N, K)
+    ws = torch.empty((max(ws_bytes, 256),), dtype=torch.uint8, device=A.device)
+    mdnn_gemm_split3(layout, M, N, K, alpha, A, A.stride(0), a_scale, B, B.stride(0), b_scale, beta, Cm,
+                     Cm.stride(0) if Cm is not None else 0, out, out.stride(0), ws, ws_bytes, stream)
+    return out
+
+
+def pow2_scale(x) -> float:
+    """A power-of-two split scale that puts max|x| in [2^14, 2^15): convenience
+    for callers whose data is not of moderate magnitude (reads max|x| back to
+    the host)."""
+    import math
+    m = float(x.abs().max().item()) if x.numel() else 0.0
+    if not math.isfinite(m) or m == 0.0:
+        return 1.0
+    return 2.0 ** (math.floor(math.log2(m)) - 14)
 
 
 def conv_shape(x_shape: Sequence[int], c_out: int, r: int, s: int, pad: int) -> ConvShape:

@@ -110,6 +110,36 @@ def test_other_entry_points_reject_bad_arguments(m):
     assert e.value.status == m.ERR_NULL
 
 
+def test_split_entry_points_reject_bad_arguments(m):
+    with pytest.raises(m.MdnnError) as e:                    # scale not a power of two
+        m.mdnn_split_f16(4, 4, FAKE, 4, 3.0, FAKE, 4, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:                    # ldh < cols
+        m.mdnn_split_f16(4, 4, FAKE, 4, 1.0, FAKE, 2, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_LAYOUT
+    with pytest.raises(m.MdnnError) as e:                    # misaligned x
+        m.mdnn_split_f16(4, 4, FAKE + 2, 4, 1.0, FAKE, 4, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_MISALIGNED
+    need = m.mdnn_gemm_split3_workspace(64, 32, 16)
+    assert need >= 2 * 64 * 16 * 2 + 2 * 16 * 32 * 2 + 64 * 32 * 4
+    assert m.mdnn_gemm_split3_workspace(-1, 2, 2) == 0
+    args = (0, 64, 32, 16, 1.0, FAKE, 16, 1.0, FAKE, 32, 1.0, 0.0, None, 0, FAKE, 32)
+    with pytest.raises(m.MdnnError) as e:                    # workspace too small
+        m.mdnn_gemm_split3(*args, FAKE, need - 256, stream=0)
+    assert e.value.status == m.ERR_WORKSPACE
+    with pytest.raises(m.MdnnError) as e:                    # workspace not 256-byte aligned
+        m.mdnn_gemm_split3(*args, FAKE + 16, need, stream=0)
+    assert e.value.status == m.ERR_WORKSPACE
+    bad_scale = (0, 64, 32, 16, 1.0, FAKE, 16, 0.75, FAKE, 32, 1.0, 0.0, None, 0, FAKE, 32)
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_gemm_split3(*bad_scale, FAKE, need, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:                    # NT: ldb < K
+        m.mdnn_gemm_split3(1, 64, 32, 16, 1.0, FAKE, 16, 1.0, FAKE, 8, 1.0, 0.0, None, 0, FAKE, 32,
+                           FAKE, need, stream=0)
+    assert e.value.status == m.ERR_LAYOUT
+
+
 def test_net_create_validates_the_chain(m):
     import workloads as W
     L = m.LayerDesc
