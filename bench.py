@@ -18,6 +18,8 @@ Also on the same JSON line:
   gemm_sweep    the fp16 GEMM sweep (M = N = K in 1024/4096/8192, NN/NT/TN);
   conv          the ResNet-style 3x3 layers (batch 128) fwd / bwd-data /
                 bwd-filter;
+  gemm_fp32_split3  fp32 GEMMs (4096, 8192) through three fp16 MFMA
+                products of the Eq. (1) splits, next to the native fp32 kernel;
   workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step.
 Only one GPU is used; --gpus > 1 exits with a message.
 """
@@ -107,8 +109,11 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
     aligned operands (mirrors the library's fixed table)."""
     cd = lambda a, b: -(-a // b)  # noqa: E731
     mn_contig = {"NN": [n], "NT": [], "TN": [m, n]}[layout]
-    if k % 64 == 0 and all(d % 8 == 0 for d in mn_contig) and cd(m, 256) * cd(n, 256) >= 128:
-        return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
+    if k % 64 == 0 and all(d % 8 == 0 for d in mn_contig):
+        if cd(m, 256) * cd(n, 256) >= 256:
+            return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
+        if cd(m, 128) * cd(n, 128) >= 32:
+            return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
     if cd(m, 256) * cd(n, 256) >= 256:
         return "gemm_mfma_kernel 256x256"
     if cd(m, 128) * cd(n, 128) >= 160:
@@ -149,22 +154,19 @@ def _replay_group(mdnn, net, cfg, group, reps):
     for c in calls:  # warm
         mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0, None, 0,
                              c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    # one event pair around every launch: the sum is the kernels' own time,
-    # without the gaps between back-to-back launches
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(reps * len(calls))]
+    # one event pair around `reps` back-to-back replays: launches are queued
+    # ahead of the GPU, so the mean is the kernels' own duration plus the
+    # (microsecond) dispatch gaps between them
     _sync()
-    i = 0
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
     for _ in range(reps):
         for c in calls:
-            evs[i][0].record()
             mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
                                  None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-            evs[i][1].record()
-            i += 1
+    b.record()
     _sync()
-    total = sum(a.elapsed_time(b) for a, b in evs)
-    return total / len(evs), flops
+    return a.elapsed_time(b) / (reps * len(calls)), flops
 
 
 def _gemm_sweep(mdnn, reps_scale=1.0):
@@ -192,6 +194,44 @@ def _gemm_sweep(mdnn, reps_scale=1.0):
             res[f"{layout}_{size}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
                                        "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
             del A, B, D
+    return res
+
+
+def _split3_sweep(mdnn):
+    """fp32 GEMMs through three fp16 MFMA products (section 3.2, Eq. (1)),
+    next to the native fp32 (VALU) kernel; inputs fp32 N(0,1)/sqrt(K)."""
+    import torch
+    import workloads as W
+    res = {}
+    for size in (4096, 8192):
+        for layout in W.GEMM_LAYOUTS:
+            a, b = W.gemm_operands(layout, size, size, size, dtype="f32")
+            A, B = torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()
+            D = torch.empty((size, size), dtype=torch.float32, device="cuda")
+            lay = {"NN": 0, "NT": 1, "TN": 2}[layout]
+            wsb = mdnn.mdnn_gemm_split3_workspace(size, size, size)
+            ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+            fns = {"split3": lambda: mdnn.mdnn_gemm_split3(lay, size, size, size, 1.0, A, A.stride(0), 1.0,
+                                                           B, B.stride(0), 1.0, 0.0, None, 0, D, size,
+                                                           ws, wsb)}
+            if size == 4096:
+                fns["native_f32"] = lambda: mdnn.mdnn_gemm_mixed(lay, size, size, size, 1.0, A, A.stride(0), B,
+                                                                 B.stride(0), 0, 0.0, None, 0, D, size, 0)
+            for name, fn in fns.items():
+                for _ in range(2):
+                    fn()
+                reps = 10 if size == 4096 else 4
+                with _Timer() as tm:
+                    for _ in range(reps):
+                        fn()
+                ms = tm.ms / reps
+                tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
+                ent = {"ms": round(ms, 4), "fp32_tflops": round(tf, 1),
+                       "vs_fp32_peak": round(tf / PEAK_F32_TFLOPS, 3)}
+                if name == "split3":   # three fp16 products of depth K on the matrix cores
+                    ent["mfma_frac"] = round(3 * tf / PEAK_F16_TFLOPS, 4)
+                res[f"{name}_{layout}_{size}"] = ent
+            del A, B, D, ws
     return res
 
 
@@ -226,23 +266,32 @@ def _conv_bench(mdnn, reps=20):
     return res
 
 
+def _traffic_key(kernel_desc: str) -> str:
+    """'NN f16 -> f16 256x256' style key of a step kernel description."""
+    tile = "256x256" if "256x256" in kernel_desc else "128x128"
+    parts = kernel_desc.split(", ")
+    return f"{parts[1]} {tile}"
+
+
 def _traffic_record(kernel_desc: str):
-    """HBM bytes per launch of the dominant kernel measured with rocprofv3
-    counters (profiles/), used only while the kernel source is unchanged."""
+    """HBM bytes per launch of a step kernel measured with rocprofv3 counters
+    (profiles/), used only while the kernel source is unchanged."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "gemm_lds_kernel_traffic.txt")
     src = os.path.join(ROOT, "paper_2011_11188_amd", "csrc", "gemm_lds.h")
     if not os.path.exists(path) or "gemm_lds_kernel" not in kernel_desc:
         return None
-    rec = {}
+    sha, recs = None, {}
     for ln in open(path):
-        if ":" in ln and not ln.startswith("#"):
-            k, v = ln.split(":", 1)
-            rec[k.strip()] = v.strip()
+        if ln.startswith("source_sha256:"):
+            sha = ln.split(":", 1)[1].strip()
+        elif ln.startswith("record:"):
+            f = [x.strip() for x in ln.split(":", 1)[1].split("|")]
+            recs[f[0]] = float(f[-1].split()[-1])
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if rec.get("source_sha256") != digest or "bytes_per_launch" not in rec:
+    if sha != digest:
         return None
-    return float(rec["bytes_per_launch"])
+    return recs.get(_traffic_key(kernel_desc))
 
 
 def _cpu_baseline(cfg):
@@ -349,6 +398,8 @@ def main():
         print("[bench] gemm sweep done", file=sys.stderr, flush=True)
         line["conv"] = _conv_bench(mdnn)
         print("[bench] conv done", file=sys.stderr, flush=True)
+        line["gemm_fp32_split3"] = _split3_sweep(mdnn)
+        print("[bench] fp32 split3 sweep done", file=sys.stderr, flush=True)
         wl = {}
         for c in (W.lenet_bf16(), W.mlp784_fp32()):
             n2, xs2, ts2 = _train_setup(mdnn, c)
