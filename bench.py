@@ -21,6 +21,10 @@ Also on the same JSON line:
   gemm_fp32_split3  fp32 GEMMs (4096, 8192) through three fp16 MFMA
                 products of the Eq. (1) splits, next to the native fp32 kernel;
   workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step.
+Every timed region follows sustained untimed load (about a second of the
+same work, or 3 runs of at least 50 ms with the median kept for the
+sub-benchmarks): the GPU's clocks settle under sustained load, which is the
+state a training run spends its time in.
 Only one GPU is used; --gpus > 1 exits with a message.
 """
 from __future__ import annotations
@@ -80,7 +84,47 @@ def _train_setup(mdnn, cfg, n_batches=10):
     return net, xs, ts
 
 
+WARM_SECONDS = 1.0   # sustained load before a timed region: the GPU's clock settles under it
+
+
+def _warm(fn, seconds=WARM_SECONDS):
+    """Run fn back to back for about `seconds` (untimed): GPU clocks ramp up
+    under sustained load, and a training run spends its life in that state."""
+    fn()
+    _sync()
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(max(1, 2 ** min(n, 6))):
+            fn()
+        _sync()
+        n += 1
+
+
+def _measure(fn, min_ms=50.0, chunks=3):
+    """Median per-call time (ms) over `chunks` back-to-back runs of at least
+    `min_ms` each, after a short warm-up."""
+    for _ in range(3):
+        fn()
+    with _Timer() as tm:
+        fn()
+    reps = max(3, int(min_ms / max(tm.ms, 1e-3)))
+    res = []
+    for _ in range(chunks):
+        with _Timer() as tm:
+            for _ in range(reps):
+                fn()
+        res.append(tm.ms / reps)
+    return sorted(res)[len(res) // 2]
+
+
 def _time_steps(net, xs, ts, steps, warmup):
+    it = iter(range(1 << 62))
+
+    def one():
+        i = next(it)
+        net.step(xs[i % len(xs)], ts[i % len(ts)])
+    _warm(one)
     for i in range(warmup):
         net.step(xs[i % len(xs)], ts[i % len(ts)])
     with _Timer() as tm:
@@ -157,16 +201,11 @@ def _replay_group(mdnn, net, cfg, group, reps):
     # one event pair around `reps` back-to-back replays: launches are queued
     # ahead of the GPU, so the mean is the kernels' own duration plus the
     # (microsecond) dispatch gaps between them
-    _sync()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
+    def replay():
         for c in calls:
             mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
                                  None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    b.record()
-    _sync()
-    return a.elapsed_time(b) / (reps * len(calls)), flops
+    return _measure(replay, min_ms=max(50.0, reps)) / len(calls), flops
 
 
 def _gemm_sweep(mdnn, reps_scale=1.0):
@@ -183,13 +222,7 @@ def _gemm_sweep(mdnn, reps_scale=1.0):
             def run():
                 mdnn.mdnn_gemm_mixed(lay, size, size, size, 1.0, A, A.stride(0), B, B.stride(0), 1,
                                      0.0, None, 0, D, size, 0)
-            for _ in range(3):
-                run()
-            reps = max(5, int(reps_scale * {1024: 200, 4096: 40, 8192: 10}[size]))
-            with _Timer() as tm:
-                for _ in range(reps):
-                    run()
-            ms = tm.ms / reps
+            ms = _measure(run, min_ms=50.0 * reps_scale)
             tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
             res[f"{layout}_{size}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
                                        "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
@@ -218,13 +251,7 @@ def _split3_sweep(mdnn):
                 fns["native_f32"] = lambda: mdnn.mdnn_gemm_mixed(lay, size, size, size, 1.0, A, A.stride(0), B,
                                                                  B.stride(0), 0, 0.0, None, 0, D, size, 0)
             for name, fn in fns.items():
-                for _ in range(2):
-                    fn()
-                reps = 10 if size == 4096 else 4
-                with _Timer() as tm:
-                    for _ in range(reps):
-                        fn()
-                ms = tm.ms / reps
+                ms = _measure(fn, min_ms=40.0, chunks=3)
                 tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
                 ent = {"ms": round(ms, 4), "fp32_tflops": round(tf, 1),
                        "vs_fp32_peak": round(tf / PEAK_F32_TFLOPS, 3)}
@@ -254,12 +281,7 @@ def _conv_bench(mdnn, reps=20):
             "bwd_filter": lambda: mdnn.mdnn_conv2d_bwd_filter(cs, X, DY, 1, dw, None, ws, wsb),
         }
         for op, fn in fns.items():
-            for _ in range(3):
-                fn()
-            with _Timer() as tm:
-                for _ in range(reps):
-                    fn()
-            ms = tm.ms / reps
+            ms = _measure(fn, min_ms=30.0)
             tf = sh.flops() / (ms * 1e-3) / 1e12
             res[f"L{li + 1}_{sh.c_in}x{sh.h}_{op}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
                                                        "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}

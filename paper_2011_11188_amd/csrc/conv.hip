@@ -157,6 +157,7 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
   Epilogue ep = plain_epilogue(dx, g.c, dx_type);
   ep.mask = mask_src;
   ep.ldm = g.c;
+  ep.vec4_m = mask_src && (g.c % 4 == 0) && aligned(mask_src, 4 * es);
   clear_error();
   hipStream_t st = as_stream(stream);
   if (pipe_allowed()) {

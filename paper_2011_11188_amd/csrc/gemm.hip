@@ -271,6 +271,8 @@ extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_
   ep.ldm = ldm;
   ep.act = act;
   ep.vec4 = (ldd % 4 == 0) && aligned(D, 4 * ds);
+  ep.vec4_c = beta != 0.0f && (ldc % 4 == 0) && aligned(C, 4 * ds);
+  ep.vec4_m = mask_src && (ldm % 4 == 0) && aligned(mask_src, 4 * es);
   ep.partial = nullptr;
   ep.k_per_split = K;
   hipStream_t st = as_stream(stream);

@@ -250,31 +250,62 @@ struct Epilogue {
   const void* mask;    // ab_type [M, ldm] or null
   int64_t ldm;
   int32_t act;
-  int32_t vec4;        // 4-wide stores allowed (ldd, ldc, ldm % 4 == 0 and aligned bases)
+  int32_t vec4;        // 4-wide stores of D allowed (ldd % 4 == 0, D aligned to 4 elements)
+  int32_t vec4_c;      // 4-wide loads of C allowed (ldc % 4 == 0, C aligned to 4 elements)
+  int32_t vec4_m;      // 4-wide loads of the mask allowed (ldm % 4 == 0, mask aligned to 4 elements)
   float* partial;      // split-K: fp32 [splits][M][N]; null otherwise
   int64_t k_per_split; // multiple of GEMM_BK
 };
+
+// Four consecutive stored elements as floats, in one vector load (p aligned
+// to four elements).
+template <class T>
+__device__ __forceinline__ void load4(const typename T::storage* p, float (&o)[4]) {
+  if constexpr (sizeof(typename T::storage) == 4) {
+    const float4 q = *(const float4*)p;
+    o[0] = q.x, o[1] = q.y, o[2] = q.z, o[3] = q.w;
+  } else {
+    const uint2 q = *(const uint2*)p;
+    o[0] = to_f<T>((uint16_t)(q.x & 0xffffu));
+    o[1] = to_f<T>((uint16_t)(q.x >> 16));
+    o[2] = to_f<T>((uint16_t)(q.y & 0xffffu));
+    o[3] = to_f<T>((uint16_t)(q.y >> 16));
+  }
+}
 
 template <class MaskT, class OutT>
 __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, int64_t N, int64_t m,
                                                 int64_t n, float4_t acc) {
   if (m >= M) return;
   float v[4] = {acc[0], acc[1], acc[2], acc[3]};
-  const bool full = ep.vec4 && n + 4 <= N;
+  const bool in4 = n + 4 <= N;
+  const bool full = ep.vec4 && in4;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     v[e] *= ep.alpha;
   }
   if (ep.beta != 0.0f) {
     const typename OutT::storage* c = (const typename OutT::storage*)ep.C + m * ep.ldc + n;
+    if (ep.vec4_c && in4) {
+      float cv[4];
+      load4<OutT>(c, cv);
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (n + e < N) v[e] += ep.beta * to_f<OutT>(c[e]);
+      for (int e = 0; e < 4; ++e) v[e] += ep.beta * cv[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N) v[e] += ep.beta * to_f<OutT>(c[e]);
+    }
   }
   if (ep.bias) {
+    if (in4 && ((uintptr_t)(ep.bias + n) & 15) == 0) {
+      const float4 b = *(const float4*)(ep.bias + n);
+      v[0] += b.x, v[1] += b.y, v[2] += b.z, v[3] += b.w;
+    } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (n + e < N) v[e] += ep.bias[n + e];
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N) v[e] += ep.bias[n + e];
+    }
   }
   if (ep.act == MDNN_ACT_RELU) {
 #pragma unroll
@@ -282,9 +313,17 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
   }
   if (ep.mask) {
     const typename MaskT::storage* mk = (const typename MaskT::storage*)ep.mask + m * ep.ldm + n;
+    if (ep.vec4_m && in4) {
+      float mv[4];
+      load4<MaskT>(mk, mv);
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (n + e < N && !(to_f<MaskT>(mk[e]) > 0.0f)) v[e] = 0.0f;
+      for (int e = 0; e < 4; ++e)
+        if (!(mv[e] > 0.0f)) v[e] = 0.0f;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N && !(to_f<MaskT>(mk[e]) > 0.0f)) v[e] = 0.0f;
+    }
   }
   typename OutT::storage* d = (typename OutT::storage*)ep.D + m * ep.ldd + n;
   if (full) {

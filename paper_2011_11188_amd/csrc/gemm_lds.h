@@ -185,6 +185,11 @@ struct MatLoader {
 #pragma unroll
     for (int i = 0; i < L; ++i) dma_global(kb, off[i], dst + (uint32_t)i * 1024u);
   }
+  // load i alone (loads of one tile may be issued one at a time, in any order)
+  static constexpr bool SPLIT_ISSUE = true;
+  __device__ __forceinline__ void issue_one(int t, uint32_t dst, int i) {
+    dma_global(base + (int64_t)t * step, off[i], dst + (uint32_t)i * 1024u);
+  }
 };
 
 // im2col rows: GEMM row m = (n, i, j) over an ho x wo grid, GEMM column
@@ -203,6 +208,7 @@ struct ConvRowsArgs {
 template <int W, int L>
 struct ConvRowsLoader {
   static constexpr bool KC = true;
+  static constexpr bool SPLIT_ISSUE = false;  // the per-step state advances once per tile
   typedef ConvRowsArgs Args;
   int4_t rsrc;
   int32_t hs, ws, c, s, pad, flip, cb_n;
@@ -263,6 +269,7 @@ struct TapWeightArgs {
 template <int W, int L>
 struct TapWeightLoader {
   static constexpr bool KC = false;
+  static constexpr bool SPLIT_ISSUE = false;  // the per-step state advances once per tile
   typedef TapWeightArgs Args;
   const char* p;
   int64_t kstride;  // bytes between consecutive k
@@ -312,6 +319,7 @@ struct ConvColsArgs {
 template <int W, int L>
 struct ConvColsLoader {
   static constexpr bool KC = false;
+  static constexpr bool SPLIT_ISSUE = false;  // the per-step state advances once per tile
   typedef ConvColsArgs Args;
   int4_t rsrc;
   int32_t h, w;
@@ -442,6 +450,14 @@ __device__ __forceinline__ void interleave_reads_mfma() {
   }
 }
 
+// LDS instructions of fragments F0 .. F1-1 (A's FM fragments, then B's)
+template <bool A_KC, bool B_KC, int FM>
+constexpr int chunk_reads(int f0, int f1) {
+  int r = 0;
+  for (int f = f0; f < f1; ++f) r += (f < FM ? (A_KC ? 1 : 2) : (B_KC ? 1 : 2));
+  return r;
+}
+
 // LDS stages are separate objects so that the compiler can prove a stage
 // being filled by LDS-DMA does not alias the stage being read: otherwise it
 // waits for every outstanding load before each fragment read, which
@@ -479,9 +495,16 @@ __device__ __forceinline__ void wait_tiles(int ahead) {
   }
 }
 
+template <class T, class TL, class LA, class LB, int C>
+__device__ __forceinline__ void spread_chunk(int tn, uint32_t dst_a, uint32_t dst_b, const char* sa, const char* sb,
+                                             int wm, int wn, const LaneFrag& fa_l, const LaneFrag& fb_l, LA& la, LB& lb,
+                                             Frags<TL>& f0, const Frags<TL>& f1, float4_t (&acc)[TL::FM][TL::FN]);
+
 // One K step of the pipeline: tile t in stage S = t % NS (see the kernel).
 // f0 holds k-step 0 of tile t on entry and k-step 0 of tile t+1 on exit.
-template <class T, class TL, int NS, class LA, class LB, int S>
+// CHECK = false is the steady state (t + NS < nk): no conditions, so each
+// half step is one basic block whose LDS reads interleave with its MFMAs.
+template <class T, class TL, int NS, class LA, class LB, int S, bool CHECK>
 __device__ __forceinline__ void pipeline_step(int t, int nk, const Stages<NS>& st, int wave, LaneFrag fa_l,
                                               LaneFrag fb_l, int wm, int wn, LA& la, LB& lb, Frags<TL>& f0,
                                               Frags<TL>& f1, float4_t (&acc)[TL::FM][TL::FN]) {
@@ -500,14 +523,24 @@ __device__ __forceinline__ void pipeline_step(int t, int nk, const Stages<NS>& s
     for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::run(f0.b[j], f0.a[i], acc[i][j]);
   interleave_reads_mfma<READS, FM * FN>();
   // this wave's reads of stage S, and its loads of tile t+1
-  const int newest = t + NS - 1 < nk - 1 ? t + NS - 1 : nk - 1;
-  wait_tiles<NS - 2, TL::LA + TL::LB>(newest - (t + 1));
+  if constexpr (CHECK) {
+    const int newest = t + NS - 1 < nk - 1 ? t + NS - 1 : nk - 1;
+    wait_tiles<NS - 2, TL::LA + TL::LB>(newest - (t + 1));
+  } else {
+    wait_vm_lgkm0<(NS - 2) * (TL::LA + TL::LB)>();
+  }
   __syncthreads();
-  if (t + NS < nk) {
+  if constexpr (!CHECK && LA::SPLIT_ISSUE && LB::SPLIT_ISSUE) {
+    spread_chunk<T, TL, LA, LB, 0>(t + NS, lds_address(st.a[S]) + (uint32_t)(wave * TL::LA) * 1024u,
+                                   lds_address(st.b[S]) + (uint32_t)(wave * TL::LB) * 1024u, st.a[S1], st.b[S1], wm,
+                                   wn, fa_l, fb_l, la, lb, f0, f1, acc);
+    return;
+  }
+  if (!CHECK || t + NS < nk) {
     la.issue(t + NS, lds_address(st.a[S]) + (uint32_t)(wave * TL::LA) * 1024u);
     lb.issue(t + NS, lds_address(st.b[S]) + (uint32_t)(wave * TL::LB) * 1024u);
   }
-  if (t + 1 < nk) {
+  if (!CHECK || t + 1 < nk) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) f0.a[i] = fragment<LA::KC, TL::BM>(st.a[S1], wm * TL::WTM + i * 16, 0, fa_l);
 #pragma unroll
@@ -520,16 +553,55 @@ __device__ __forceinline__ void pipeline_step(int t, int nk, const Stages<NS>& s
   interleave_reads_mfma<READS, FM * FN>();
 }
 
+// Second half of a steady-state K step with the LDS-DMA loads of tile t+NS
+// spread over it: chunk C issues load C (A's loads, then B's), then its
+// share of the next tile's fragment reads and of this k-step's MFMAs.
+// Issuing all of a step's loads at once right after the barrier stalls the
+// issuing waves while the loads queue; spread out, they hide behind MFMAs.
+template <class T, class TL, class LA, class LB, int C>
+__device__ __forceinline__ void spread_chunk(int tn, uint32_t dst_a, uint32_t dst_b, const char* sa, const char* sb,
+                                             int wm, int wn, const LaneFrag& fa_l, const LaneFrag& fb_l, LA& la, LB& lb,
+                                             Frags<TL>& f0, const Frags<TL>& f1, float4_t (&acc)[TL::FM][TL::FN]) {
+  constexpr int FM = TL::FM, FN = TL::FN, NL = TL::LA + TL::LB;
+  if constexpr (C < NL) {
+    if constexpr (C < TL::LA)
+      la.issue_one(tn, dst_a, C);
+    else
+      lb.issue_one(tn, dst_b, C - TL::LA);
+    __builtin_amdgcn_sched_barrier(0);
+    constexpr int NFR = FM + FN, F0 = C * NFR / NL, F1 = (C + 1) * NFR / NL;
+    constexpr int MF = FM * FN, M0 = C * MF / NL, M1 = (C + 1) * MF / NL;
+    int reads = 0;
+#pragma unroll
+    for (int f = F0; f < F1; ++f) {
+      if (f < FM) {
+        f0.a[f] = fragment<LA::KC, TL::BM>(sa, wm * TL::WTM + f * 16, 0, fa_l);
+        reads += LA::KC ? 1 : 2;
+      } else {
+        f0.b[f - FM] = fragment<LB::KC, TL::BN>(sb, wn * TL::WTN + (f - FM) * 16, 0, fb_l);
+        reads += LB::KC ? 1 : 2;
+      }
+    }
+    (void)reads;
+#pragma unroll
+    for (int m = M0; m < M1; ++m) acc[m / FN][m % FN] = Mfma<T>::run(f1.b[m % FN], f1.a[m / FN], acc[m / FN][m % FN]);
+    constexpr int R = chunk_reads<LA::KC, LB::KC, FM>(F0, F1);
+    if constexpr (R > 0) interleave_reads_mfma<R, M1 - M0>();
+    __builtin_amdgcn_sched_barrier(0);
+    spread_chunk<T, TL, LA, LB, C + 1>(tn, dst_a, dst_b, sa, sb, wm, wn, fa_l, fb_l, la, lb, f0, f1, acc);
+  }
+}
+
 // Steps t + J .. t + U - 1 of one unrolled round, U = lcm(NS, 2): the stage
 // index J % NS is a compile-time constant.
-template <class T, class TL, int NS, class LA, class LB, int J, int U>
+template <class T, class TL, int NS, class LA, class LB, int J, int U, bool CHECK>
 __device__ __forceinline__ void pipeline_round(int t, int nk, const Stages<NS>& st, int wave, LaneFrag fa_l,
                                                LaneFrag fb_l, int wm, int wn, LA& la, LB& lb, Frags<TL>& f0,
                                                Frags<TL>& f1, float4_t (&acc)[TL::FM][TL::FN]) {
   if constexpr (J < U) {
-    if (t + J >= nk) return;
-    pipeline_step<T, TL, NS, LA, LB, J % NS>(t + J, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
-    pipeline_round<T, TL, NS, LA, LB, J + 1, U>(t, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
+    if (CHECK && t + J >= nk) return;
+    pipeline_step<T, TL, NS, LA, LB, J % NS, CHECK>(t + J, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
+    pipeline_round<T, TL, NS, LA, LB, J + 1, U, CHECK>(t, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
   }
 }
 
@@ -610,8 +682,15 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
     for (int j = 0; j < FN; ++j) f0.b[j] = fragment<LB::KC, TL::BN>(st.b[0], wn * TL::WTN + j * 16, 0, fb_l);
   }
   constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
-  for (int t = 0; t < nk; t += U)
-    pipeline_round<T, TL, NS, LA, LB, 0, U>(t, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
+  // the unconditional steady state needs a few more live registers; with two
+  // MN-contiguous operands (more address terms) the 256 x 256 tile would spill
+  constexpr bool STEADY = LA::KC || LB::KC || TL::FM * TL::FN < 32;
+  int t = 0;
+  if constexpr (STEADY)
+    for (; t + U - 1 + NS < nk; t += U)  // every step of the round still issues a tile
+      pipeline_round<T, TL, NS, LA, LB, 0, U, false>(t, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
+  for (; t < nk; t += U)
+    pipeline_round<T, TL, NS, LA, LB, 0, U, true>(t, nk, st, wave, fa_l, fb_l, wm, wn, la, lb, f0, f1, acc);
 
   const int64_t mb = m0 + wm * TL::WTM + (lane & 15);
   const int64_t nb = n0 + wn * TL::WTN + 4 * (lane >> 4);
