@@ -93,18 +93,20 @@ class OracleNet:
     def w_lp(self) -> np.ndarray:
         return self.R(self.w32)
 
-    def _wb(self, wl: np.ndarray, i: int):
+    def _wb(self, wl: np.ndarray, i: int, w32: Optional[np.ndarray] = None):
         l = self.layers[i]
         wo, bo, nw, nb = self.offsets[i]
         if l.kind == FC:
             w = wl[wo:wo + nw].reshape(l.c_in, l.c_out)
         else:
             w = wl[wo:wo + nw].reshape(l.c_out, l.r, l.s, l.c_in)
-        return w, self.w32[bo:bo + nb]
+        return w, (self.w32 if w32 is None else w32)[bo:bo + nb]
 
     # -- forward / backward -------------------------------------------------
-    def forward(self, x: np.ndarray, wl: Optional[np.ndarray] = None):
-        """Returns (stored activations a_0..a_L, pool argmaxes, output)."""
+    def forward(self, x: np.ndarray, wl: Optional[np.ndarray] = None,
+                w32: Optional[np.ndarray] = None):
+        """Returns (stored activations a_0..a_L, pool argmaxes, output).  The
+        biases come from the fp32 weights w32 (default: the current ones)."""
         wl = self.w_lp() if wl is None else wl
         b = self.batch
         a = self.R(np.asarray(x, np.float64).reshape(b, -1))
@@ -113,10 +115,10 @@ class OracleNet:
         for i, l in enumerate(self.layers):
             last = i == n_l - 1
             if l.kind == FC:
-                w, bias = self._wb(wl, i)
+                w, bias = self._wb(wl, i, w32)
                 z = a.reshape(b, -1) @ w + bias
             elif l.kind == CONV:
-                w, bias = self._wb(wl, i)
+                w, bias = self._wb(wl, i, w32)
                 z = ops.conv2d_fwd(a.reshape(b, l.h, l.w, l.c_in), w, l.pad) + bias
             else:
                 z, args[i] = ops.maxpool2_fwd(a.reshape(b, l.h, l.w, l.c_in))
