@@ -271,6 +271,16 @@ mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v3
                               mdnn_dtype_t lp_type, float lr, float momentum,
                               mdnn_scaler_t* scaler, mdnn_stream_t stream);
 
+/* Asynchronous variant (section 4.1: asynchronous SGD with lock-free updates
+ * of a shared parameter vector): the same check and state machine, but the
+ * step -lr*v (or -lr*g) is added to w32 with fp32 atomics, so several streams
+ * may update one w32 concurrently without losing updates; no working copy is
+ * written.  The order of concurrent updates (hence the rounding of w32) is
+ * not deterministic.  v32 and the scaler belong to the caller of this update
+ * (one per worker).  g32 16-byte aligned when a scaler is given. */
+mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const float* g32, float* v32, float lr,
+                                    float momentum, mdnn_scaler_t* scaler, mdnn_stream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Precision conversion (section 3.2: fp32 data stored as fp16 or bf16).
  * dst[i] = convert(src[i]) for i < n, round to nearest even.
@@ -333,6 +343,16 @@ mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream);
  * loss_out: device fp32 scalar, the unscaled loss of this step's forward pass. */
 mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
                               float* loss_out, mdnn_stream_t stream);
+/* Asynchronous step (section 4.1): for several nets bound to the same
+ * master_w (each with its own grads, momentum, lowp_w, workspace and scaler)
+ * stepping concurrently on different streams.  The step first re-derives its
+ * working copy from the shared master weights (fp32 nets read them directly),
+ * runs forward, loss and backward, then adds its update to the shared
+ * weights with mdnn_sgd_update_async.  Reads may see other workers' updates
+ * part-applied and gradients may be stale: results are not deterministic,
+ * by design.  A net sharing master_w must only use this step. */
+mdnn_status_t mdnn_train_step_async(mdnn_net_t* net, const float* x, const void* target,
+                                    float* loss_out, mdnn_stream_t stream);
 /* Device pointer of stored activation i (0 = the low-precision input, i = output
  * of layer i-1) inside the bound workspace, for inspection; NULL if invalid. */
 const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i);

@@ -81,6 +81,8 @@ _SIGS = {
     "mdnn_mse_loss": [_i64, _i64, _vp, _vp, _vp, _vp, _vp, _i, _vp],
     "mdnn_sgd_update": [_i64, _vp, _vp, _vp, _vp, _i, _f, _f, _vp, _vp],
     "mdnn_cast": [_i64, _vp, _i, _vp, _i, _vp],
+    "mdnn_sgd_update_async": [_i64, _vp, _vp, _vp, _f, _f, _vp, _vp],
+    "mdnn_train_step_async": [_vp, _vp, _vp, _vp, _vp],
     "mdnn_split_f16": [_i64, _i64, _vp, _i64, _f, _vp, _i64, _vp, _i64, _vp],
     "mdnn_gemm_split3": [_i, _i64, _i64, _i64, _f, _vp, _i64, _f, _vp, _i64, _f, _f, _vp, _i64, _vp,
                          _i64, _vp, C.c_size_t, _vp],
@@ -234,6 +236,15 @@ def mdnn_sgd_update(n, w32, g32, v32, w_lp, lp_type, lr, momentum, scaler, strea
 
 def mdnn_cast(n, src, src_type, dst, dst_type, stream=None):
     return _call("mdnn_cast", n, _p(src), src_type, _p(dst), dst_type, _s(stream))
+
+
+def mdnn_sgd_update_async(n, w32, g32, v32, lr, momentum, scaler=None, stream=None):
+    return _call("mdnn_sgd_update_async", n, _p(w32), _p(g32), _p(v32), lr, momentum, _p(scaler),
+                 _s(stream))
+
+
+def mdnn_train_step_async(net, x, target, loss_out, stream=None):
+    return _call("mdnn_train_step_async", net, _p(x), _p(target), _p(loss_out), _s(stream))
 
 
 def mdnn_split_f16(rows, cols, x, ldx, scale, hi, ldh, lo, ldl, stream=None):

@@ -13,7 +13,7 @@ from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, L
                mdnn_conv2d_bwd_filter, mdnn_conv2d_bwd_filter_workspace, mdnn_conv2d_fwd,
                mdnn_gemm_mixed, mdnn_gemm_split3, mdnn_gemm_split3_workspace, mdnn_net_activation,
                mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
-               mdnn_split_f16, mdnn_train_step)
+               mdnn_split_f16, mdnn_train_step, mdnn_train_step_async)
 
 __all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "pow2_scale", "conv_shape", "conv2d_fwd",
            "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net"]
@@ -138,7 +138,9 @@ class Net:
 
     def __init__(self, layers, batch: int, dtype: int, loss: int, lr: float,
                  momentum: float = 0.0, loss_scaling: bool = False, init_scale: float = 1.0,
-                 n_classes: int = 10, device="cuda"):
+                 n_classes: int = 10, device="cuda", shared_master=None):
+        """shared_master: another Net's `master` tensor to bind instead of a
+        private one (asynchronous workers; step with step_async only)."""
         import torch
         descs = [LayerDesc(l.kind, l.act, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.pad) for l in layers]
         self.cfg = TrainCfg(dtype, loss, lr, momentum, 1 if loss_scaling else 0,
@@ -148,7 +150,12 @@ class Net:
         self.dtype = dtype
         self.n_params, self.ws_bytes = mdnn_net_sizes(self.handle)
         dev = torch.device(device)
-        self.master = torch.zeros(self.n_params, dtype=torch.float32, device=dev)
+        if shared_master is not None:
+            if shared_master.numel() != self.n_params or shared_master.dtype != torch.float32:
+                raise ValueError("shared_master must be fp32 with this net's parameter count")
+            self.master = shared_master
+        else:
+            self.master = torch.zeros(self.n_params, dtype=torch.float32, device=dev)
         self.grads = torch.zeros(self.n_params, dtype=torch.float32, device=dev)
         self.mom = torch.zeros(self.n_params, dtype=torch.float32, device=dev) if momentum else None
         self.lowp = (torch.zeros(self.n_params, dtype=torch_dtype(dtype), device=dev)
@@ -169,6 +176,13 @@ class Net:
     def step(self, x, target, loss_out=None, stream=None):
         out = self.loss if loss_out is None else loss_out
         mdnn_train_step(self.handle, x, target, out, stream)
+        return out
+
+    def step_async(self, x, target, loss_out=None, stream=None):
+        """Asynchronous step (section 4.1) on a master vector shared with other
+        workers: see mdnn_train_step_async."""
+        out = self.loss if loss_out is None else loss_out
+        mdnn_train_step_async(self.handle, x, target, out, stream)
         return out
 
     def activation_ptr(self, i: int) -> Optional[int]:

@@ -297,6 +297,31 @@ __global__ void sgd_kernel(int64_t n, float* __restrict__ w, const float* __rest
   }
 }
 
+// Asynchronous variant (section 4.1): the step -lr*v (or -lr*g) is added to
+// the shared weights with hardware fp32 atomics, so concurrent updates from
+// other streams are never lost; reads of w by other work may see any mix of
+// old and new values (Hogwild!-style inconsistent reads).
+template <bool MOM, bool SCALE>
+__global__ void sgd_async_kernel(int64_t n, float* w, const float* __restrict__ g, float* __restrict__ v,
+                                 float lr, float mu, const mdnn_scaler_t* __restrict__ sc) {
+  float S = 1.0f;
+  if (SCALE) {
+    if (sc->reserved) return;  // overflow: this worker's update is skipped
+    S = sc->scale;
+  }
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    float gi = g[i];
+    if (SCALE) gi = gi / S;
+    if (MOM) {
+      const float vi = fmaf(mu, v[i], gi);
+      v[i] = vi;
+      gi = vi;
+    }
+    unsafeAtomicAdd(&w[i], -lr * gi);
+  }
+}
+
 __global__ void scaler_finalize_kernel(mdnn_scaler_t* sc) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   if (sc->reserved) {
@@ -505,6 +530,45 @@ extern "C" mdnn_status_t mdnn_mse_loss(int64_t B, int64_t O, const float* y, con
     default: hipLaunchKernelGGL(mse_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), 0, st, n, B, y, t, loss_scale, loss_out, (uint16_t*)dy); break;
   }
   return check_launch("mse_kernel");
+}
+
+extern "C" mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const float* g32, float* v32,
+                                               float lr, float momentum, mdnn_scaler_t* scaler,
+                                               mdnn_stream_t stream) {
+  if (n < 0) return fail(MDNN_ERR_SHAPE, "sgd_update_async: n < 0");
+  if (n > 0 && (!w32 || !g32)) return fail(MDNN_ERR_NULL, "sgd_update_async: w32 and g32 are required");
+  if ((w32 && !aligned(w32, 4)) || (g32 && !aligned(g32, 4)) || (v32 && !aligned(v32, 4)) ||
+      (scaler && !aligned(scaler, 4)))
+    return fail(MDNN_ERR_MISALIGNED, "sgd_update_async: misaligned pointer");
+  if (scaler && n > 0 && !aligned(g32, 16))
+    return fail(MDNN_ERR_MISALIGNED, "sgd_update_async: g32 needs 16-byte alignment with a scaler");
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  if (scaler && n > 0) {
+    unsigned g = grid_for(ceil_div(n, 4), 256);
+    if (g > 2048) g = 2048;
+    hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);
+    MDNN_TRY(check_launch("finite_check_kernel"));
+  }
+  if (n > 0) {
+    unsigned g = grid_for(n, 256);
+    if (g > 4096) g = 4096;
+    const bool mom = v32 != nullptr, sc = scaler != nullptr;
+    if (mom && sc)
+      hipLaunchKernelGGL((sgd_async_kernel<true, true>), dim3(g), dim3(256), 0, st, n, w32, g32, v32, lr, momentum, scaler);
+    else if (mom)
+      hipLaunchKernelGGL((sgd_async_kernel<true, false>), dim3(g), dim3(256), 0, st, n, w32, g32, v32, lr, momentum, scaler);
+    else if (sc)
+      hipLaunchKernelGGL((sgd_async_kernel<false, true>), dim3(g), dim3(256), 0, st, n, w32, g32, v32, lr, momentum, scaler);
+    else
+      hipLaunchKernelGGL((sgd_async_kernel<false, false>), dim3(g), dim3(256), 0, st, n, w32, g32, v32, lr, momentum, scaler);
+    MDNN_TRY(check_launch("sgd_async_kernel"));
+  }
+  if (scaler) {
+    hipLaunchKernelGGL(scaler_finalize_kernel, dim3(1), dim3(64), 0, st, scaler);
+    MDNN_TRY(check_launch("scaler_finalize_kernel"));
+  }
+  return MDNN_SUCCESS;
 }
 
 extern "C" mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v32,

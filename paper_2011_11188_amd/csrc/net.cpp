@@ -218,8 +218,13 @@ extern "C" const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i) {
 
 extern "C" void mdnn_net_destroy(mdnn_net_t* net) { delete net; }
 
-extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
-                                         float* loss_out, mdnn_stream_t stream) {
+// One step; `async`: section 4.1's asynchronous variant, for nets that share
+// their master weights with other nets stepping concurrently: the working
+// copy is re-derived from the shared weights at the start of the step (an
+// inconsistent snapshot while others update them), and the update is added
+// to the shared weights with atomics instead of being written.
+static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* target, float* loss_out,
+                              mdnn_stream_t stream, bool async) {
   if (!net) return fail(MDNN_ERR_NULL, "train_step: NULL net");
   if (!net->bound) return fail(MDNN_ERR_STATE, "train_step: net not bound");
   if (!x || !target || !loss_out) return fail(MDNN_ERR_NULL, "train_step: x, target and loss_out are required");
@@ -236,8 +241,10 @@ extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const 
   };
   auto wptr = [&](const LayerPlan& p) { return (const char*)wlp + p.w_off * lps; };
 
-  // a1: input batch to the storage type
+  // a1: input batch to the storage type (and, asynchronously, this worker's
+  // snapshot of the shared weights)
   MDNN_TRY(mdnn_cast(B * net->in_feat, x, MDNN_F32, act_ptr(0), lp, stream));
+  if (async && net->lowp) MDNN_TRY(mdnn_cast(net->n_params, net->master, MDNN_F32, net->lowp, lp, stream));
 
   // forward
   for (size_t i = 0; i < net->layers.size(); ++i) {
@@ -306,6 +313,19 @@ extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const 
   }
 
   // update (and the low-precision working copy)
+  if (async)
+    return mdnn_sgd_update_async(net->n_params, net->master, net->grads, net->mom, net->cfg.lr,
+                                 net->cfg.momentum, net->scaler, stream);
   return mdnn_sgd_update(net->n_params, net->master, net->grads, net->mom, net->lowp, lp,
                          net->cfg.lr, net->cfg.momentum, net->scaler, stream);
+}
+
+extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
+                                         float* loss_out, mdnn_stream_t stream) {
+  return run_step(net, x, target, loss_out, stream, false);
+}
+
+extern "C" mdnn_status_t mdnn_train_step_async(mdnn_net_t* net, const float* x, const void* target,
+                                               float* loss_out, mdnn_stream_t stream) {
+  return run_step(net, x, target, loss_out, stream, true);
 }
