@@ -20,7 +20,10 @@ Also on the same JSON line:
                 bwd-filter;
   gemm_fp32_split3  fp32 GEMMs (4096, 8192) through three fp16 MFMA
                 products of the Eq. (1) splits, next to the native fp32 kernel;
-  workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step.
+  workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step;
+  async_sgd     the same two nets trained asynchronously (section 4.1) by
+                several workers on separate streams sharing one parameter
+                vector, samples/s over all workers.
 Every timed region follows sustained untimed load (about a second of the
 same work, or 3 runs of at least 50 ms with the median kept for the
 sub-benchmarks): the GPU's clocks settle under sustained load, which is the
@@ -288,6 +291,49 @@ def _conv_bench(mdnn, reps=20):
     return res
 
 
+def _async_bench(mdnn, steps=40):
+    """Asynchronous SGD (section 4.1): W workers on W streams share one fp32
+    parameter vector (mdnn_train_step_async), next to the synchronous step of
+    the same net; samples/s over all workers' steps."""
+    import torch
+    import workloads as W
+    res = {}
+    for cfg, workers in ((W.mlp784_fp32(), 4), (W.lenet_bf16(), 2)):
+        lp = {"f32": 0, "f16": 1, "bf16": 2}[cfg.dtype]
+        params = torch.as_tensor(W.init_params(cfg), dtype=torch.float32)
+        nets = []
+        for k in range(workers):
+            n = mdnn.Net(cfg.layers, cfg.batch, lp, cfg.loss, cfg.lr, cfg.momentum, cfg.loss_scaling,
+                         cfg.init_scale, cfg.n_classes, shared_master=nets[0].master if nets else None)
+            if not nets:
+                n.set_params(params)
+            nets.append(n)
+        streams = [torch.cuda.Stream() for _ in range(workers)]
+        data = []
+        for s in range(8):
+            x, t = W.batch_inputs(cfg, s)
+            tt = torch.from_numpy(t).cuda()
+            data.append((torch.from_numpy(x).cuda(), tt))
+        losses = [torch.zeros(1, device="cuda") for _ in range(workers)]
+
+        def round_():
+            for k in range(workers):
+                x, t = data[k % len(data)]
+                nets[k].step_async(x, t, loss_out=losses[k], stream=streams[k])
+        _warm(round_, 0.3)
+        with _Timer() as tm:
+            for _ in range(steps):
+                round_()
+            for st in streams:
+                torch.cuda.current_stream().wait_stream(st)
+        ms = tm.ms / (steps * workers)
+        res[f"{cfg.name}_async{workers}"] = {"workers": workers, "ms_per_step": round(ms, 4),
+                                             "samples_per_s": round(cfg.batch / (ms * 1e-3), 1)}
+        for n in nets:
+            n.close()
+    return res
+
+
 def _traffic_key(kernel_desc: str) -> str:
     """'NN f16 -> f16 256x256' style key of a step kernel description."""
     tile = "256x256" if "256x256" in kernel_desc else "128x128"
@@ -431,6 +477,8 @@ def main():
             n2.close()
         line["workloads"] = wl
         print("[bench] workloads done", file=sys.stderr, flush=True)
+        line["async_sgd"] = _async_bench(mdnn)
+        print("[bench] async sgd done", file=sys.stderr, flush=True)
     if not args.no_cpu:
         line["cpu_baseline"] = _cpu_baseline(cfg)
     print(json.dumps(line), flush=True)
