@@ -4,6 +4,7 @@
 //   bwd_filter: M = c_out,   N = r*s*c_in, K = n*Ho*Wo (A = dy^T, B = shifted x), split over K
 // No im2col buffer is materialised: the operand sources compute addresses.
 #include "conv_pipe.h"
+#include "conv_small.h"
 #include "gemm_launch.h"
 
 namespace mdnn {
@@ -129,6 +130,7 @@ extern "C" mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const v
   clear_error();
   hipStream_t st = as_stream(stream);
   if (pipe_allowed()) {
+    if (conv_small_fwd_ok(g)) return conv_small_fwd(g, x, w, ep, io_type, y_type, st);
     bool done = false;
     MDNN_TRY(conv_pipe_fwd(g, x, w, ep, io_type, y_type, st, &done));
     if (done) return MDNN_SUCCESS;
@@ -180,6 +182,8 @@ static size_t filter_ws_split_bytes(const ConvGeom& g) {
   const SplitPlan p = filter_plan(g), q = conv_pipe_filter_plan(g);
   size_t splits = p.splits > 1 ? (size_t)p.splits : 0;
   if (q.splits > 1 && (size_t)q.splits > splits) splits = (size_t)q.splits;
+  const int64_t sb = conv_small_filter_blocks(g);
+  if (sb > 0 && (size_t)sb > splits) splits = (size_t)sb;
   return (splits * mn + 255) & ~(size_t)255;
 }
 
@@ -215,7 +219,11 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
     return db ? fill_zero(db, (size_t)g.k * 4, st) : MDNN_SUCCESS;
   }
   bool done = false;
-  if (pipe_allowed()) MDNN_TRY(conv_pipe_bwd_filter(g, x, dy, dw, workspace, io_type, st, &done));
+  if (pipe_allowed() && conv_small_filter_blocks(g) > 0) {
+    MDNN_TRY(conv_small_filter(g, x, dy, dw, workspace, io_type, st));
+    done = true;
+  }
+  if (!done && pipe_allowed()) MDNN_TRY(conv_pipe_bwd_filter(g, x, dy, dw, workspace, io_type, st, &done));
   if (!done) {
     switch (io_type) {
       case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st)); break;

@@ -1,0 +1,23 @@
+// Direct kernels for convolutions whose reduction is tiny (conv_small.hip).
+#pragma once
+
+#include "gemm_core.h"
+#include "internal.h"
+
+namespace mdnn {
+
+// Forward with K = r*s*c_in <= 64 and c_out <= 256: any storage type, any
+// epilogue (bias, ReLU, output type).
+bool conv_small_fwd_ok(const ConvGeom& g);
+mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
+                             mdnn_dtype_t out, hipStream_t st);
+
+// Filter gradient with r*s*c_in <= 64 and c_out * r*s*c_in <= 1024: number
+// of pixel blocks (the partials it writes:
+// blocks * c_out * r*s*c_in floats), or 0 when the shape does not qualify.
+int64_t conv_small_filter_blocks(const ConvGeom& g);
+// dw = sum over pixel blocks of the partials in ws (fixed order).
+mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
+                                mdnn_dtype_t io, hipStream_t st);
+
+}  // namespace mdnn

@@ -1,0 +1,178 @@
+// Convolutions with a tiny reduction (section 3.1's convolution layers; the
+// first layer of an image network, e.g. one input channel and a 5x5 filter):
+// the GEMM engine would spend almost all of a tile on padding, so these run
+// as direct kernels on the vector ALUs, fp32 accumulation.
+//
+//   forward (K = r*s*c_in <= 64): a block stages the im2col rows of 64
+//     output pixels and the whole filter in LDS; each thread produces four
+//     consecutive output channels of one pixel through the shared epilogue.
+//   backward filter (c_out * r*s*c_in <= 1024 outputs, r*s*c_in <= 64): each
+//     block accumulates every filter element over its chunk of output pixels
+//     into fp32 partials, which the split reduction then sums in a fixed
+//     order (deterministic).
+#include "conv_small.h"
+
+namespace mdnn {
+namespace {
+
+constexpr int TP = 64;  // output pixels per staging round
+
+template <class T>
+__device__ __forceinline__ float ld_elem(const typename T::storage* p, int64_t i) {
+  return to_f<T>(p[i]);
+}
+
+// im2col element (pixel m of the output grid, column kk = (r*s_ + s)*c + ch)
+template <class T>
+__device__ __forceinline__ float patch(const typename T::storage* x, const ConvGeom& g, int64_t m, int kk) {
+  const int64_t hw = (int64_t)g.ho * g.wo;
+  const int64_t n = m / hw;
+  const int rem = (int)(m - n * hw);
+  const int i = rem / g.wo, j = rem - i * g.wo;
+  const int tap = kk / g.c, ch = kk - tap * g.c;
+  const int r = tap / g.s, s = tap - r * g.s;
+  const int y = i + r - g.pad, xx = j + s - g.pad;
+  if (y < 0 || y >= g.h || xx < 0 || xx >= g.w) return 0.0f;
+  return ld_elem<T>(x, ((n * g.h + y) * g.w + xx) * g.c + ch);
+}
+
+// Row stride of an LDS table with `cols` columns: odd, so that a column walk
+// by consecutive lanes spreads over the banks.
+__host__ __device__ constexpr int odd_stride(int cols) { return cols | 1; }
+
+template <class T, class OutT>
+__global__ void __launch_bounds__(256)
+conv_small_fwd_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ w,
+                      ConvGeom g, int64_t M, Epilogue ep) {
+  extern __shared__ float smem[];
+  const int K = g.r * g.s * g.c, N = g.k, KS = odd_stride(K);
+  float* xs = smem;            // [TP][KS] im2col rows
+  float* ws = smem + TP * KS;  // [N][KS] filter
+  const int tid = threadIdx.x;
+  for (int e = tid; e < N * K; e += 256) {
+    const int n = e / K;
+    ws[n * KS + (e - n * K)] = ld_elem<T>(w, e);
+  }
+  const int64_t m0 = (int64_t)blockIdx.x * TP;
+  for (int e = tid; e < TP * K; e += 256) {
+    const int p = e / K, kk = e - p * K;
+    xs[p * KS + kk] = m0 + p < M ? patch<T>(x, g, m0 + p, kk) : 0.0f;
+  }
+  __syncthreads();
+  const int groups = (N + 3) / 4;
+  for (int q = tid; q < TP * groups; q += 256) {
+    const int p = q / groups, n4 = (q - p * groups) * 4;
+    float4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < K; ++kk) {
+      const float a = xs[p * KS + kk];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n4 + e < N) acc[e] = fmaf(a, ws[(n4 + e) * KS + kk], acc[e]);
+    }
+    epilogue_store4<T, OutT>(ep, M, N, m0 + p, n4, acc);
+  }
+}
+
+// partial[b][k][kk] over the pixels of block b (pixels_per_block of them)
+template <class T>
+__global__ void __launch_bounds__(256)
+conv_small_filter_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ dy,
+                         ConvGeom g, int64_t P, int64_t pixels_per_block, float* __restrict__ partial) {
+  extern __shared__ float smem[];
+  const int K = g.r * g.s * g.c, N = g.k, MN = N * K, KS = odd_stride(K), NS = odd_stride(N);
+  float* xs = smem;            // [TP][KS] im2col rows
+  float* ds = smem + TP * KS;  // [TP][NS] output gradient rows
+  const int tid = threadIdx.x;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  const int64_t p_beg = (int64_t)blockIdx.x * pixels_per_block;
+  const int64_t p_end = p_beg + pixels_per_block < P ? p_beg + pixels_per_block : P;
+  for (int64_t p0 = p_beg; p0 < p_end; p0 += TP) {
+    __syncthreads();
+    for (int e = tid; e < TP * K; e += 256) {
+      const int p = e / K, kk = e - p * K;
+      xs[p * KS + kk] = p0 + p < p_end ? patch<T>(x, g, p0 + p, kk) : 0.0f;
+    }
+    for (int e = tid; e < TP * N; e += 256) {
+      const int p = e / N, k = e - p * N;
+      ds[p * NS + k] = p0 + p < p_end ? ld_elem<T>(dy, (p0 + p) * N + k) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int o = 0; o < 4; ++o) {
+      const int idx = tid + o * 256;
+      if (idx < MN) {
+        const int k = idx / K, kk = idx - k * K;
+        float s = acc[o];
+        for (int p = 0; p < TP; ++p) s = fmaf(ds[p * NS + k], xs[p * KS + kk], s);
+        acc[o] = s;
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 0; o < 4; ++o) {
+    const int idx = tid + o * 256;
+    if (idx < MN) partial[(int64_t)blockIdx.x * MN + idx] = acc[o];
+  }
+}
+
+constexpr int64_t FILTER_PIXELS = 512;  // pixels per block of the filter gradient
+constexpr size_t LDS_LIMIT = 65536;      // dynamic LDS bytes per block
+
+size_t fwd_lds(const ConvGeom& g) {
+  return (size_t)(TP + g.k) * odd_stride(g.r * g.s * g.c) * sizeof(float);
+}
+size_t filter_lds(const ConvGeom& g) {
+  return (size_t)TP * (odd_stride(g.r * g.s * g.c) + odd_stride(g.k)) * sizeof(float);
+}
+
+}  // namespace
+
+bool conv_small_fwd_ok(const ConvGeom& g) {
+  return g.r * g.s * g.c <= 64 && g.k <= 256 && fwd_lds(g) <= LDS_LIMIT;
+}
+
+mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
+                             mdnn_dtype_t out, hipStream_t st) {
+  const int64_t M = (int64_t)g.n * g.ho * g.wo;
+  if (M == 0) return MDNN_SUCCESS;
+  if (ceil_div(M, TP) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: too many output pixels");
+  const dim3 grid((unsigned)ceil_div(M, TP));
+#define MDNN_SMALL_FWD(T, O)                                                                                   \
+  hipLaunchKernelGGL((conv_small_fwd_kernel<T, O>), grid, dim3(256), fwd_lds(g), st, (const T::storage*)x,            \
+                     (const T::storage*)w, g, M, ep)
+  if (io == MDNN_F16) {
+    if (out == MDNN_F32) MDNN_SMALL_FWD(F16, F32); else MDNN_SMALL_FWD(F16, F16);
+  } else if (io == MDNN_BF16) {
+    if (out == MDNN_F32) MDNN_SMALL_FWD(BF16, F32); else MDNN_SMALL_FWD(BF16, BF16);
+  } else {
+    MDNN_SMALL_FWD(F32, F32);
+  }
+#undef MDNN_SMALL_FWD
+  return check_launch("conv_small_fwd_kernel");
+}
+
+int64_t conv_small_filter_blocks(const ConvGeom& g) {
+  const int K = g.r * g.s * g.c;
+  if (K > 64 || g.k > 256 || (int64_t)g.k * K > 1024 || filter_lds(g) > LDS_LIMIT) return 0;
+  const int64_t P = (int64_t)g.n * g.ho * g.wo;
+  return ceil_div(P, FILTER_PIXELS);
+}
+
+mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
+                                mdnn_dtype_t io, hipStream_t st) {
+  const int64_t blocks = conv_small_filter_blocks(g);
+  const int64_t P = (int64_t)g.n * g.ho * g.wo;
+  if (blocks <= 0 || blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: filter gradient shape");
+  float* part = (float*)ws;
+#define MDNN_SMALL_FILT(T)                                                                                      \
+  hipLaunchKernelGGL((conv_small_filter_kernel<T>), dim3((unsigned)blocks), dim3(256), filter_lds(g), st,               \
+                     (const T::storage*)x, (const T::storage*)dy, g, P, FILTER_PIXELS, part)
+  if (io == MDNN_F16) MDNN_SMALL_FILT(F16);
+  else if (io == MDNN_BF16) MDNN_SMALL_FILT(BF16);
+  else MDNN_SMALL_FILT(F32);
+#undef MDNN_SMALL_FILT
+  MDNN_TRY(check_launch("conv_small_filter_kernel"));
+  return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st);
+}
+
+}  // namespace mdnn

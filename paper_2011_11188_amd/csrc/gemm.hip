@@ -32,10 +32,36 @@ __global__ void reduce_splits_kernel(const float* __restrict__ part, int splits,
   }
 }
 
+// Few outputs, many splits: block b sums outputs 64b .. 64b+63; thread
+// (g, j) sums splits g, g+16, g+32, ... of output j, then the 16 group sums
+// are added in order g = 0..15 (a fixed order: deterministic).
+__global__ void __launch_bounds__(1024)
+reduce_splits_wide_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ out) {
+  __shared__ float red[16][64];
+  const int j = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + j;
+  float s = 0.0f;
+  if (e < n)
+    for (int k = g; k < splits; k += 16) s += part[(int64_t)k * n + e];
+  red[g][j] = s;
+  __syncthreads();
+  if (g == 0 && e < n) {
+    float t = red[0][j];
+#pragma unroll
+    for (int q = 1; q < 16; ++q) t += red[q][j];
+    out[e] = t;
+  }
+}
+
 mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int64_t cols,
                             float* out, hipStream_t stream) {
   const int64_t n = rows * cols;
   if (n == 0) return MDNN_SUCCESS;
+  if (splits >= 32 && n <= ((int64_t)1 << 18)) {
+    hipLaunchKernelGGL(reduce_splits_wide_kernel, dim3((unsigned)ceil_div(n, 64)), dim3(1024), 0, stream,
+                       partial, splits, n, out);
+    return check_launch("reduce_splits_wide_kernel");
+  }
   const int64_t blocks = ceil_div(ceil_div(n, 4), 256);
   hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, partial,
                      splits, n, out);

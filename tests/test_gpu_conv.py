@@ -57,6 +57,62 @@ def test_conv_small_against_oracle(mdnn, shape, dt):
     assert norm_max_err(db, dy.sum(axis=(0, 1, 2))) <= TOL
 
 
+# Shapes on the direct small-reduction kernels (r*s*c_in <= 64; the filter
+# gradient also needs c_out*r*s*c_in <= 1024): ragged channel groups,
+# valid (non-"same") padding, several 512-pixel filter blocks with a ragged
+# tail, the largest filter gradient (1024 outputs), c_out = 256 (forward
+# only: its filter gradient exceeds the LDS budget and takes the GEMM path).
+DIRECT = [  # n, h, w, c_in, c_out, r, s, pad
+    (3, 13, 11, 3, 10, 3, 3, 1),
+    (2, 9, 8, 2, 7, 3, 3, 0),
+    (5, 17, 15, 1, 32, 5, 5, 2),
+    (2, 10, 9, 4, 16, 4, 4, 1),
+    (2, 6, 5, 3, 256, 1, 1, 0),
+    (1, 1, 1, 64, 4, 1, 1, 0),
+]
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16", "f32"])
+@pytest.mark.parametrize("shape", DIRECT)
+def test_conv_direct_against_oracle(mdnn, shape, dt):
+    n, h, w, ci, co, r, s, pad = shape
+    (x, wt, dy), (y, dx, dw, db) = _ops(mdnn, shape, dt, 23)
+    assert norm_max_err(y, ops.conv2d_fwd(x, wt, pad)) <= TOL
+    assert norm_max_err(dx, ops.conv2d_bwd_data(dy, wt, pad, h, w)) <= TOL
+    assert norm_max_err(dw, ops.conv2d_bwd_filter(x, dy, pad, r, s)) <= TOL
+    assert norm_max_err(db, dy.sum(axis=(0, 1, 2))) <= TOL
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_conv_direct_epilogue_lowp(mdnn, dt):
+    """Direct forward with bias+ReLU stored in the storage type (c_out = 10:
+    a ragged group of four channels), ragged pixel count."""
+    n, h, w, ci, co, r, s, pad = 3, 7, 9, 2, 10, 5, 5, 2
+    x = W.normal((n, h, w, ci), 24, 1, dt, 0.3)
+    wt = W.normal((co, r, s, ci), 24, 2, dt, 0.3)
+    b = W.normal((co,), 24, 3, "f32", 0.2)
+    y = mdnn.conv2d_fwd(dev(x, dt), dev(wt, dt), pad, bias=dev(b, "f32"), act=mdnn.ACT_RELU)
+    x64, w64 = decode(x, dt), decode(wt, dt)
+    exact = ops.bias_act(ops.conv2d_fwd(x64, w64, pad), b.astype(np.float64), "relu")
+    err = accum_bound(ops.conv2d_fwd(np.abs(x64), np.abs(w64), pad) + np.abs(b), r * s * ci + 1)
+    assert lowp_close(host64(y), exact, dt, err)
+
+
+def test_conv_direct_integer_exact(mdnn):
+    import torch
+    n, h, w, ci, co, r, s, pad = 4, 12, 11, 2, 12, 5, 5, 2
+    x = W.small_ints((n, h, w, ci), 25, 1, dtype="f16")
+    wt = W.small_ints((co, r, s, ci), 25, 2, dtype="f16")
+    dy = W.small_ints((n, h, w, co), 25, 3, dtype="f16")
+    X, Wt, DY = dev(x, "f16"), dev(wt, "f16"), dev(dy, "f16")
+    y = mdnn.conv2d_fwd(X, Wt, pad, out_dtype=torch.float32)
+    dwt, _ = mdnn.conv2d_bwd_filter(X, DY, r, s, pad)
+    torch.cuda.synchronize()
+    x64, w64, dy64 = x.astype(np.float64), wt.astype(np.float64), dy.astype(np.float64)
+    assert np.array_equal(host64(y), ops.conv2d_fwd(x64, w64, pad))
+    assert np.array_equal(host64(dwt), ops.conv2d_bwd_filter(x64, dy64, pad, r, s))
+
+
 # Shapes on the pipelined kernels (forward: c_in % 64 == 0; backward data:
 # c_out % 64 == 0 and c_in % 8 == 0; backward filter: size-preserving, channels
 # multiples of 8, n*h*w % 64 == 0), with ragged M and N, non-square grids,
