@@ -136,6 +136,49 @@ def _time_steps(net, xs, ts, steps, warmup):
     return tm.ms / steps
 
 
+def _time_graph_steps(net, xs, ts, steps, warmup):
+    """As _time_steps, with each batch's step recorded once into a HIP graph
+    and replayed (one launch per step instead of one per kernel)."""
+    graphs = [net.record_step(x, t) for x, t in zip(xs, ts)]
+    it = iter(range(1 << 62))
+
+    def one():
+        graphs[next(it) % len(graphs)].launch()
+    _warm(one)
+    for i in range(warmup):
+        graphs[i % len(graphs)].launch()
+    with _Timer() as tm:
+        for i in range(steps):
+            graphs[i % len(graphs)].launch()
+    for g in graphs:
+        g.close()
+    return tm.ms / steps
+
+
+def _clocks():
+    """Current shader / memory clocks (MHz) as rocm-smi reports them, or None."""
+    import re
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True,
+                             timeout=30).stdout
+        d = json.loads(out)
+    except Exception:
+        return None
+    res = {}
+    for card in d.values():
+        if not isinstance(card, dict):
+            continue
+        for k, v in card.items():
+            m = re.search(r"(\d+)\s*mhz", str(v), re.I)
+            if m and "speed" in k.lower():
+                for clk in ("sclk", "mclk", "fclk", "socclk"):
+                    if k.lower().startswith(clk):
+                        res[clk + "_mhz"] = int(m.group(1))
+        break
+    return res or None
+
+
 def _step_gemms(cfg):
     """Every GEMM one step of an FC chain issues, as (layout, M, N, K, out)."""
     import workloads as W
@@ -405,6 +448,7 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
 
+    clocks_before = _clocks()
     cfg = W.wide_mlp_fp16()
     net, xs, ts = _train_setup(mdnn, cfg)
     ms = _time_steps(net, xs, ts, args.steps, args.warmup)
@@ -412,6 +456,8 @@ def main():
     step_tf = cfg.flops_per_step() / (ms * 1e-3) / 1e12
     print(f"[bench] {cfg.name}: {ms:.3f} ms/step, {samples:.0f} samples/s, "
           f"{step_tf:.1f} TFLOP/s", file=sys.stderr, flush=True)
+    graph_ms = _time_graph_steps(net, xs, ts, args.steps, args.warmup)
+    print(f"[bench] {cfg.name} as a recorded graph: {graph_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     # dominant kernel: the kernel instantiation (layout, output type, tile)
     # whose launches in the step take the most time
@@ -457,6 +503,7 @@ def main():
                                "scaling (2^16), SGD momentum 0.9, lr 1e-3",
                    "global_batch": cfg.batch, "parallelism": "single GPU",
                    "step_tflops": round(step_tf, 1),
+                   "graph_ms_per_step": round(graph_ms, 4),
                    "step_mfma_frac": round(step_tf / PEAK_F16_TFLOPS, 4),
                    "flop_per_step": cfg.flops_per_step()},
         "roofline": roofline,
@@ -472,13 +519,17 @@ def main():
         for c in (W.lenet_bf16(), W.mlp784_fp32()):
             n2, xs2, ts2 = _train_setup(mdnn, c)
             m2 = _time_steps(n2, xs2, ts2, 50, 5)
+            g2 = _time_graph_steps(n2, xs2, ts2, 200, 5)
             wl[c.name] = {"ms_per_step": round(m2, 4), "samples_per_s": round(c.batch / (m2 * 1e-3), 1),
-                          "tflops": round(c.flops_per_step() / (m2 * 1e-3) / 1e12, 2)}
+                          "tflops": round(c.flops_per_step() / (m2 * 1e-3) / 1e12, 2),
+                          "graph_ms_per_step": round(g2, 4),
+                          "graph_samples_per_s": round(c.batch / (g2 * 1e-3), 1)}
             n2.close()
         line["workloads"] = wl
         print("[bench] workloads done", file=sys.stderr, flush=True)
         line["async_sgd"] = _async_bench(mdnn)
         print("[bench] async sgd done", file=sys.stderr, flush=True)
+    line["clocks"] = {"before": clocks_before, "after": _clocks()}
     if not args.no_cpu:
         line["cpu_baseline"] = _cpu_baseline(cfg)
     print(json.dumps(line), flush=True)

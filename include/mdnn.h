@@ -101,6 +101,27 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
                               const float* bias, mdnn_act_t act, const void* mask_src,
                               int64_t ldm, mdnn_stream_t stream);
 
+/* The same GEMM with a caller-provided device workspace (section 3.2's
+ * product on shapes whose output is only a few tiles, e.g. a batch of 64 to
+ * 256 rows against a narrow layer: the few workgroups' serial K loops would
+ * leave most CUs idle).  When the workspace holds at least
+ * mdnn_gemm_workspace(ab_type, M, N, K) bytes (16-byte aligned), such a
+ * problem splits K across workgroups into fp32 partials that one more kernel
+ * sums in a fixed order before the epilogue: deterministic, but the fp32
+ * summation order differs from mdnn_gemm_mixed's.  A NULL / smaller /
+ * misaligned workspace, or a shape that does not need splitting, gives
+ * exactly mdnn_gemm_mixed.  mdnn_gemm_workspace returns 0 when no split is
+ * planned (and for negative sizes).  The workspace is scratch, overwritten;
+ * calls that share one must be ordered on one stream. */
+size_t mdnn_gemm_workspace(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K);
+mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
+                                 float alpha, const void* A, int64_t lda, const void* B,
+                                 int64_t ldb, mdnn_dtype_t ab_type, float beta, const void* C,
+                                 int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
+                                 const float* bias, mdnn_act_t act, const void* mask_src,
+                                 int64_t ldm, void* workspace, size_t ws_bytes,
+                                 mdnn_stream_t stream);
+
 /* Tuning knob for measurements (process-wide): force the MFMA kernel of the
  * GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128, 3 = 64x64
  * general kernels (convolutions then also use the general kernels), 4 / 5 =
@@ -357,6 +378,32 @@ mdnn_status_t mdnn_train_step_async(mdnn_net_t* net, const float* x, const void*
  * of layer i-1) inside the bound workspace, for inspection; NULL if invalid. */
 const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i);
 void mdnn_net_destroy(mdnn_net_t* net);
+
+/* Recorded steps.  Section 3.1's SGD step for a small network is a few
+ * dozen short kernels, so its time is set by launch latency: these calls
+ * record one mdnn_train_step (forward, loss, backward, update; the same
+ * kernels in the same order) into a HIP graph once, and replay it with a
+ * single launch.
+ *   mdnn_train_graph_create: records the step of `net` on the buffers x,
+ *     target and loss_out exactly as mdnn_train_step would run it; nothing
+ *     executes.  The graph keeps those device addresses and the net's bound
+ *     memory: they must stay allocated, unmoved, for the graph's lifetime (to
+ *     feed new data, write it into the same x / target buffers first).  The
+ *     recording happens on a private stream; the caller's streams are not
+ *     touched.  *out receives a library-owned handle (a host object plus the
+ *     HIP runtime's instantiated graph).  Errors: those of mdnn_train_step
+ *     (the step is validated while it is recorded) and MDNN_ERR_LAUNCH if the
+ *     runtime refuses the capture; *out is NULL then.
+ *   mdnn_graph_launch: enqueues one replay on `stream` (any stream, the
+ *     legacy default included); replays on one stream run in order.  The
+ *     result equals mdnn_train_step's on the same inputs, bit for bit.
+ *   mdnn_graph_destroy: releases the handle (NULL is ignored).  Pending
+ *     replays must have finished. */
+typedef struct mdnn_graph mdnn_graph_t;
+mdnn_status_t mdnn_train_graph_create(mdnn_net_t* net, const float* x, const void* target,
+                                      float* loss_out, mdnn_graph_t** out);
+mdnn_status_t mdnn_graph_launch(mdnn_graph_t* graph, mdnn_stream_t stream);
+void mdnn_graph_destroy(mdnn_graph_t* graph);
 
 #ifdef __cplusplus
 }

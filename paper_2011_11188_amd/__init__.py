@@ -70,6 +70,8 @@ _vp, _i64, _f, _i = C.c_void_p, C.c_int64, C.c_float, C.c_int
 _SIGS = {
     "mdnn_gemm_mixed": [_i, _i64, _i64, _i64, _f, _vp, _i64, _vp, _i64, _i, _f, _vp, _i64, _vp,
                         _i64, _i, _vp, _i, _vp, _i64, _vp],
+    "mdnn_gemm_mixed_ws": [_i, _i64, _i64, _i64, _f, _vp, _i64, _vp, _i64, _i, _f, _vp, _i64, _vp,
+                           _i64, _i, _vp, _i, _vp, _i64, _vp, C.c_size_t, _vp],
     "mdnn_conv2d_fwd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp],
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
@@ -91,6 +93,8 @@ _SIGS = {
     "mdnn_net_bind": [_vp, _vp, _vp, _vp, _vp, _vp, C.c_size_t, _vp],
     "mdnn_net_sync_lowp": [_vp, _vp],
     "mdnn_train_step": [_vp, _vp, _vp, _vp, _vp],
+    "mdnn_train_graph_create": [_vp, _vp, _vp, _vp, _vp],
+    "mdnn_graph_launch": [_vp, _vp],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -98,6 +102,8 @@ for _name, _args in _SIGS.items():
     _fn.restype = C.c_int
 _lib.mdnn_conv2d_bwd_filter_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_bwd_filter_workspace.restype = C.c_size_t
+_lib.mdnn_gemm_workspace.argtypes = [_i, _i64, _i64, _i64]
+_lib.mdnn_gemm_workspace.restype = C.c_size_t
 _lib.mdnn_gemm_split3_workspace.argtypes = [_i64, _i64, _i64]
 _lib.mdnn_gemm_split3_workspace.restype = C.c_size_t
 _lib.mdnn_bias_act_bwd_workspace.argtypes = [_i64, _i64]
@@ -108,6 +114,8 @@ _lib.mdnn_net_activation.argtypes = [_vp, C.c_int32]
 _lib.mdnn_net_activation.restype = _vp
 _lib.mdnn_net_destroy.argtypes = [_vp]
 _lib.mdnn_net_destroy.restype = None
+_lib.mdnn_graph_destroy.argtypes = [_vp]
+_lib.mdnn_graph_destroy.restype = None
 _lib.mdnn_set_gemm_tile.argtypes = [_i]
 _lib.mdnn_set_gemm_tile.restype = _i
 
@@ -156,10 +164,10 @@ def last_error() -> str:
 
 def exported_symbols():
     return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
-                                 "mdnn_gemm_split3_workspace",
+                                 "mdnn_gemm_split3_workspace", "mdnn_gemm_workspace",
                                  "mdnn_last_error",
                                  "mdnn_version", "mdnn_net_activation", "mdnn_net_destroy",
-                                 "mdnn_set_gemm_tile"])
+                                 "mdnn_graph_destroy", "mdnn_set_gemm_tile"])
 
 
 # ---------------------------------------------------------------------------
@@ -184,6 +192,18 @@ def mdnn_conv2d_fwd(shape: ConvShape, x, w, io_type, bias, act, y, y_type, strea
 def mdnn_conv2d_bwd_data(shape: ConvShape, dy, w, io_type, mask_src, dx, dx_type, stream=None):
     return _call("mdnn_conv2d_bwd_data", _p(shape), _p(dy), _p(w), io_type, _p(mask_src), _p(dx),
                  dx_type, _s(stream))
+
+
+def mdnn_gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, Cm, ldc, D, ldd,
+                       d_type, bias=None, act=ACT_NONE, mask_src=None, ldm=0, workspace=None, ws_bytes=0,
+                       stream=None):
+    return _call("mdnn_gemm_mixed_ws", layout, M, N, K, alpha, _p(A), lda, _p(B), ldb, ab_type, beta,
+                 _p(Cm), ldc, _p(D), ldd, d_type, _p(bias), act, _p(mask_src), ldm, _p(workspace), ws_bytes,
+                 _s(stream))
+
+
+def mdnn_gemm_workspace(ab_type, M, N, K) -> int:
+    return _lib.mdnn_gemm_workspace(ab_type, M, N, K)
 
 
 def mdnn_conv2d_bwd_filter_workspace(shape: ConvShape, io_type) -> int:
@@ -294,6 +314,21 @@ def mdnn_net_activation(net, i: int) -> Optional[int]:
 
 def mdnn_net_destroy(net) -> None:
     _lib.mdnn_net_destroy(net)
+
+
+def mdnn_train_graph_create(net, x, target, loss_out) -> int:
+    """Returns the graph handle (an int)."""
+    out = C.c_void_p()
+    _call("mdnn_train_graph_create", net, _p(x), _p(target), _p(loss_out), C.byref(out))
+    return out.value
+
+
+def mdnn_graph_launch(graph, stream=None):
+    return _call("mdnn_graph_launch", graph, _s(stream))
+
+
+def mdnn_graph_destroy(graph) -> None:
+    _lib.mdnn_graph_destroy(graph)
 
 
 from .api import *  # noqa: E402,F401,F403  (tensor-level conveniences)

@@ -11,12 +11,13 @@ from typing import Optional, Sequence
 from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, LOSS_MSE, LOSS_XENT,
                NN, NT, TN, ConvShape, LayerDesc, Scaler, TrainCfg, dtype_of, mdnn_conv2d_bwd_data,
                mdnn_conv2d_bwd_filter, mdnn_conv2d_bwd_filter_workspace, mdnn_conv2d_fwd,
-               mdnn_gemm_mixed, mdnn_gemm_split3, mdnn_gemm_split3_workspace, mdnn_net_activation,
-               mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
-               mdnn_split_f16, mdnn_train_step, mdnn_train_step_async)
+               mdnn_gemm_mixed, mdnn_gemm_mixed_ws, mdnn_gemm_workspace, mdnn_gemm_split3,
+               mdnn_gemm_split3_workspace, mdnn_net_activation, mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
+               mdnn_split_f16, mdnn_train_step, mdnn_train_step_async, mdnn_train_graph_create,
+               mdnn_graph_launch, mdnn_graph_destroy)
 
 __all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "pow2_scale", "conv_shape", "conv2d_fwd",
-           "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net"]
+           "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net", "StepGraph"]
 
 
 def torch_dtype(code: int):
@@ -25,8 +26,10 @@ def torch_dtype(code: int):
 
 
 def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask=None,
-         alpha: float = 1.0, beta: float = 0.0, Cm=None, out=None, stream=None):
-    """D = epi(alpha op(A) op(B) + beta C) for row-major 2-D tensors A, B."""
+         alpha: float = 1.0, beta: float = 0.0, Cm=None, out=None, stream=None, workspace=None):
+    """D = epi(alpha op(A) op(B) + beta C) for row-major 2-D tensors A, B.
+    workspace: None (mdnn_gemm_mixed), True (allocate what
+    mdnn_gemm_workspace asks for) or a device byte tensor (mdnn_gemm_mixed_ws)."""
     import torch
     if layout == TN:
         K, M = A.shape
@@ -35,9 +38,16 @@ def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask
     N = B.shape[0] if layout == NT else B.shape[1]
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype or torch.float32, device=A.device)
-    mdnn_gemm_mixed(layout, M, N, K, alpha, A, A.stride(0), B, B.stride(0), dtype_of(A), beta, Cm,
-                    Cm.stride(0) if Cm is not None else 0, out, out.stride(0), dtype_of(out), bias,
-                    act, mask, mask.stride(0) if mask is not None else 0, stream)
+    args = (layout, M, N, K, alpha, A, A.stride(0), B, B.stride(0), dtype_of(A), beta, Cm,
+            Cm.stride(0) if Cm is not None else 0, out, out.stride(0), dtype_of(out), bias,
+            act, mask, mask.stride(0) if mask is not None else 0)
+    if workspace is None:
+        mdnn_gemm_mixed(*args, stream)
+        return out
+    if workspace is True:
+        nb = mdnn_gemm_workspace(dtype_of(A), M, N, K)
+        workspace = torch.empty((max(nb, 16),), dtype=torch.uint8, device=A.device)
+    mdnn_gemm_mixed_ws(*args, workspace, workspace.numel(), stream)
     return out
 
 
@@ -178,6 +188,12 @@ class Net:
         mdnn_train_step(self.handle, x, target, out, stream)
         return out
 
+    def record_step(self, x, target, loss_out=None) -> "StepGraph":
+        """Record one step on these exact buffers into a HIP graph (see
+        mdnn_train_graph_create); replay it with .launch()."""
+        out = self.loss if loss_out is None else loss_out
+        return StepGraph(mdnn_train_graph_create(self.handle, x, target, out), (self, x, target, out))
+
     def step_async(self, x, target, loss_out=None, stream=None):
         """Asynchronous step (section 4.1) on a master vector shared with other
         workers: see mdnn_train_step_async."""
@@ -191,6 +207,29 @@ class Net:
     def close(self):
         if getattr(self, "handle", None):
             mdnn_net_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class StepGraph:
+    """A recorded train step.  Holds references to the net and the buffers
+    the graph reads and writes, so they outlive it."""
+
+    def __init__(self, handle: int, keep):
+        self.handle = handle
+        self._keep = keep
+
+    def launch(self, stream=None):
+        mdnn_graph_launch(self.handle, stream)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            mdnn_graph_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -171,6 +171,68 @@ __global__ void maxpool2_bwd_kernel(const typename T::storage* __restrict__ dy,
   }
 }
 
+// 16-bit storage, even h and w, c % 8 == 0: a thread owns eight channels of
+// one pooled position (16-byte loads and stores), 32-bit index arithmetic
+// (the caller checks the sizes).  Same window order and tie rule as above.
+__global__ void maxpool2_fwd_vec_kernel(const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                        uint8_t* __restrict__ arg, int32_t units, int32_t wo, int32_t c8,
+                                        int32_t c, bool bf16) {
+  const int32_t u = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (u >= units) return;
+  const int32_t cg = u % c8, t = u / c8;
+  const int32_t j = t % wo, r = t / wo;  // r = b * ho + i: input rows 2r, 2r + 1
+  const int64_t wc = (int64_t)2 * wo * c;
+  const uint16_t* p = x + (int64_t)2 * r * wc + (int64_t)2 * j * c + cg * 8;
+  uint4 cand[4] = {*(const uint4*)p, *(const uint4*)(p + c), *(const uint4*)(p + wc), *(const uint4*)(p + wc + c)};
+  const uint16_t* cv[4] = {(const uint16_t*)&cand[0], (const uint16_t*)&cand[1], (const uint16_t*)&cand[2],
+                           (const uint16_t*)&cand[3]};
+  uint16_t out[8];
+  uint8_t am[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    uint16_t best = cv[0][e];
+    float bv = bf16 ? bf16_to_f32(best) : f16_to_f32(best);
+    int bi = 0;
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const float v = bf16 ? bf16_to_f32(cv[k][e]) : f16_to_f32(cv[k][e]);
+      if (v > bv) { bv = v; best = cv[k][e]; bi = k; }
+    }
+    out[e] = best;
+    am[e] = (uint8_t)bi;
+  }
+  const int64_t o = ((int64_t)r * wo + j) * c + cg * 8;
+  *(uint4*)(y + o) = *(const uint4*)out;
+  if (arg) *(uint2*)(arg + o) = *(const uint2*)am;
+}
+
+__global__ void maxpool2_bwd_vec_kernel(const uint16_t* __restrict__ dy, const uint8_t* __restrict__ arg,
+                                        uint16_t* __restrict__ dx, int32_t units, int32_t wo, int32_t c8,
+                                        int32_t c) {
+  const int32_t u = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (u >= units) return;
+  const int32_t cg = u % c8, t = u / c8;
+  const int32_t j = t % wo, r = t / wo;
+  const int64_t o = ((int64_t)r * wo + j) * c + cg * 8;
+  const uint4 g = *(const uint4*)(dy + o);
+  const uint2 a = *(const uint2*)(arg + o);
+  const uint16_t* gv = (const uint16_t*)&g;
+  const uint8_t* av = (const uint8_t*)&a;
+  const int64_t wc = (int64_t)2 * wo * c;
+  uint16_t* q = dx + (int64_t)2 * r * wc + (int64_t)2 * j * c + cg * 8;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = av[e] == k ? gv[e] : (uint16_t)0;
+    *(uint4*)(q + (k >> 1) * wc + (k & 1) * c) = *(const uint4*)v;
+  }
+}
+
+static bool pool_vec_ok(int64_t n, int64_t h, int64_t w, int64_t c, mdnn_dtype_t t) {
+  return t != MDNN_F32 && h % 2 == 0 && w % 2 == 0 && c % 8 == 0 && n * h * w * c < ((int64_t)1 << 31);
+}
+
 // ---------------------------------------------------------------------------
 // losses: one block; waves own rows in a fixed order, block sum in a fixed order
 // ---------------------------------------------------------------------------
@@ -225,6 +287,56 @@ softmax_xent_kernel(int64_t B, int64_t C, const float* __restrict__ z, int64_t l
     for (int k = 0; k < nw; ++k) t += wsum[k];
     *loss_out = t * inv_b;
   }
+}
+
+// Few classes (C <= 32): one thread per row, so all rows run at once (a
+// wave per row would leave most lanes idle and walk the rows 16 at a time).
+// Thread t sums the losses of rows t, t + 1024, ... in order; the block then
+// adds the 1024 partial sums in a fixed tree order.
+constexpr int SMALL_C = 32;
+
+template <class OutT>
+__global__ void __launch_bounds__(LOSS_THREADS)
+softmax_xent_rows_kernel(int64_t B, int64_t C, const float* __restrict__ z, int64_t ldl,
+                         const int32_t* __restrict__ labels, const float* __restrict__ scale_p,
+                         float* __restrict__ loss_out, typename OutT::storage* __restrict__ dz, int64_t ldd) {
+  __shared__ float red[LOSS_THREADS];
+  const float S = scale_p ? *scale_p : 1.0f;
+  const float inv_b = 1.0f / (float)B;
+  float acc = 0.0f;
+  for (int64_t r = threadIdx.x; r < B; r += LOSS_THREADS) {
+    const float* zr = z + r * ldl;
+    float v[SMALL_C];
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < SMALL_C; ++j) {
+      v[j] = j < C ? zr[j] : -INFINITY;
+      m = fmaxf(m, v[j]);
+    }
+    float se = 0.0f;
+#pragma unroll
+    for (int j = 0; j < SMALL_C; ++j)
+      if (j < C) se += expf(v[j] - m);
+    const float lse = m + logf(se);
+    const int32_t lab = labels[r];
+    const bool ok = lab >= 0 && lab < C;
+#pragma unroll
+    for (int j = 0; j < SMALL_C; ++j) {
+      if (j < C) {
+        float g = S * (expf(v[j] - lse) - (j == lab ? 1.0f : 0.0f)) * inv_b;
+        if (!ok) g = NAN;
+        dz[r * ldd + j] = from_f<OutT>(g);
+      }
+    }
+    acc += ok ? (lse - zr[lab]) : NAN;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = LOSS_THREADS / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss_out = red[0] * inv_b;
 }
 
 template <class OutT>
@@ -456,6 +568,13 @@ extern "C" mdnn_status_t mdnn_maxpool2_fwd(int64_t n, int64_t h, int64_t w, int6
   if (!aligned(x, es) || !aligned(y, es)) return fail(MDNN_ERR_MISALIGNED, "maxpool2_fwd: misaligned");
   clear_error();
   hipStream_t st = as_stream(stream);
+  if (pool_vec_ok(n, h, w, c, dtype) && aligned(x, 16) && aligned(y, 16) && (!argmax || aligned(argmax, 8))) {
+    const int64_t units = total / 8;
+    hipLaunchKernelGGL(maxpool2_fwd_vec_kernel, dim3((unsigned)ceil_div(units, 256)), dim3(256), 0, st,
+                       (const uint16_t*)x, (uint16_t*)y, argmax, (int32_t)units, (int32_t)(w / 2), (int32_t)(c / 8),
+                       (int32_t)c, dtype == MDNN_BF16);
+    return check_launch("maxpool2_fwd_vec_kernel");
+  }
   unsigned g = grid_for(total, 256);
   if (g > 16384) g = 16384;
   switch (dtype) {
@@ -481,6 +600,13 @@ extern "C" mdnn_status_t mdnn_maxpool2_bwd(int64_t n, int64_t h, int64_t w, int6
   if ((dy && !aligned(dy, es)) || !aligned(dx, es)) return fail(MDNN_ERR_MISALIGNED, "maxpool2_bwd: misaligned");
   clear_error();
   hipStream_t st = as_stream(stream);
+  if (pool_vec_ok(n, h, w, c, dtype) && aligned(dy, 16) && aligned(dx, 16) && aligned(argmax, 8)) {
+    const int64_t units = n * (h / 2) * (w / 2) * (c / 8);
+    hipLaunchKernelGGL(maxpool2_bwd_vec_kernel, dim3((unsigned)ceil_div(units, 256)), dim3(256), 0, st,
+                       (const uint16_t*)dy, argmax, (uint16_t*)dx, (int32_t)units, (int32_t)(w / 2), (int32_t)(c / 8),
+                       (int32_t)c);
+    return check_launch("maxpool2_bwd_vec_kernel");
+  }
   unsigned g = grid_for(total, 256);
   if (g > 16384) g = 16384;
   switch (dtype) {
@@ -504,6 +630,14 @@ extern "C" mdnn_status_t mdnn_softmax_xent(int64_t B, int64_t C, const float* lo
     return fail(MDNN_ERR_MISALIGNED, "softmax_xent: misaligned buffer");
   clear_error();
   hipStream_t st = as_stream(stream);
+  if (C <= SMALL_C) {
+    switch (dlogits_type) {
+      case MDNN_F32: hipLaunchKernelGGL(softmax_xent_rows_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd); break;
+      case MDNN_F16: hipLaunchKernelGGL(softmax_xent_rows_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
+      default: hipLaunchKernelGGL(softmax_xent_rows_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
+    }
+    return check_launch("softmax_xent_rows_kernel");
+  }
   switch (dlogits_type) {
     case MDNN_F32: hipLaunchKernelGGL(softmax_xent_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd); break;
     case MDNN_F16: hipLaunchKernelGGL(softmax_xent_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;

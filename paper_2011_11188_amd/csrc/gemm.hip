@@ -32,36 +32,55 @@ __global__ void reduce_splits_kernel(const float* __restrict__ part, int splits,
   }
 }
 
-// Few outputs, many splits: block b sums outputs 64b .. 64b+63; thread
-// (g, j) sums splits g, g+16, g+32, ... of output j, then the 16 group sums
-// are added in order g = 0..15 (a fixed order: deterministic).
+// Few outputs, many splits: a block of 1024 threads sums OPB outputs with
+// G = 1024 / OPB split groups.  Thread (g, j) sums splits g, g+G, g+2G, ...
+// of output j into four interleaved accumulators (four loads in flight),
+// adds them in order, and the G group sums are combined by a fixed tree in
+// LDS: a fixed order, so the result is deterministic.
+template <int OPB>
 __global__ void __launch_bounds__(1024)
 reduce_splits_wide_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ out) {
-  __shared__ float red[16][64];
-  const int j = threadIdx.x & 63, g = threadIdx.x >> 6;
-  const int64_t e = (int64_t)blockIdx.x * 64 + j;
-  float s = 0.0f;
-  if (e < n)
-    for (int k = g; k < splits; k += 16) s += part[(int64_t)k * n + e];
-  red[g][j] = s;
-  __syncthreads();
-  if (g == 0 && e < n) {
-    float t = red[0][j];
-#pragma unroll
-    for (int q = 1; q < 16; ++q) t += red[q][j];
-    out[e] = t;
+  constexpr int G = 1024 / OPB;
+  __shared__ float red[G][OPB];
+  const int j = threadIdx.x % OPB, g = threadIdx.x / OPB;
+  const int64_t e = (int64_t)blockIdx.x * OPB + j;
+  float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+  if (e < n) {
+    int k = g;
+    for (; k + 3 * G < splits; k += 4 * G) {
+      s0 += part[(int64_t)k * n + e];
+      s1 += part[(int64_t)(k + G) * n + e];
+      s2 += part[(int64_t)(k + 2 * G) * n + e];
+      s3 += part[(int64_t)(k + 3 * G) * n + e];
+    }
+    for (; k < splits; k += G) s0 += part[(int64_t)k * n + e];
   }
+  red[g][j] = (s0 + s1) + (s2 + s3);
+  __syncthreads();
+#pragma unroll
+  for (int h = G / 2; h > 0; h >>= 1) {
+    if (g < h) red[g][j] += red[g + h][j];
+    __syncthreads();
+  }
+  if (g == 0 && e < n) out[e] = red[0][j];
+}
+
+static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream) {
+  if (n <= 16)
+    hipLaunchKernelGGL(reduce_splits_wide_kernel<16>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
+  else if (n <= 32)
+    hipLaunchKernelGGL(reduce_splits_wide_kernel<32>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
+  else
+    hipLaunchKernelGGL(reduce_splits_wide_kernel<64>, dim3((unsigned)ceil_div(n, 64)), dim3(1024), 0, stream,
+                       partial, splits, n, out);
+  return check_launch("reduce_splits_wide_kernel");
 }
 
 mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int64_t cols,
                             float* out, hipStream_t stream) {
   const int64_t n = rows * cols;
   if (n == 0) return MDNN_SUCCESS;
-  if (splits >= 32 && n <= ((int64_t)1 << 18)) {
-    hipLaunchKernelGGL(reduce_splits_wide_kernel, dim3((unsigned)ceil_div(n, 64)), dim3(1024), 0, stream,
-                       partial, splits, n, out);
-    return check_launch("reduce_splits_wide_kernel");
-  }
+  if (splits >= 32 && n <= ((int64_t)1 << 18)) return reduce_wide(partial, splits, n, out, stream);
   const int64_t blocks = ceil_div(ceil_div(n, 4), 256);
   hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, partial,
                      splits, n, out);
@@ -74,8 +93,9 @@ mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int6
 // With a workspace (two passes): pass 1 splits the rows into chunks of
 // COLSUM_ROWS; a block reduces one chunk x 64 columns (8 column groups of 8
 // read as 16-byte vectors, 32 row lanes, then a fixed-order combine in LDS)
-// into partial[chunk][col].  Pass 2 sums the partials of each column in chunk
-// order (8 lanes per column, strided, then a fixed-order combine).
+// into partial[chunk][col].  Pass 2 sums the partials of each column with
+// the split reduction below (many chunks) or 8 strided lanes per column (few
+// chunks), each combined in a fixed order.
 // Without a workspace: one block per 32 columns walks all rows (slow for very
 // tall matrices; kept for callers that cannot provide memory).
 constexpr int64_t COLSUM_ROWS = 256;
@@ -181,8 +201,11 @@ static void colsum_launch(const void* x, const void* y, int64_t rows, int64_t co
     const bool vec = aligned(x, 16) && (!y || aligned(y, 16)) && cols % 8 == 0;
     hipLaunchKernelGGL(colsum_partial_kernel<T>, dim3((unsigned)ceil_div(cols, 64), (unsigned)chunks), dim3(256),
                        0, st, (const S*)x, (const S*)y, rows, cols, vec, (float*)ws);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
-                       (const float*)ws, chunks, cols, out);
+    if (chunks >= 32 && cols <= ((int64_t)1 << 18))
+      (void)reduce_wide((const float*)ws, (int)chunks, cols, out, st);
+    else
+      hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
+                         (const float*)ws, chunks, cols, out);
   } else {
     hipLaunchKernelGGL(colsum_single_kernel<T>, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
                        (const S*)x, (const S*)y, rows, cols, out);
@@ -202,56 +225,193 @@ mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t 
 }
 
 // ---------------------------------------------------------------------------
+// fp32 split-K over a workspace
+// ---------------------------------------------------------------------------
+// A grid of few 64 x 64 tiles over K >= 64 is bound by the latency of its
+// serial K loop: split K so that about 256 workgroups run, each over at
+// least two K steps.
+static SplitPlan f32_split_plan(int64_t M, int64_t N, int64_t K) {
+  SplitPlan p{1, K};
+  const int64_t tiles = ceil_div(M, 64) * ceil_div(N, 64);
+  if (tiles >= 64 || K < 64) return p;
+  int64_t kps = ceil_div(ceil_div(K, ceil_div(256, tiles)), 16) * 16;
+  if (kps < 32) kps = 32;
+  p.splits = (int)ceil_div(K, kps);
+  p.k_per_split = kps;
+  if (p.splits > 65535) p = SplitPlan{1, K};
+  return p;
+}
+
+// out = epilogue(sum over splits of partial[s][m][n]).  A block covers 16
+// groups of four consecutive outputs of a row; its 16 thread rows sum splits
+// g, g+16, g+32, ... of each group, and the 16 row sums are added in row
+// order: a fixed order, so the result is deterministic.
+template <class MaskT, class OutT>
+__global__ void __launch_bounds__(256)
+reduce_splits_epilogue_kernel(const float* __restrict__ part, int splits, int64_t M, int64_t N, Epilogue ep) {
+  __shared__ float4_t rows[16][16];
+  const int ql = threadIdx.x & 15, g = threadIdx.x >> 4;
+  const int64_t groups = ceil_div(N, 4);
+  const int64_t q = (int64_t)blockIdx.x * 16 + ql;
+  const bool valid = q < M * groups;
+  const int64_t m = valid ? q / groups : 0, n = valid ? (q - m * groups) * 4 : 0;
+  const int64_t MN = M * N;
+  const bool vec = (N & 3) == 0;  // rows of 16-byte aligned quads (the workspace is 16-byte aligned)
+  float4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (valid) {
+    const float* p = part + m * N + n;
+    for (int s = g; s < splits; s += 16) {
+      const float* ps = p + (int64_t)s * MN;
+      if (vec) {
+        const float4 v = *(const float4*)ps;
+        acc[0] += v.x, acc[1] += v.y, acc[2] += v.z, acc[3] += v.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < N) acc[e] += ps[e];
+      }
+    }
+  }
+  rows[g][ql] = acc;
+  __syncthreads();
+  if (g != 0 || !valid) return;
+  float4_t tot = rows[0][ql];
+  for (int r = 1; r < 16; ++r) tot += rows[r][ql];
+  epilogue_store4<MaskT, OutT>(ep, M, N, m, n, tot);
+}
+
+template <class MaskT, class OutT>
+static mdnn_status_t reduce_epilogue(const void* ws, int splits, int64_t M, int64_t N, const Epilogue& ep,
+                                     hipStream_t st) {
+  const int64_t quads = M * ceil_div(N, 4);
+  if (ceil_div(quads, 16) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the reduction");
+  hipLaunchKernelGGL((reduce_splits_epilogue_kernel<MaskT, OutT>), dim3((unsigned)ceil_div(quads, 16)), dim3(256),
+                     0, st, (const float*)ws, splits, M, N, ep);
+  return check_launch("reduce_splits_epilogue_kernel");
+}
+
+// Low-precision problems whose grid of `tile` x `tile` tiles covers fewer
+// than half of the CUs, over K >= 256: split K (whole 64-deep steps, at
+// least two per split) so that about 256 workgroups run.
+static SplitPlan lp_split_plan(int64_t M, int64_t N, int64_t K, int64_t tile) {
+  SplitPlan p{1, K};
+  const int64_t tiles = ceil_div(M, tile) * ceil_div(N, tile);
+  if (tiles >= 128 || K < 256 || gemm_tile_override() != TILE_AUTO) return p;
+  int64_t sp = ceil_div(256, tiles);
+  if (sp > K / 128) sp = K / 128;
+  if (sp < 2) return p;
+  const int64_t kps = ceil_div(ceil_div(K, sp), 64) * 64;
+  p.splits = (int)ceil_div(K, kps);
+  p.k_per_split = kps;
+  if (p.splits < 2) p = SplitPlan{1, K};
+  return p;
+}
+
+static bool ws_fits(const SplitPlan& p, int64_t M, int64_t N, const void* ws, size_t ws_bytes) {
+  return p.splits > 1 && ws && aligned(ws, 16) && ws_bytes >= (size_t)p.splits * M * N * sizeof(float);
+}
+
+// ---------------------------------------------------------------------------
 // mdnn_gemm_mixed
 // ---------------------------------------------------------------------------
 template <class T, class OutT>
 static mdnn_status_t gemm_dispatch16(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
                                      const void* A, int64_t lda, bool va, const void* B,
-                                     int64_t ldb, bool vb, const Epilogue& ep, hipStream_t st) {
+                                     int64_t ldb, bool vb, const Epilogue& ep_in, void* ws, size_t ws_bytes,
+                                     hipStream_t st) {
   const uint16_t* a = (const uint16_t*)A;
   const uint16_t* b = (const uint16_t*)B;
   const LdsOperand la{A, lda, M, layout != MDNN_TN}, lb{B, ldb, N, layout == MDNN_NT};
-  if (lds_pipe_eligible(la, lb, M, N, K, K, 1)) {
-    switch (layout) {
-      case MDNN_NN: return run_gemm_lds<T, OutT, true, false>(la, lb, M, N, K, ep, 1, st);
-      case MDNN_NT: return run_gemm_lds<T, OutT, true, true>(la, lb, M, N, K, ep, 1, st);
-      default: return run_gemm_lds<T, OutT, false, false>(la, lb, M, N, K, ep, 1, st);
+  // split K over the workspace when the grid is small (partials in fp32,
+  // then the epilogue in a fixed-order reduction)
+  Epilogue ep = ep_in;
+  int splits = 1;
+  SplitPlan plan = lp_split_plan(M, N, K, 128);
+  bool pipe = ws_fits(plan, M, N, ws, ws_bytes) && lds_pipe_eligible(la, lb, M, N, K, plan.k_per_split, plan.splits);
+  if (pipe) {
+    splits = plan.splits;
+  } else {
+    pipe = lds_pipe_eligible(la, lb, M, N, K, K, 1);
+    if (!pipe) {
+      plan = lp_split_plan(M, N, K, 64);
+      if (ws_fits(plan, M, N, ws, ws_bytes)) splits = plan.splits;
     }
   }
-  switch (layout) {
-    case MDNN_NN:
-      return run_gemm16<T, OutT>(SrcMatK<uint16_t>{a, lda, M, K, va},
-                                 SrcMatMN<uint16_t>{b, ldb, N, K, vb}, M, N, K, ep, 1, st);
-    case MDNN_NT:
-      return run_gemm16<T, OutT>(SrcMatK<uint16_t>{a, lda, M, K, va},
-                                 SrcMatK<uint16_t>{b, ldb, N, K, vb}, M, N, K, ep, 1, st);
-    default:
-      return run_gemm16<T, OutT>(SrcMatMN<uint16_t>{a, lda, M, K, va},
-                                 SrcMatMN<uint16_t>{b, ldb, N, K, vb}, M, N, K, ep, 1, st);
+  if (splits > 1) {
+    ep.partial = (float*)ws;
+    ep.k_per_split = plan.k_per_split;
   }
+  if (pipe) {
+    switch (layout) {
+      case MDNN_NN: MDNN_TRY((run_gemm_lds<T, OutT, true, false>(la, lb, M, N, K, ep, splits, st))); break;
+      case MDNN_NT: MDNN_TRY((run_gemm_lds<T, OutT, true, true>(la, lb, M, N, K, ep, splits, st))); break;
+      default: MDNN_TRY((run_gemm_lds<T, OutT, false, false>(la, lb, M, N, K, ep, splits, st)));
+    }
+  } else {
+    switch (layout) {
+      case MDNN_NN:
+        MDNN_TRY((run_gemm16<T, OutT>(SrcMatK<uint16_t>{a, lda, M, K, va}, SrcMatMN<uint16_t>{b, ldb, N, K, vb}, M,
+                                      N, K, ep, splits, st)));
+        break;
+      case MDNN_NT:
+        MDNN_TRY((run_gemm16<T, OutT>(SrcMatK<uint16_t>{a, lda, M, K, va}, SrcMatK<uint16_t>{b, ldb, N, K, vb}, M,
+                                      N, K, ep, splits, st)));
+        break;
+      default:
+        MDNN_TRY((run_gemm16<T, OutT>(SrcMatMN<uint16_t>{a, lda, M, K, va}, SrcMatMN<uint16_t>{b, ldb, N, K, vb},
+                                      M, N, K, ep, splits, st)));
+    }
+  }
+  if (splits == 1) return MDNN_SUCCESS;
+  return reduce_epilogue<T, OutT>(ws, splits, M, N, ep_in, st);
 }
 
 static mdnn_status_t gemm_dispatch32(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
                                      const void* A, int64_t lda, const void* B, int64_t ldb,
-                                     const Epilogue& ep, hipStream_t st) {
+                                     const Epilogue& ep_in, void* ws, size_t ws_bytes, hipStream_t st) {
   const float* a = (const float*)A;
   const float* b = (const float*)B;
+  Epilogue ep = ep_in;
+  const SplitPlan plan = f32_split_plan(M, N, K);
+  const bool split = ws_fits(plan, M, N, ws, ws_bytes);
+  int splits = 1;
+  if (split) {
+    ep.partial = (float*)ws;
+    ep.k_per_split = plan.k_per_split;
+    splits = plan.splits;
+  }
   switch (layout) {
     case MDNN_NN:
-      return run_gemm32(SrcMatK<float>{a, lda, M, K, false}, SrcMatMN<float>{b, ldb, N, K, false},
-                        M, N, K, ep, 1, st);
+      MDNN_TRY(run_gemm32(SrcMatK<float>{a, lda, M, K, false}, SrcMatMN<float>{b, ldb, N, K, false},
+                          M, N, K, ep, splits, st));
+      break;
     case MDNN_NT:
-      return run_gemm32(SrcMatK<float>{a, lda, M, K, false}, SrcMatK<float>{b, ldb, N, K, false},
-                        M, N, K, ep, 1, st);
+      MDNN_TRY(run_gemm32(SrcMatK<float>{a, lda, M, K, false}, SrcMatK<float>{b, ldb, N, K, false},
+                          M, N, K, ep, splits, st));
+      break;
     default:
-      return run_gemm32(SrcMatMN<float>{a, lda, M, K, false}, SrcMatMN<float>{b, ldb, N, K, false},
-                        M, N, K, ep, 1, st);
+      MDNN_TRY(run_gemm32(SrcMatMN<float>{a, lda, M, K, false}, SrcMatMN<float>{b, ldb, N, K, false},
+                          M, N, K, ep, splits, st));
   }
+  if (!split) return MDNN_SUCCESS;
+  return reduce_epilogue<F32, F32>(ws, splits, M, N, ep_in, st);
 }
 
 }  // namespace mdnn
 
 using namespace mdnn;
+
+size_t mdnn::gemm_ws_bytes(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K <= 0 || !dtype_ok(ab_type)) return 0;
+  int splits = 1;
+  if (ab_type == MDNN_F32) {
+    splits = f32_split_plan(M, N, K).splits;
+  } else {  // either kernel family may run: room for the larger plan
+    const int s128 = lp_split_plan(M, N, K, 128).splits, s64 = lp_split_plan(M, N, K, 64).splits;
+    splits = s128 > s64 ? s128 : s64;
+  }
+  return splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+}
 
 extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
                                          float alpha, const void* A, int64_t lda, const void* B,
@@ -259,6 +419,29 @@ extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_
                                          const void* C, int64_t ldc, void* D, int64_t ldd,
                                          mdnn_dtype_t d_type, const float* bias, mdnn_act_t act,
                                          const void* mask_src, int64_t ldm, mdnn_stream_t stream) {
+  return gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, C, ldc, D, ldd, d_type, bias, act,
+                       mask_src, ldm, nullptr, 0, stream);
+}
+
+extern "C" size_t mdnn_gemm_workspace(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K) {
+  return gemm_ws_bytes(ab_type, M, N, K);
+}
+
+extern "C" mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, float alpha,
+                                            const void* A, int64_t lda, const void* B, int64_t ldb,
+                                            mdnn_dtype_t ab_type, float beta, const void* C, int64_t ldc, void* D,
+                                            int64_t ldd, mdnn_dtype_t d_type, const float* bias, mdnn_act_t act,
+                                            const void* mask_src, int64_t ldm, void* workspace, size_t ws_bytes,
+                                            mdnn_stream_t stream) {
+  return gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, C, ldc, D, ldd, d_type, bias, act,
+                       mask_src, ldm, workspace, ws_bytes, stream);
+}
+
+mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, float alpha,
+                                  const void* A, int64_t lda, const void* B, int64_t ldb, mdnn_dtype_t ab_type,
+                                  float beta, const void* C, int64_t ldc, void* D, int64_t ldd,
+                                  mdnn_dtype_t d_type, const float* bias, mdnn_act_t act, const void* mask_src,
+                                  int64_t ldm, void* ws, size_t ws_bytes, mdnn_stream_t stream) {
   if (layout != MDNN_NN && layout != MDNN_NT && layout != MDNN_TN)
     return fail(MDNN_ERR_LAYOUT, "gemm: unknown layout %d", (int)layout);
   if (M < 0 || N < 0 || K < 0) return fail(MDNN_ERR_SHAPE, "gemm: negative size");
@@ -304,15 +487,17 @@ extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_
   hipStream_t st = as_stream(stream);
   clear_error();
 
-  if (ab_type == MDNN_F32) return gemm_dispatch32(layout, M, N, K, A, lda, B, ldb, ep, st);
+  if (ab_type == MDNN_F32) return gemm_dispatch32(layout, M, N, K, A, lda, B, ldb, ep, ws, ws_bytes, st);
   const bool va = aligned(A, 16) && lda % 8 == 0;
   const bool vb = aligned(B, 16) && ldb % 8 == 0;
   if (ab_type == MDNN_F16) {
-    if (d_type == MDNN_F32) return gemm_dispatch16<F16, F32>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, st);
-    return gemm_dispatch16<F16, F16>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, st);
+    if (d_type == MDNN_F32)
+      return gemm_dispatch16<F16, F32>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
+    return gemm_dispatch16<F16, F16>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
   }
-  if (d_type == MDNN_F32) return gemm_dispatch16<BF16, F32>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, st);
-  return gemm_dispatch16<BF16, BF16>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, st);
+  if (d_type == MDNN_F32)
+    return gemm_dispatch16<BF16, F32>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
+  return gemm_dispatch16<BF16, BF16>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
 }
 
 extern "C" int mdnn_set_gemm_tile(int code) {

@@ -8,15 +8,21 @@
 
 namespace mdnn {
 
-// fp32 path: 64x64 tiles, 256 threads, 4x4 outputs per thread, K step 16,
-// operands staged through LDS element by element (vector FMA; config-sized
-// fp32 problems are small and latency-bound).
-template <class SrcA, class SrcB>
-__global__ void __launch_bounds__(256)
+// fp32 path: 64x64 tiles, 4x4 outputs per thread, K step 16, operands staged
+// through LDS element by element (vector FMA; config-sized fp32 problems are
+// small and latency-bound).  KG groups of 256 threads split the tile's K range
+// among themselves and combine their sums through LDS in group order (fixed,
+// so deterministic): a grid of only a few tiles over a long K then keeps KG
+// times as many waves busy.
+template <class SrcA, class SrcB, int KG>
+__global__ void __launch_bounds__(256 * KG)
 gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
-  __shared__ float As[16][64 + 4];
-  __shared__ float Bs[16][64 + 4];
-  const int tid = threadIdx.x;
+  constexpr int STAGE = 2 * 16 * 68;  // As + Bs of one group
+  constexpr int RED = (KG - 1) * 64 * 64;
+  __shared__ float smem[KG * STAGE > RED ? KG * STAGE : RED];
+  const int grp = threadIdx.x >> 8, tid = threadIdx.x & 255;
+  float(*As)[68] = (float(*)[68])(smem + grp * STAGE);
+  float(*Bs)[68] = (float(*)[68])(smem + grp * STAGE + 16 * 68);
   const int tx = tid & 15, ty = tid >> 4;
   const int64_t m0 = (int64_t)blockIdx.x * 64, n0 = (int64_t)blockIdx.y * 64;
   int64_t kbeg = 0, kend = K;
@@ -24,16 +30,41 @@ gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
     kbeg = (int64_t)blockIdx.z * ep.k_per_split;
     kend = kbeg + ep.k_per_split < K ? kbeg + ep.k_per_split : K;
   }
+  // this group's share of [kbeg, kend), whole K steps; every group runs the
+  // same number of steps (the barriers are block-wide)
+  const int64_t steps = ceil_div(kend - kbeg, 16), per = ceil_div(steps, KG);
+  const int64_t gbeg = kbeg + grp * per * 16;
+  const int64_t gend = gbeg + per * 16 < kend ? gbeg + per * 16 : kend;
+  // staging: thread tid owns elements tid + 256 q (q < 4) of each 64 x 16
+  // operand slab; the next step's elements are loaded into registers while
+  // the current step computes (one memory latency per step, overlapped)
+  int sr[2][4], sk[2][4];  // (row, k) of each owned element, per operand
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int idx = tid + q * 256;
+    sr[0][q] = SrcA::KC ? idx >> 4 : idx & 63;
+    sk[0][q] = SrcA::KC ? idx & 15 : idx >> 6;
+    sr[1][q] = SrcB::KC ? idx >> 4 : idx & 63;
+    sk[1][q] = SrcB::KC ? idx & 15 : idx >> 6;
+  }
+  float ra[4], rb[4];
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ra[q] = (k0 + sk[0][q] < gend) ? (float)a.elem(m0 + sr[0][q], k0 + sk[0][q]) : 0.0f;
+      rb[q] = (k0 + sk[1][q] < gend) ? (float)b.elem(n0 + sr[1][q], k0 + sk[1][q]) : 0.0f;
+    }
+  };
   float acc[4][4] = {};
-  for (int64_t k0 = kbeg; k0 < kend; k0 += 16) {
-    for (int idx = tid; idx < 64 * 16; idx += 256) {
-      int r, kk;
-      if (SrcA::KC) { r = idx >> 4; kk = idx & 15; } else { kk = idx >> 6; r = idx & 63; }
-      As[kk][r] = (k0 + kk < kend) ? a.elem(m0 + r, k0 + kk) : 0.0f;
-      if (SrcB::KC) { r = idx >> 4; kk = idx & 15; } else { kk = idx >> 6; r = idx & 63; }
-      Bs[kk][r] = (k0 + kk < kend) ? b.elem(n0 + r, k0 + kk) : 0.0f;
+  if (per > 0) fetch(gbeg);
+  for (int64_t it = 0; it < per; ++it) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      As[sk[0][q]][sr[0][q]] = ra[q];
+      Bs[sk[1][q]][sr[1][q]] = rb[q];
     }
     __syncthreads();
+    if (it + 1 < per) fetch(gbeg + (it + 1) * 16);
 #pragma unroll
     for (int kk = 0; kk < 16; ++kk) {
       float av[4], bv[4];
@@ -45,6 +76,22 @@ gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
         for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
     }
     __syncthreads();
+  }
+  if (KG > 1) {
+    // groups 1.. hand their sums to group 0, which adds them in group order
+    if (grp > 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) smem[(grp - 1) * 4096 + (ty * 4 + i) * 64 + tx * 4 + j] = acc[i][j];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+    for (int g = 1; g < KG; ++g)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += smem[(g - 1) * 4096 + (ty * 4 + i) * 64 + tx * 4 + j];
   }
   const int64_t n = n0 + tx * 4;
 #pragma unroll
@@ -176,7 +223,13 @@ inline mdnn_status_t run_gemm32(const SrcA& a, const SrcB& b, int64_t M, int64_t
   if (ceil_div(M, 64) > 0x7fffffffLL || ceil_div(N, 64) > 65535 || splits > 65535)
     return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the fp32 launch grid");
   dim3 grid((unsigned)ceil_div(M, 64), (unsigned)ceil_div(N, 64), (unsigned)splits);
-  hipLaunchKernelGGL((gemm_f32_kernel<SrcA, SrcB>), grid, dim3(256), 0, stream, a, b, M, N, K, ep);
+  // few workgroups over a long K: four K groups per tile
+  const int64_t blocks = (int64_t)grid.x * grid.y * grid.z;
+  const int64_t k_each = splits > 1 ? ep.k_per_split : K;
+  if (blocks < 128 && k_each >= 256)
+    hipLaunchKernelGGL((gemm_f32_kernel<SrcA, SrcB, 4>), grid, dim3(1024), 0, stream, a, b, M, N, K, ep);
+  else
+    hipLaunchKernelGGL((gemm_f32_kernel<SrcA, SrcB, 1>), grid, dim3(256), 0, stream, a, b, M, N, K, ep);
   return check_launch("gemm_f32_kernel");
 }
 

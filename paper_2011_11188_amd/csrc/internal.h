@@ -51,4 +51,15 @@ size_t column_sums_ws_bytes(int64_t rows, int64_t cols);
 mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
                           float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+// mdnn_gemm_mixed with an optional workspace (NULL / too small: same as
+// mdnn_gemm_mixed).  With one, fp32 problems whose grid would be a handful of
+// tiles over a long K split K across workgroups and reduce the fp32
+// partials in split order (deterministic) before the epilogue.
+size_t gemm_ws_bytes(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K);
+mdnn_status_t gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, float alpha, const void* A,
+                            int64_t lda, const void* B, int64_t ldb, mdnn_dtype_t ab_type, float beta,
+                            const void* C, int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
+                            const float* bias, mdnn_act_t act, const void* mask_src, int64_t ldm, void* ws,
+                            size_t ws_bytes, mdnn_stream_t stream);
+
 }  // namespace mdnn

@@ -12,7 +12,8 @@
 //   argmax[i]       window index of each max-pool output
 //   grad0, grad1    ping-pong buffers for activation gradients (low precision)
 //   reduce_ws       split-K partials of the convolution backward-filter and
-//                   partial column sums of the bias gradients
+//                   of fp32 fully connected GEMMs, partial column sums of the
+//                   bias gradients (the users run one after another)
 #include <new>
 #include <vector>
 
@@ -153,8 +154,11 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
       if (need > fws) fws = need;
     }
     if (p.L.kind == MDNN_LAYER_FC) {
-      size_t need = mdnn_bias_act_bwd_workspace(batch, p.L.c_out);
-      if (need > fws) fws = need;
+      const int64_t in = p.L.c_in, o = p.L.c_out;
+      const size_t needs[4] = {mdnn_bias_act_bwd_workspace(batch, o), gemm_ws_bytes(net->lp, batch, o, in),
+                               gemm_ws_bytes(net->lp, in, o, batch), gemm_ws_bytes(net->lp, batch, in, o)};
+      for (size_t need : needs)
+        if (need > fws) fws = need;
     }
     if (p.in_feat > max_feat) max_feat = p.in_feat;
     if (p.out_feat > max_feat) max_feat = p.out_feat;
@@ -253,9 +257,9 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     const float* bias = net->master + p.b_off;
     const mdnn_act_t act = (mdnn_act_t)p.L.act;
     if (p.L.kind == MDNN_LAYER_FC) {
-      MDNN_TRY(mdnn_gemm_mixed(MDNN_NN, B, p.L.c_out, p.L.c_in, 1.0f, act_ptr(i), p.L.c_in, wptr(p),
-                               p.L.c_out, lp, 0.0f, nullptr, 0, act_ptr(i + 1), p.L.c_out, out_t, bias,
-                               act, nullptr, 0, stream));
+      MDNN_TRY(gemm_mixed_ws(MDNN_NN, B, p.L.c_out, p.L.c_in, 1.0f, act_ptr(i), p.L.c_in, wptr(p), p.L.c_out,
+                             lp, 0.0f, nullptr, 0, act_ptr(i + 1), p.L.c_out, out_t, bias, act, nullptr, 0,
+                             ws + net->fws_off, net->fws_bytes, stream));
     } else if (p.L.kind == MDNN_LAYER_CONV) {
       mdnn_conv_shape_t cs = conv_shape(p.L, B);
       MDNN_TRY(mdnn_conv2d_fwd(&cs, act_ptr(i), wptr(p), lp, bias, act, act_ptr(i + 1), out_t, stream));
@@ -288,14 +292,14 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     if (p.L.kind == MDNN_LAYER_FC) {
       const int64_t in = p.L.c_in, o = p.L.c_out;
       // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
-      MDNN_TRY(mdnn_gemm_mixed(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o,
-                               MDNN_F32, nullptr, MDNN_ACT_NONE, nullptr, 0, stream));
+      MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
+                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream));
       MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp,
                                  ws + net->fws_off, net->fws_bytes, stream));
       if (ii > 0) {
         // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
-        MDNN_TRY(mdnn_gemm_mixed(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0,
-                                 gnxt, in, lp, nullptr, MDNN_ACT_NONE, mask, in, stream));
+        MDNN_TRY(gemm_mixed_ws(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0, gnxt, in, lp,
+                               nullptr, MDNN_ACT_NONE, mask, in, ws + net->fws_off, net->fws_bytes, stream));
       }
     } else if (p.L.kind == MDNN_LAYER_CONV) {
       mdnn_conv_shape_t cs = conv_shape(p.L, B);
@@ -328,4 +332,72 @@ extern "C" mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const 
 extern "C" mdnn_status_t mdnn_train_step_async(mdnn_net_t* net, const float* x, const void* target,
                                                float* loss_out, mdnn_stream_t stream) {
   return run_step(net, x, target, loss_out, stream, true);
+}
+
+// ---------------------------------------------------------------------------
+// Recorded steps: one mdnn_train_step captured into a HIP graph, replayed
+// with a single launch (the small configurations are bound by launch
+// latency, not by their kernels).
+// ---------------------------------------------------------------------------
+struct mdnn_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+extern "C" mdnn_status_t mdnn_train_graph_create(mdnn_net_t* net, const float* x, const void* target,
+                                                 float* loss_out, mdnn_graph_t** out) {
+  if (!out) return fail(MDNN_ERR_NULL, "train_graph_create: out is NULL");
+  *out = nullptr;
+  if (!net) return fail(MDNN_ERR_NULL, "train_graph_create: NULL net");
+  if (!net->bound) return fail(MDNN_ERR_STATE, "train_graph_create: net not bound");
+  // capture on a private stream (the legacy default stream cannot be captured)
+  hipStream_t s = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail(MDNN_ERR_LAUNCH, "train_graph_create: stream: %s", hipGetErrorString(e));
+  e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    (void)hipStreamDestroy(s);
+    return fail(MDNN_ERR_LAUNCH, "train_graph_create: begin capture: %s", hipGetErrorString(e));
+  }
+  const mdnn_status_t st = run_step(net, x, target, loss_out, (mdnn_stream_t)s, false);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(s, &graph);  // always end the capture, also after a failed step
+  (void)hipStreamDestroy(s);
+  if (st != MDNN_SUCCESS) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return st;  // the step's own message stays
+  }
+  if (e != hipSuccess || !graph)
+    return fail(MDNN_ERR_LAUNCH, "train_graph_create: end capture: %s", hipGetErrorString(e));
+  hipGraphExec_t exec = nullptr;
+  e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    (void)hipGraphDestroy(graph);
+    return fail(MDNN_ERR_LAUNCH, "train_graph_create: instantiate: %s", hipGetErrorString(e));
+  }
+  mdnn_graph_t* g = new (std::nothrow) mdnn_graph_t;
+  if (!g) {
+    (void)hipGraphExecDestroy(exec);
+    (void)hipGraphDestroy(graph);
+    return fail(MDNN_ERR_STATE, "train_graph_create: out of host memory");
+  }
+  g->graph = graph;
+  g->exec = exec;
+  *out = g;
+  clear_error();
+  return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_graph_launch(mdnn_graph_t* g, mdnn_stream_t stream) {
+  if (!g || !g->exec) return fail(MDNN_ERR_NULL, "graph_launch: NULL graph");
+  const hipError_t e = hipGraphLaunch(g->exec, as_stream(stream));
+  if (e != hipSuccess) return fail(MDNN_ERR_LAUNCH, "graph_launch: %s", hipGetErrorString(e));
+  return MDNN_SUCCESS;
+}
+
+extern "C" void mdnn_graph_destroy(mdnn_graph_t* g) {
+  if (!g) return;
+  if (g->exec) (void)hipGraphExecDestroy(g->exec);
+  if (g->graph) (void)hipGraphDestroy(g->graph);
+  delete g;
 }

@@ -110,6 +110,26 @@ def test_other_entry_points_reject_bad_arguments(m):
     assert e.value.status == m.ERR_NULL
 
 
+def test_gemm_workspace_plan(m):
+    """Host-side split plan of mdnn_gemm_mixed_ws: shapes whose output is a
+    few tiles over a long K ask for fp32 partials, others for nothing."""
+    for dt in (m.F32, m.F16, m.BF16):
+        for (mm, n, k) in [(256, 10, 1024), (70, 136, 1000), (64, 128, 784)]:
+            nb = m.mdnn_gemm_workspace(dt, mm, n, k)
+            assert nb > 0 and nb % (4 * mm * n) == 0, (dt, mm, n, k)
+        assert m.mdnn_gemm_workspace(dt, 4096, 4096, 4096) == 0
+        assert m.mdnn_gemm_workspace(dt, 64, 64, 32) == 0
+        assert m.mdnn_gemm_workspace(dt, -1, 64, 1024) == 0
+    # 16 tiles of 128 x 128 split for fp16; 64 fp32 tiles of 64 x 64 do not
+    assert m.mdnn_gemm_workspace(m.F16, 256, 1024, 3136) > 0
+    assert m.mdnn_gemm_workspace(m.F32, 256, 1024, 3136) == 0
+    assert m.mdnn_gemm_workspace(7, 64, 128, 784) == 0
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_gemm_mixed_ws(7, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0, None, 0, None, 0,
+                             FAKE, 1024, stream=0)
+    assert e.value.status == m.ERR_LAYOUT
+
+
 def test_split_entry_points_reject_bad_arguments(m):
     with pytest.raises(m.MdnnError) as e:                    # scale not a power of two
         m.mdnn_split_f16(4, 4, FAKE, 4, 3.0, FAKE, 4, FAKE, 4, stream=0)
@@ -155,6 +175,17 @@ def test_net_create_validates_the_chain(m):
     with pytest.raises(m.MdnnError) as e:
         m.mdnn_train_step(h, FAKE, FAKE, FAKE, stream=0)                 # not bound
     assert e.value.status == m.ERR_STATE
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_train_graph_create(h, FAKE, FAKE, FAKE)                   # not bound
+    assert e.value.status == m.ERR_STATE
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_train_graph_create(None, FAKE, FAKE, FAKE)
+    assert e.value.status == m.ERR_NULL
+    assert m._lib.mdnn_train_graph_create(h, FAKE, FAKE, FAKE, None) == m.ERR_NULL   # out NULL
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_graph_launch(None, stream=0)
+    assert e.value.status == m.ERR_NULL
+    m.mdnn_graph_destroy(None)
     m.mdnn_net_destroy(h)
     bad = list(good)
     bad[2] = L(m.LAYER_FC, 1, 100, 1, 1, 64, 0, 0, 0)                     # size mismatch

@@ -104,10 +104,13 @@ def test_column_sums_tall_and_wide(mdnn, shape):
     assert torch.equal(db, db2)
 
 
+# c = 12: element-wise kernels; c = 16 and 64 (16-bit types): eight channels
+# per thread with 16-byte accesses
+@pytest.mark.parametrize("c", [12, 16, 64])
 @pytest.mark.parametrize("dt", ["f16", "bf16", "f32"])
-def test_maxpool_bitexact_with_ties(mdnn, dt):
+def test_maxpool_bitexact_with_ties(mdnn, dt, c):
     import torch
-    n, h, w, c = 3, 10, 14, 12
+    n, h, w = 3, 10, 14
     x = W.small_ints((n, h, w, c), 23, 1, lo=-2, hi=2, dtype=dt)     # many ties
     X = dev(x, dt)
     y = empty((n, h // 2, w // 2, c), dt)
@@ -140,10 +143,13 @@ def test_maxpool_odd_sizes(mdnn):
     assert np.array_equal(host64(dx), ops.maxpool2_bwd(yw, aw, h, w))
 
 
+# (256, 10) and (3000, 7): a thread per row (few classes; B > 1024 walks
+# rows in turns); (100, 33) and (5, 1000): a wave per row.
+@pytest.mark.parametrize("shape", [(256, 10), (3000, 7), (100, 33), (5, 1000)])
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-def test_softmax_xent(mdnn, dt):
+def test_softmax_xent(mdnn, dt, shape):
     import torch
-    B, Cn = 256, 10
+    B, Cn = shape
     z = W.normal((B, Cn), 25, 1, "f32", 3.0)
     lab = W.rng(25, 2).integers(0, Cn, B).astype(np.int32)
     scale = torch.tensor([256.0], dtype=torch.float32, device="cuda")

@@ -175,17 +175,35 @@ def test_gemm_relu_mask_epilogue(mdnn, dt):
     assert np.all(got[decode(y_in, dt) <= 0] == 0)
 
 
-def test_gemm_fp32_path(mdnn):
+# (70, 130, 200): one K group per tile; the others leave fewer than 128
+# workgroups over K >= 256, so four K groups share each tile (a ragged last
+# group at K = 784 and 1001).
+@pytest.mark.parametrize("mnk", [(70, 130, 200), (64, 128, 784), (33, 10, 1001)])
+def test_gemm_fp32_path(mdnn, mnk):
     for layout in ("NN", "NT", "TN"):
-        m, n, k = 70, 130, 200
+        m, n, k = mnk
         sa, sb = _shapes(layout, m, n, k)
         a = W.normal(sa, 8, 1, "f32")
         b = W.normal(sb, 8, 2, "f32")
         bias = W.normal((n,), 8, 3, "f32")
         got = _run(mdnn, layout, dev(a, "f32"), dev(b, "f32"), "f32", m, n, k, bias=dev(bias, "f32"), act=1)
-        want = ops.bias_act(ops.gemm(layout, a.astype(np.float64), b.astype(np.float64)),
-                            bias.astype(np.float64), "relu")
-        assert norm_max_err(got, want) <= 1e-6
+        a64, b64 = a.astype(np.float64), b.astype(np.float64)
+        want = ops.bias_act(ops.gemm(layout, a64, b64), bias.astype(np.float64), "relu")
+        # fp32 inputs: each product rounds too, gamma_{k+1} covers it
+        err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)) + np.abs(bias), k + 1)
+        assert np.all(np.abs(got - want) <= err)
+
+
+def test_gemm_fp32_k_groups_integer_exact(mdnn):
+    """Four K groups per tile summed in a fixed order: small integers stay
+    exact, so the result is bit-identical to the exact product."""
+    m, n, k = 64, 128, 784
+    for layout in ("NN", "NT", "TN"):
+        sa, sb = _shapes(layout, m, n, k)
+        a = W.small_ints(sa, 10, 1, dtype="f32")
+        b = W.small_ints(sb, 10, 2, dtype="f32")
+        got = _run(mdnn, layout, dev(a, "f32"), dev(b, "f32"), "f32", m, n, k)
+        assert np.array_equal(got, ops.gemm(layout, a.astype(np.float64), b.astype(np.float64)))
 
 
 def test_gemm_k_zero_and_empty(mdnn):
