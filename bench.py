@@ -121,7 +121,7 @@ def _measure(fn, min_ms=50.0, chunks=3):
     return sorted(res)[len(res) // 2]
 
 
-def _time_steps(net, xs, ts, steps, warmup):
+def _time_steps(net, xs, ts, steps, warmup, check=None):
     it = iter(range(1 << 62))
 
     def one():
@@ -130,13 +130,41 @@ def _time_steps(net, xs, ts, steps, warmup):
     _warm(one)
     for i in range(warmup):
         net.step(xs[i % len(xs)], ts[i % len(ts)])
+    _sync()
+    if check is not None:
+        check.start()
     with _Timer() as tm:
         for i in range(steps):
             net.step(xs[i % len(xs)], ts[i % len(ts)])
     return tm.ms / steps
 
 
-def _time_graph_steps(net, xs, ts, steps, warmup):
+class _UpdateCheck:
+    """Whether every step between start() and stop() applied its update.  A
+    loss-scaled step that overflows skips its update (and halves the scale);
+    a timed step must do the whole step's work, so the benchmark checks the
+    scaler's state machine: with no overflow, good_steps advanced by exactly
+    the number of steps (modulo growth_interval, where the scale grows)."""
+
+    def __init__(self, mdnn, net):
+        self.mdnn, self.net = mdnn, net
+        self.before = None
+
+    def start(self):
+        if self.net.scaler is not None:
+            self.before = self.mdnn.read_scaler(self.net.scaler)
+
+    def stop(self, steps: int) -> bool:
+        if self.net.scaler is None:
+            return True
+        b, a = self.before, self.mdnn.read_scaler(self.net.scaler)
+        total = b["good_steps"] + steps
+        gi = b["growth_interval"]
+        grown = b["scale"] * b["growth"] ** (total // gi)
+        return a["good_steps"] == total % gi and a["scale"] == grown
+
+
+def _time_graph_steps(net, xs, ts, steps, warmup, check=None):
     """As _time_steps, with each batch's step recorded once into a HIP graph
     and replayed (one launch per step instead of one per kernel)."""
     graphs = [net.record_step(x, t) for x, t in zip(xs, ts)]
@@ -147,6 +175,9 @@ def _time_graph_steps(net, xs, ts, steps, warmup):
     _warm(one)
     for i in range(warmup):
         graphs[i % len(graphs)].launch()
+    _sync()
+    if check is not None:
+        check.start()
     with _Timer() as tm:
         for i in range(steps):
             graphs[i % len(graphs)].launch()
@@ -451,12 +482,17 @@ def main():
     clocks_before = _clocks()
     cfg = W.wide_mlp_fp16()
     net, xs, ts = _train_setup(mdnn, cfg)
-    ms = _time_steps(net, xs, ts, args.steps, args.warmup)
+    check = _UpdateCheck(mdnn, net)
+    ms = _time_steps(net, xs, ts, args.steps, args.warmup, check)
+    applied = check.stop(args.steps)
+    if not applied:
+        print("[bench] WARNING: a timed step overflowed and skipped its update", file=sys.stderr, flush=True)
     samples = cfg.batch / (ms * 1e-3)
     step_tf = cfg.flops_per_step() / (ms * 1e-3) / 1e12
     print(f"[bench] {cfg.name}: {ms:.3f} ms/step, {samples:.0f} samples/s, "
           f"{step_tf:.1f} TFLOP/s", file=sys.stderr, flush=True)
-    graph_ms = _time_graph_steps(net, xs, ts, args.steps, args.warmup)
+    graph_ms = _time_graph_steps(net, xs, ts, args.steps, args.warmup, check)
+    graph_applied = check.stop(args.steps)
     print(f"[bench] {cfg.name} as a recorded graph: {graph_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     # dominant kernel: the kernel instantiation (layout, output type, tile)
@@ -504,6 +540,7 @@ def main():
                    "global_batch": cfg.batch, "parallelism": "single GPU",
                    "step_tflops": round(step_tf, 1),
                    "graph_ms_per_step": round(graph_ms, 4),
+                   "every_timed_update_applied": bool(applied and graph_applied),
                    "step_mfma_frac": round(step_tf / PEAK_F16_TFLOPS, 4),
                    "flop_per_step": cfg.flops_per_step()},
         "roofline": roofline,

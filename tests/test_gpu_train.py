@@ -94,6 +94,27 @@ def test_wide_mlp_fp16_full_size_two_steps(mdnn):
     _check(gl, ol)
 
 
+@pytest.mark.timeout(300)
+def test_wide_mlp_full_size_trains_without_skipped_updates(mdnn):
+    """The benchmark's workload over 60 steps cycling over 10 batches (as the
+    benchmark feeds it): no step overflows (every update is applied, the
+    scale stays 2^16) and the loss falls well below its start."""
+    import torch
+    cfg = W.wide_mlp_fp16()
+    net = _gpu_net(mdnn, cfg)
+    dev_b = []
+    for s in range(10):
+        x, t = W.batch_inputs(cfg, s)
+        dev_b.append((dev(x, "f32"), _target(cfg, t)))
+    losses = torch.zeros(60, device="cuda")
+    for i in range(60):
+        net.step(*dev_b[i % 10], loss_out=losses[i:i + 1])
+    ls = losses.cpu().numpy()
+    sc = mdnn.read_scaler(net.scaler)
+    assert sc["good_steps"] == 60 and sc["scale"] == 2.0 ** 16 and sc["overflow"] == 0
+    assert np.all(np.isfinite(ls)) and ls[-10:].mean() < 0.5 * ls[0], ls
+
+
 def test_forced_overflow_skips_steps(mdnn):
     """Initial loss scale 2^40: the scaled fp16 loss gradient overflows, the
     update is skipped and the scale halves until it fits; the trajectory
