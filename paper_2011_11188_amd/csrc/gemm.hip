@@ -3,6 +3,7 @@
 #include <atomic>
 
 #include "gemm_launch.h"
+#include "gemm_skinny.h"
 
 namespace mdnn {
 
@@ -290,6 +291,16 @@ static mdnn_status_t reduce_epilogue(const void* ws, int splits, int64_t M, int6
   return check_launch("reduce_splits_epilogue_kernel");
 }
 
+mdnn_status_t reduce_splits_epilogue(const void* ws, int splits, int64_t M, int64_t N, const Epilogue& ep,
+                                     mdnn_dtype_t mask_t, mdnn_dtype_t out_t, hipStream_t st) {
+  if (mask_t == MDNN_F32) return reduce_epilogue<F32, F32>(ws, splits, M, N, ep, st);
+  if (mask_t == MDNN_F16)
+    return out_t == MDNN_F32 ? reduce_epilogue<F16, F32>(ws, splits, M, N, ep, st)
+                             : reduce_epilogue<F16, F16>(ws, splits, M, N, ep, st);
+  return out_t == MDNN_F32 ? reduce_epilogue<BF16, F32>(ws, splits, M, N, ep, st)
+                           : reduce_epilogue<BF16, BF16>(ws, splits, M, N, ep, st);
+}
+
 // Low-precision problems whose grid of `tile` x `tile` tiles covers fewer
 // than half of the CUs, over K >= 256: split K (whole 64-deep steps, at
 // least two per split) so that about 256 workgroups run.
@@ -410,7 +421,10 @@ size_t mdnn::gemm_ws_bytes(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K
     const int s128 = lp_split_plan(M, N, K, 128).splits, s64 = lp_split_plan(M, N, K, 64).splits;
     splits = s128 > s64 ? s128 : s64;
   }
-  return splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+  const size_t tiles = splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+  // the skinny TN kernel's split (the layout is not an argument: room for it)
+  const size_t sk = skinny_ws_bytes(MDNN_TN, M, N, K);
+  return tiles > sk ? tiles : sk;
 }
 
 extern "C" mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
@@ -487,6 +501,8 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
   hipStream_t st = as_stream(stream);
   clear_error();
 
+  if (skinny_takes(layout, M, N, K, ws, ws_bytes))
+    return gemm_skinny(layout, M, N, K, A, lda, B, ldb, ab_type, d_type, ep, ws, ws_bytes, st);
   if (ab_type == MDNN_F32) return gemm_dispatch32(layout, M, N, K, A, lda, B, ldb, ep, ws, ws_bytes, st);
   const bool va = aligned(A, 16) && lda % 8 == 0;
   const bool vb = aligned(B, 16) && ldb % 8 == 0;

@@ -126,7 +126,7 @@ def test_short_workspace_is_the_plain_gemm(mdnn, dt):
     b = W.normal((k, n), 35, 2, dt)
     A, B = dev(a, dt), dev(b, dt)
     plain = _run(mdnn, "NN", A, B, "f32", m, n, k, None)
-    ws, nb = _ws(mdnn, dt, m, n, k, short=4)
+    ws, nb = _ws(mdnn, dt, m, n, k, short=(1 << 40))   # 16 bytes: below any plan
     assert ws.numel() < nb
     assert np.array_equal(_run(mdnn, "NN", A, B, "f32", m, n, k, ws), plain)
     # a shape that plans no split (K < 256 for fp16 / bf16, 64 tiles for
