@@ -206,6 +206,28 @@ mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void*
                                      mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
                                      size_t ws_bytes, mdnn_stream_t stream);
 
+/* Alternative forward algorithm for 3x3 filters (section 2.1: the
+ * convolution algorithm is swappable per layer): Winograd minimal filtering
+ * F(2x2, 3x3) (Lavin and Gray).  Same operands, output, bias and activation
+ * as mdnn_conv2d_fwd (any padding; r = s = 3), computed as
+ *   U = G g G^T per (c_out, c_in), V = B^T d B per 2x2 output tile and c_in
+ *   (d: the tile's 4x4 input window), M = 16 products V U^T on the matrix
+ *   cores (fp32 accumulation), y = A^T M A + bias, ReLU.
+ * U and V are rounded once to io_type, so the result carries one more
+ * storage rounding per operand than the implicit GEMM: its error is bounded
+ * by about 2u * |A^T| (sum_c |U||V|) |A| (u: io_type's unit roundoff), not by
+ * the implicit GEMM's 1e-4.  io_type: fp16 or bf16 (MDNN_ERR_DTYPE for fp32);
+ * MDNN_ERR_SHAPE unless r = s = 3.  workspace: at least
+ * mdnn_conv2d_fwd_winograd_workspace(shape, io_type) bytes (16 * (c_out*c_in
+ * + tiles*c_in) io_type elements + 16 * tiles*c_out floats, tiles =
+ * n * ceil(Ho/2) * ceil(Wo/2)), 256-byte aligned, overwritten (0 for an
+ * invalid shape or type).  Deterministic. */
+size_t mdnn_conv2d_fwd_winograd_workspace(const mdnn_conv_shape_t* shape, mdnn_dtype_t io_type);
+mdnn_status_t mdnn_conv2d_fwd_winograd(const mdnn_conv_shape_t* shape, const void* x, const void* w,
+                                       mdnn_dtype_t io_type, const float* bias, mdnn_act_t act, void* y,
+                                       mdnn_dtype_t y_type, void* workspace, size_t ws_bytes,
+                                       mdnn_stream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Bias + activation epilogue as stand-alone kernels (section 2.1: a layer's
  * activation and its derivative in backpropagation).

@@ -64,14 +64,30 @@ def input_tiles(x: np.ndarray, pad: int) -> np.ndarray:
     return d
 
 
+def _sandwich(left: np.ndarray, t: np.ndarray, right: np.ndarray) -> np.ndarray:
+    """left @ t @ right^T over the two tile axes (3 and 4) of t [..., P, Q, C]."""
+    s = np.tensordot(left, t, axes=([1], [3]))          # [a, N, TH, TW, Q, C]
+    s = np.tensordot(right, s, axes=([1], [4]))         # [b, a, N, TH, TW, C]
+    return np.moveaxis(np.moveaxis(s, 0, 4), 0, 3)      # [N, TH, TW, a, b, C]
+
+
 def input_transform(d: np.ndarray) -> np.ndarray:
     """d [N, TH, TW, 4, 4, C] -> V = B^T d B, same shape."""
-    return np.einsum("ai,ntuijc,bj->ntuabc", BT, d, BT)
+    return _sandwich(BT, d, BT)
 
 
 def output_transform(m: np.ndarray) -> np.ndarray:
     """m [N, TH, TW, 4, 4, K] -> Y = A^T m A, [N, TH, TW, 2, 2, K]."""
-    return np.einsum("ia,ntuabk,jb->ntuijk", AT, m, AT)
+    return _sandwich(AT, m, AT)
+
+
+def products(v: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """M[..., a, b, k] = sum_c V[..., a, b, c] U[a, b, k, c]: the 16 matrix products."""
+    m = np.empty(v.shape[:5] + (u.shape[2],))
+    for a in range(4):
+        for b in range(4):
+            m[..., a, b, :] = v[..., a, b, :] @ u[a, b].T
+    return m
 
 
 def untile(yt: np.ndarray, ho: int, wo: int) -> np.ndarray:
@@ -87,8 +103,7 @@ def conv2d_fwd_winograd(x: np.ndarray, w: np.ndarray, pad: int) -> np.ndarray:
     ho, wo, _, _ = tiles_hw(h, wd, pad)
     u = filter_transform(w)
     v = input_transform(input_tiles(x, pad))
-    m = np.einsum("ntuabc,abkc->ntuabk", v, u)
-    return untile(output_transform(m), ho, wo)
+    return untile(output_transform(products(v, u)), ho, wo)
 
 
 def error_scale(x: np.ndarray, w: np.ndarray, pad: int) -> np.ndarray:
@@ -99,5 +114,4 @@ def error_scale(x: np.ndarray, w: np.ndarray, pad: int) -> np.ndarray:
     ho, wo, _, _ = tiles_hw(h, wd, pad)
     u = np.abs(filter_transform(w))
     v = np.abs(input_transform(input_tiles(x, pad)))
-    m = np.einsum("ntuabc,abkc->ntuabk", v, u)
-    return untile(np.einsum("ia,ntuabk,jb->ntuijk", np.abs(AT), m, np.abs(AT)), ho, wo)
+    return untile(_sandwich(np.abs(AT), products(v, u), np.abs(AT)), ho, wo)

@@ -75,6 +75,7 @@ _SIGS = {
     "mdnn_conv2d_fwd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp],
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
+    "mdnn_conv2d_fwd_winograd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp, C.c_size_t, _vp],
     "mdnn_bias_act_fwd": [_i64, _i64, _vp, _vp, _i, _vp, _i, _vp],
     "mdnn_bias_act_bwd": [_i64, _i64, _vp, _vp, _i, _vp, _vp, _i, _vp, C.c_size_t, _vp],
     "mdnn_maxpool2_fwd": [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _i, _vp],
@@ -102,6 +103,8 @@ for _name, _args in _SIGS.items():
     _fn.restype = C.c_int
 _lib.mdnn_conv2d_bwd_filter_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_bwd_filter_workspace.restype = C.c_size_t
+_lib.mdnn_conv2d_fwd_winograd_workspace.argtypes = [_vp, _i]
+_lib.mdnn_conv2d_fwd_winograd_workspace.restype = C.c_size_t
 _lib.mdnn_gemm_workspace.argtypes = [_i, _i64, _i64, _i64]
 _lib.mdnn_gemm_workspace.restype = C.c_size_t
 _lib.mdnn_gemm_split3_workspace.argtypes = [_i64, _i64, _i64]
@@ -165,6 +168,7 @@ def last_error() -> str:
 def exported_symbols():
     return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
                                  "mdnn_gemm_split3_workspace", "mdnn_gemm_workspace",
+                                 "mdnn_conv2d_fwd_winograd_workspace",
                                  "mdnn_last_error",
                                  "mdnn_version", "mdnn_net_activation", "mdnn_net_destroy",
                                  "mdnn_graph_destroy", "mdnn_set_gemm_tile"])
@@ -204,6 +208,16 @@ def mdnn_gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, Cm
 
 def mdnn_gemm_workspace(ab_type, M, N, K) -> int:
     return _lib.mdnn_gemm_workspace(ab_type, M, N, K)
+
+
+def mdnn_conv2d_fwd_winograd(shape: ConvShape, x, w, io_type, bias, act, y, y_type, workspace, ws_bytes,
+                             stream=None):
+    return _call("mdnn_conv2d_fwd_winograd", _p(shape), _p(x), _p(w), io_type, _p(bias), act, _p(y), y_type,
+                 _p(workspace), ws_bytes, _s(stream))
+
+
+def mdnn_conv2d_fwd_winograd_workspace(shape: ConvShape, io_type) -> int:
+    return _lib.mdnn_conv2d_fwd_winograd_workspace(_p(shape), io_type)
 
 
 def mdnn_conv2d_bwd_filter_workspace(shape: ConvShape, io_type) -> int:

@@ -9,7 +9,7 @@
 
 namespace mdnn {
 
-static mdnn_status_t check_shape(const mdnn_conv_shape_t* s, ConvGeom& g) {
+mdnn_status_t check_conv_shape(const mdnn_conv_shape_t* s, ConvGeom& g) {
   if (!s) return fail(MDNN_ERR_NULL, "conv: shape is NULL");
   if (s->n < 0 || s->h < 1 || s->w < 1 || s->c_in < 1 || s->c_out < 1 || s->r < 1 || s->s < 1 ||
       s->pad < 0)
@@ -115,7 +115,7 @@ extern "C" mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const v
                                          mdnn_act_t act, void* y, mdnn_dtype_t y_type,
                                          mdnn_stream_t stream) {
   ConvGeom g;
-  MDNN_TRY(check_shape(shape, g));
+  MDNN_TRY(check_conv_shape(shape, g));
   if (!dtype_ok(io_type) || !dtype_ok(y_type) || (y_type != MDNN_F32 && y_type != io_type))
     return fail(MDNN_ERR_DTYPE, "conv fwd: y_type must be fp32 or io_type");
   if (act != MDNN_ACT_NONE && act != MDNN_ACT_RELU) return fail(MDNN_ERR_DTYPE, "conv fwd: unknown act");
@@ -147,7 +147,7 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
                                               const void* mask_src, void* dx,
                                               mdnn_dtype_t dx_type, mdnn_stream_t stream) {
   ConvGeom g;
-  MDNN_TRY(check_shape(shape, g));
+  MDNN_TRY(check_conv_shape(shape, g));
   if (!dtype_ok(io_type) || !dtype_ok(dx_type) || (dx_type != MDNN_F32 && dx_type != io_type))
     return fail(MDNN_ERR_DTYPE, "conv bwd_data: dx_type must be fp32 or io_type");
   if (g.n == 0) return MDNN_SUCCESS;
@@ -191,7 +191,7 @@ static size_t filter_ws_split_bytes(const ConvGeom& g) {
 extern "C" size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shape,
                                                    mdnn_dtype_t io_type) {
   ConvGeom g;
-  if (check_shape(shape, g) != MDNN_SUCCESS || !dtype_ok(io_type)) return 0;
+  if (check_conv_shape(shape, g) != MDNN_SUCCESS || !dtype_ok(io_type)) return 0;
   return filter_ws_split_bytes(g) + column_sums_ws_bytes((int64_t)g.n * g.ho * g.wo, g.k);
 }
 
@@ -200,7 +200,7 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
                                                 float* db, void* workspace, size_t ws_bytes,
                                                 mdnn_stream_t stream) {
   ConvGeom g;
-  MDNN_TRY(check_shape(shape, g));
+  MDNN_TRY(check_conv_shape(shape, g));
   if (!dtype_ok(io_type)) return fail(MDNN_ERR_DTYPE, "conv bwd_filter: unknown io_type");
   if (!dw) return fail(MDNN_ERR_NULL, "conv bwd_filter: dw is required");
   if (g.n > 0 && (!x || !dy)) return fail(MDNN_ERR_NULL, "conv bwd_filter: x and dy are required");

@@ -6,6 +6,9 @@
 
 namespace mdnn {
 
+// Validates a convolution shape (sizes, output not empty, ranges) into g.
+mdnn_status_t check_conv_shape(const mdnn_conv_shape_t* s, ConvGeom& g);
+
 // Forward with K = r*s*c_in <= 64 and c_out <= 256: any storage type, any
 // epilogue (bias, ReLU, output type).
 bool conv_small_fwd_ok(const ConvGeom& g);

@@ -17,14 +17,9 @@ namespace {
 
 constexpr int TP = 64;  // output pixels per staging round
 
-template <class T>
-__device__ __forceinline__ float ld_elem(const typename T::storage* p, int64_t i) {
-  return to_f<T>(p[i]);
-}
-
-// im2col element (pixel m of the output grid, column kk = (r*s_ + s)*c + ch)
-template <class T>
-__device__ __forceinline__ float patch(const typename T::storage* x, const ConvGeom& g, int64_t m, int kk) {
+// Offset in x of the im2col element (pixel m of the output grid, column
+// kk = (r*s_ + s)*c + ch), or -1 in the zero padding.
+__device__ __forceinline__ int64_t patch_off(const ConvGeom& g, int64_t m, int kk) {
   const int64_t hw = (int64_t)g.ho * g.wo;
   const int64_t n = m / hw;
   const int rem = (int)(m - n * hw);
@@ -32,8 +27,33 @@ __device__ __forceinline__ float patch(const typename T::storage* x, const ConvG
   const int tap = kk / g.c, ch = kk - tap * g.c;
   const int r = tap / g.s, s = tap - r * g.s;
   const int y = i + r - g.pad, xx = j + s - g.pad;
-  if (y < 0 || y >= g.h || xx < 0 || xx >= g.w) return 0.0f;
-  return ld_elem<T>(x, ((n * g.h + y) * g.w + xx) * g.c + ch);
+  if (y < 0 || y >= g.h || xx < 0 || xx >= g.w) return -1;
+  return ((n * g.h + y) * g.w + xx) * g.c + ch;
+}
+
+// Stage `count` table entries into LDS: entry e comes from src[off(e)] (0
+// where off(e) < 0) and goes to lds[dst(e)].  Each thread issues eight loads
+// before it stores any (the address is clamped to src[0] instead of
+// branching around the load), so a round of staging costs one memory latency
+// rather than one per element.
+template <class T, class Off, class Dst>
+__device__ __forceinline__ void stage(const typename T::storage* __restrict__ src, int count, Off off, Dst dst,
+                                      float* lds) {
+  for (int base = 0; base < count; base += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = base + u * 256 + (int)threadIdx.x;
+      const int64_t o = e < count ? off(e) : -1;
+      const float x = to_f<T>(src[o >= 0 ? o : 0]);
+      v[u] = o >= 0 ? x : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = base + u * 256 + (int)threadIdx.x;
+      if (e < count) lds[dst(e)] = v[u];
+    }
+  }
 }
 
 // Row stride of an LDS table with `cols` columns: odd, so that a column walk
@@ -49,15 +69,11 @@ conv_small_fwd_kernel(const typename T::storage* __restrict__ x, const typename 
   float* xs = smem;            // [TP][KS] im2col rows
   float* ws = smem + TP * KS;  // [N][KS] filter
   const int tid = threadIdx.x;
-  for (int e = tid; e < N * K; e += 256) {
-    const int n = e / K;
-    ws[n * KS + (e - n * K)] = ld_elem<T>(w, e);
-  }
+  stage<T>(w, N * K, [](int e) -> int64_t { return e; }, [=](int e) { return (e / K) * KS + e % K; }, ws);
   const int64_t m0 = (int64_t)blockIdx.x * TP;
-  for (int e = tid; e < TP * K; e += 256) {
-    const int p = e / K, kk = e - p * K;
-    xs[p * KS + kk] = m0 + p < M ? patch<T>(x, g, m0 + p, kk) : 0.0f;
-  }
+  stage<T>(
+      x, TP * K, [=](int e) -> int64_t { const int p = e / K; return m0 + p < M ? patch_off(g, m0 + p, e - p * K) : -1; },
+      [=](int e) { return (e / K) * KS + e % K; }, xs);
   __syncthreads();
   const int groups = (N + 3) / 4;
   for (int q = tid; q < TP * groups; q += 256) {
@@ -88,14 +104,13 @@ conv_small_filter_kernel(const typename T::storage* __restrict__ x, const typena
   const int64_t p_end = p_beg + pixels_per_block < P ? p_beg + pixels_per_block : P;
   for (int64_t p0 = p_beg; p0 < p_end; p0 += TP) {
     __syncthreads();
-    for (int e = tid; e < TP * K; e += 256) {
-      const int p = e / K, kk = e - p * K;
-      xs[p * KS + kk] = p0 + p < p_end ? patch<T>(x, g, p0 + p, kk) : 0.0f;
-    }
-    for (int e = tid; e < TP * N; e += 256) {
-      const int p = e / N, k = e - p * N;
-      ds[p * NS + k] = p0 + p < p_end ? ld_elem<T>(dy, (p0 + p) * N + k) : 0.0f;
-    }
+    stage<T>(
+        x, TP * K,
+        [=](int e) -> int64_t { const int p = e / K; return p0 + p < p_end ? patch_off(g, p0 + p, e - p * K) : -1; },
+        [=](int e) { return (e / K) * KS + e % K; }, xs);
+    stage<T>(
+        dy, TP * N, [=](int e) -> int64_t { return p0 + e / N < p_end ? p0 * N + e : -1; },
+        [=](int e) { return (e / N) * NS + e % N; }, ds);
     __syncthreads();
 #pragma unroll
     for (int o = 0; o < 4; ++o) {

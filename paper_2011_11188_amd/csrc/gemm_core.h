@@ -46,7 +46,8 @@ __device__ __forceinline__ uint4 pack8(const uint16_t v[8]) {
 }
 
 // Every source gives elem(mn, k) (bounds-checked, zero outside; mn is the
-// operand's M index for A and N index for B) for any storage type S, and, for
+// operand's M index for A and N index for B) for any storage type S, the
+// same as an offset from base() (off(mn, k), -1 outside or in padding), and, for
 // 16-bit storage, chunk(...) = 8 consecutive elements along the contiguous
 // dimension packed into 16 bytes: chunk(mn, k) for K-contiguous sources,
 // chunk(k, mn) for MN-contiguous ones.
@@ -58,9 +59,12 @@ struct SrcMatK {
   const S* p;
   int64_t ld, MN, K;
   bool vec;
+  int64_t bs = 0;  // elements between consecutive matrices of a batch (grid z)
   __device__ __forceinline__ S elem(int64_t mn, int64_t k) const {
     return (mn < MN && k < K) ? p[mn * ld + k] : (S)0;
   }
+  __device__ __forceinline__ const S* base() const { return p; }
+  __device__ __forceinline__ int64_t off(int64_t mn, int64_t k) const { return (mn < MN && k < K) ? mn * ld + k : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t mn, int64_t k) const {
     if (mn < MN && vec && k + 8 <= K) return *(const uint4*)(p + mn * ld + k);
     uint16_t v[8];
@@ -77,9 +81,12 @@ struct SrcMatMN {
   const S* p;
   int64_t ld, MN, K;
   bool vec;
+  int64_t bs = 0;  // elements between consecutive matrices of a batch (grid z)
   __device__ __forceinline__ S elem(int64_t mn, int64_t k) const {
     return (k < K && mn < MN) ? p[k * ld + mn] : (S)0;
   }
+  __device__ __forceinline__ const S* base() const { return p; }
+  __device__ __forceinline__ int64_t off(int64_t mn, int64_t k) const { return (k < K && mn < MN) ? k * ld + mn : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t k, int64_t mn) const {
     if (k < K && vec && mn + 8 <= MN) return *(const uint4*)(p + k * ld + mn);
     uint16_t v[8];
@@ -121,6 +128,10 @@ struct SrcConvFwdA {
     int64_t o = offset(m, kk);
     return o < 0 ? (S)0 : x[o];
   }
+  __device__ __forceinline__ const S* base() const { return x; }
+  __device__ __forceinline__ int64_t off(int64_t m, int64_t kk) const {
+    return (m < MN && kk < K) ? offset(m, kk) : -1;
+  }
   __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
     if (vec && m < MN && kk + 8 <= K) {
       int64_t o = offset(m, kk);
@@ -159,6 +170,10 @@ struct SrcConvBwdA {
     int64_t o = offset(m, kk);
     return o < 0 ? (S)0 : dy[o];
   }
+  __device__ __forceinline__ const S* base() const { return dy; }
+  __device__ __forceinline__ int64_t off(int64_t m, int64_t kk) const {
+    return (m < MN && kk < K) ? offset(m, kk) : -1;
+  }
   __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
     if (vec && m < MN && kk + 8 <= K) {
       int64_t o = offset(m, kk);
@@ -188,6 +203,8 @@ struct SrcConvBwdB {
   __device__ __forceinline__ S elem(int64_t c, int64_t kk) const {
     return (kk < K && c < MN) ? wt[row(kk) + c] : (S)0;
   }
+  __device__ __forceinline__ const S* base() const { return wt; }
+  __device__ __forceinline__ int64_t off(int64_t c, int64_t kk) const { return (kk < K && c < MN) ? row(kk) + c : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t c) const {
     if (kk >= K) return make_uint4(0, 0, 0, 0);
     const S* p = wt + row(kk);
@@ -225,6 +242,10 @@ struct SrcConvFiltB {
     int64_t o = offset(kk, nn);
     return o < 0 ? (S)0 : x[o];
   }
+  __device__ __forceinline__ const S* base() const { return x; }
+  __device__ __forceinline__ int64_t off(int64_t nn, int64_t kk) const {
+    return (kk < K && nn < MN) ? offset(kk, nn) : -1;
+  }
   __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t nn) const {
     if (vec && kk < K && nn + 8 <= MN) {
       int64_t o = offset(kk, nn);
@@ -255,7 +276,17 @@ struct Epilogue {
   int32_t vec4_m;      // 4-wide loads of the mask allowed (ldm % 4 == 0, mask aligned to 4 elements)
   float* partial;      // split-K: fp32 [splits][M][N]; null otherwise
   int64_t k_per_split; // multiple of GEMM_BK
+  int64_t bstride_d;   // batched products (grid z): elements of D between batch entries
 };
+
+// Batched products: grid z selects one matrix of a batch of plain matrices
+// (SrcMatK / SrcMatMN with bs != 0); other sources are never batched.
+template <class S>
+__device__ __forceinline__ void shift_batch(SrcMatK<S>& s, int z) { s.p += (int64_t)z * s.bs; }
+template <class S>
+__device__ __forceinline__ void shift_batch(SrcMatMN<S>& s, int z) { s.p += (int64_t)z * s.bs; }
+template <class Src>
+__device__ __forceinline__ void shift_batch(Src&, int) {}
 
 // Four consecutive stored elements as floats, in one vector load (p aligned
 // to four elements).
@@ -466,6 +497,11 @@ gemm_mfma_kernel(SrcA srcA, SrcB srcB, int64_t M, int64_t N, int64_t K, Epilogue
   int tm, tn;
   tile_coords(ceil_div(M, BM), ceil_div(N, BN), tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  if (blockIdx.z) {
+    shift_batch(srcA, (int)blockIdx.z);
+    shift_batch(srcB, (int)blockIdx.z);
+    ep.D = (typename OutT::storage*)ep.D + (int64_t)blockIdx.z * ep.bstride_d;
+  }
 
   int64_t kbeg = 0, kend = K;
   if (ep.partial) {

@@ -14,6 +14,17 @@ namespace mdnn {
 // among themselves and combine their sums through LDS in group order (fixed,
 // so deterministic): a grid of only a few tiles over a long K then keeps KG
 // times as many waves busy.
+// src.elem(mn, k) when ok, else 0, as an unconditional load from a clamped
+// address (base()[0] is an element of the operand) and a select: guarded loads
+// in divergent branches are each waited for before the branch joins, so a
+// branch-free fetch keeps all of a thread's loads in flight together.
+template <class Src>
+__device__ __forceinline__ float fetch_sel(const Src& src, int64_t mn, int64_t k, bool ok) {
+  const int64_t o = ok ? src.off(mn, k) : -1;
+  const float v = (float)src.base()[o >= 0 ? o : 0];
+  return o >= 0 ? v : 0.0f;
+}
+
 template <class SrcA, class SrcB, int KG>
 __global__ void __launch_bounds__(256 * KG)
 gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
@@ -51,8 +62,8 @@ gemm_f32_kernel(SrcA a, SrcB b, int64_t M, int64_t N, int64_t K, Epilogue ep) {
   auto fetch = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      ra[q] = (k0 + sk[0][q] < gend) ? (float)a.elem(m0 + sr[0][q], k0 + sk[0][q]) : 0.0f;
-      rb[q] = (k0 + sk[1][q] < gend) ? (float)b.elem(n0 + sr[1][q], k0 + sk[1][q]) : 0.0f;
+      ra[q] = fetch_sel(a, m0 + sr[0][q], k0 + sk[0][q], k0 + sk[0][q] < gend);
+      rb[q] = fetch_sel(b, n0 + sr[1][q], k0 + sk[1][q], k0 + sk[1][q] < gend);
     }
   };
   float acc[4][4] = {};

@@ -89,6 +89,26 @@ def test_conv_rejects_bad_arguments(m):
     assert m.mdnn_conv2d_bwd_filter_workspace(bad, 1) == 0
 
 
+def test_winograd_rejects_bad_arguments(m):
+    sh = m.ConvShape(2, 6, 6, 8, 8, 3, 3, 1)
+    need = m.mdnn_conv2d_fwd_winograd_workspace(sh, m.F16)
+    # U: 16*8*8 halves, V: 16*(2*3*3 tiles)*8 halves, M: 16*18*8 floats, 256-byte segments
+    assert need == 2048 + 4608 + 9216
+    assert m.mdnn_conv2d_fwd_winograd_workspace(sh, m.F32) == 0
+    five = m.ConvShape(2, 6, 6, 8, 8, 5, 5, 2)
+    assert m.mdnn_conv2d_fwd_winograd_workspace(five, m.F16) == 0
+    cases = [((five, FAKE, FAKE, m.F16, None, 0, FAKE, m.F32, FAKE, need), m.ERR_SHAPE),
+             ((sh, FAKE, FAKE, m.F32, None, 0, FAKE, m.F32, FAKE, need), m.ERR_DTYPE),
+             ((sh, FAKE, FAKE, m.F16, None, 0, FAKE, m.BF16, FAKE, need), m.ERR_DTYPE),
+             ((sh, None, FAKE, m.F16, None, 0, FAKE, m.F32, FAKE, need), m.ERR_NULL),
+             ((sh, FAKE, FAKE, m.F16, None, 0, FAKE, m.F32, FAKE, need - 1), m.ERR_WORKSPACE),
+             ((sh, FAKE, FAKE, m.F16, None, 0, FAKE, m.F32, FAKE + 16, need), m.ERR_WORKSPACE)]
+    for args, status in cases:
+        with pytest.raises(m.MdnnError) as e:
+            m.mdnn_conv2d_fwd_winograd(*args, stream=0)
+        assert e.value.status == status, args
+
+
 def test_other_entry_points_reject_bad_arguments(m):
     with pytest.raises(m.MdnnError) as e:
         m.mdnn_cast(-1, FAKE, 0, FAKE, 1, stream=0)
