@@ -452,19 +452,93 @@ __global__ void scaler_finalize_kernel(mdnn_scaler_t* sc) {
   sc->reserved = 0;
 }
 
+// Four consecutive parameters per thread with 16-byte loads and stores (w,
+// g, v 16-byte aligned; the working copy 4-element aligned); the same
+// arithmetic per element as sgd_kernel.  The n % 4 tail is done by thread 0.
+template <class LpT, bool MOM, bool SCALE>
+__global__ void sgd_vec_kernel(int64_t n, float* __restrict__ w, const float* __restrict__ g,
+                               float* __restrict__ v, typename LpT::storage* __restrict__ wlp, float lr,
+                               float mu, const mdnn_scaler_t* __restrict__ sc) {
+  float S = 1.0f;
+  if (SCALE) {
+    if (sc->reserved) return;  // overflow: skip the whole update
+    S = sc->scale;
+  }
+  const int64_t n4 = n / 4;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n4; q += stride) {
+    float4 gi = ((const float4*)g)[q];
+    float4 wi = ((float4*)w)[q];
+    float ga[4] = {gi.x, gi.y, gi.z, gi.w}, wa[4] = {wi.x, wi.y, wi.z, wi.w};
+    if (SCALE) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ga[e] = ga[e] / S;
+    }
+    if (MOM) {
+      const float4 vi = ((const float4*)v)[q];
+      float va[4] = {vi.x, vi.y, vi.z, vi.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        va[e] = fmaf(mu, va[e], ga[e]);
+        wa[e] = fmaf(-lr, va[e], wa[e]);
+      }
+      ((float4*)v)[q] = make_float4(va[0], va[1], va[2], va[3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wa[e] = fmaf(-lr, ga[e], wa[e]);
+    }
+    ((float4*)w)[q] = make_float4(wa[0], wa[1], wa[2], wa[3]);
+    if (wlp) {
+      if constexpr (sizeof(typename LpT::storage) == 4) {
+        ((float4*)wlp)[q] = make_float4(wa[0], wa[1], wa[2], wa[3]);
+      } else {
+        uint2 u;
+        u.x = (uint32_t)from_f<LpT>(wa[0]) | ((uint32_t)from_f<LpT>(wa[1]) << 16);
+        u.y = (uint32_t)from_f<LpT>(wa[2]) | ((uint32_t)from_f<LpT>(wa[3]) << 16);
+        ((uint2*)wlp)[q] = u;
+      }
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    for (int64_t i = n4 * 4; i < n; ++i) {
+      float gi = g[i];
+      if (SCALE) gi = gi / S;
+      float wi = w[i];
+      if (MOM) {
+        const float vi = fmaf(mu, v[i], gi);
+        v[i] = vi;
+        wi = fmaf(-lr, vi, wi);
+      } else {
+        wi = fmaf(-lr, gi, wi);
+      }
+      w[i] = wi;
+      if (wlp) wlp[i] = from_f<LpT>(wi);
+    }
+  }
+}
+
+template <class LpT, bool MOM, bool SCALE>
+static void sgd_launch_t(int64_t n, float* w, const float* g, float* v, void* wlp, float lr, float mu,
+                         const mdnn_scaler_t* sc, hipStream_t st) {
+  typedef typename LpT::storage L;
+  // w and g are 16-byte aligned (checked by the entry point)
+  const bool vec = (!v || aligned(v, 16)) && (!wlp || aligned(wlp, 4 * sizeof(L)));
+  unsigned grid = grid_for(vec ? ceil_div(n, 4) : n, 256);
+  if (grid > 8192) grid = 8192;
+  if (vec)
+    hipLaunchKernelGGL((sgd_vec_kernel<LpT, MOM, SCALE>), dim3(grid), dim3(256), 0, st, n, w, g, v, (L*)wlp, lr, mu,
+                       sc);
+  else
+    hipLaunchKernelGGL((sgd_kernel<LpT, MOM, SCALE>), dim3(grid), dim3(256), 0, st, n, w, g, v, (L*)wlp, lr, mu, sc);
+}
+
 template <class LpT>
 static void sgd_launch(int64_t n, float* w, const float* g, float* v, void* wlp, float lr, float mu,
                        const mdnn_scaler_t* sc, hipStream_t st) {
-  unsigned grid = grid_for(n, 256);
-  if (grid > 8192) grid = 8192;
-  typedef typename LpT::storage L;
-#define MDNN_SGD(M_, S_) \
-  hipLaunchKernelGGL((sgd_kernel<LpT, M_, S_>), dim3(grid), dim3(256), 0, st, n, w, g, v, (L*)wlp, lr, mu, sc)
-  if (v && sc) MDNN_SGD(true, true);
-  else if (v) MDNN_SGD(true, false);
-  else if (sc) MDNN_SGD(false, true);
-  else MDNN_SGD(false, false);
-#undef MDNN_SGD
+  if (v && sc) sgd_launch_t<LpT, true, true>(n, w, g, v, wlp, lr, mu, sc, st);
+  else if (v) sgd_launch_t<LpT, true, false>(n, w, g, v, wlp, lr, mu, sc, st);
+  else if (sc) sgd_launch_t<LpT, false, true>(n, w, g, v, wlp, lr, mu, sc, st);
+  else sgd_launch_t<LpT, false, false>(n, w, g, v, wlp, lr, mu, sc, st);
 }
 
 }  // namespace mdnn

@@ -222,6 +222,29 @@ def test_sgd_update_against_oracle(mdnn, dt, momentum):
     assert s["scale"] == 1024.0 and s["good_steps"] == 1 and s["overflow"] == 0 and s["reserved"] == 0
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_sgd_vector_and_element_paths_agree(mdnn, dt):
+    """16-byte aligned buffers take four parameters per thread (and the n % 4
+    tail), an unaligned momentum buffer the element-wise kernel: same bits."""
+    import torch
+    n = 4099
+    w = W.normal((n,), 28, 1, "f32")
+    g = W.normal((n,), 28, 2, "f32")
+    v = W.normal((n,), 28, 3, "f32")
+    outs = []
+    for off in (0, 1):
+        wt, gt = dev(w, "f32"), dev(g, "f32")
+        vbuf = torch.zeros(n + 1, dtype=torch.float32, device="cuda")
+        vt = vbuf[off:off + n]
+        vt.copy_(dev(v, "f32"))
+        wlp = empty((n,), dt)
+        mdnn.mdnn_sgd_update(n, wt, gt, vt, wlp, DT[dt], 0.05, 0.9, mdnn.make_scaler(8.0))
+        torch.cuda.synchronize()
+        outs.append((wt.clone(), vt.clone(), wlp.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_sgd_overflow_skips_and_halves(mdnn):
     import torch
     n = 4099
