@@ -60,46 +60,59 @@ __device__ __forceinline__ void stage(const typename T::storage* __restrict__ sr
 // by consecutive lanes spreads over the banks.
 __host__ __device__ constexpr int odd_stride(int cols) { return cols | 1; }
 
+// Output channels padded to a multiple of four, so that four consecutive
+// channels are one 16-byte LDS read.
+__host__ __device__ constexpr int quad_pad(int n) { return (n + 3) & ~3; }
+
 template <class T, class OutT>
 __global__ void __launch_bounds__(256)
 conv_small_fwd_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ w,
                       ConvGeom g, int64_t M, Epilogue ep) {
   extern __shared__ float smem[];
-  const int K = g.r * g.s * g.c, N = g.k, KS = odd_stride(K);
+  const int K = g.r * g.s * g.c, N = g.k, KS = odd_stride(K), NP = quad_pad(N);
   float* xs = smem;            // [TP][KS] im2col rows
-  float* ws = smem + TP * KS;  // [N][KS] filter
+  float* wt = smem + TP * KS;  // [K][NP] filter, transposed (zero beyond N)
   const int tid = threadIdx.x;
-  stage<T>(w, N * K, [](int e) -> int64_t { return e; }, [=](int e) { return (e / K) * KS + e % K; }, ws);
+  stage<T>(w, K * NP, [=](int e) -> int64_t { const int kk = e / NP, n = e - kk * NP; return n < N ? (int64_t)n * K + kk : -1; },
+           [](int e) { return e; }, wt);
   const int64_t m0 = (int64_t)blockIdx.x * TP;
   stage<T>(
       x, TP * K, [=](int e) -> int64_t { const int p = e / K; return m0 + p < M ? patch_off(g, m0 + p, e - p * K) : -1; },
       [=](int e) { return (e / K) * KS + e % K; }, xs);
   __syncthreads();
-  const int groups = (N + 3) / 4;
+  // thread task: pixel p, output channels n4 .. n4+3 (one 16-byte read of the
+  // filter and one broadcast read of the patch per four FMAs)
+  const int groups = NP / 4;
   for (int q = tid; q < TP * groups; q += 256) {
     const int p = q / groups, n4 = (q - p * groups) * 4;
     float4_t acc = {0.f, 0.f, 0.f, 0.f};
+    const float* xr = xs + p * KS;
     for (int kk = 0; kk < K; ++kk) {
-      const float a = xs[p * KS + kk];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (n4 + e < N) acc[e] = fmaf(a, ws[(n4 + e) * KS + kk], acc[e]);
+      const float a = xr[kk];
+      const float4 b = *(const float4*)(wt + kk * NP + n4);
+      acc[0] = fmaf(a, b.x, acc[0]);
+      acc[1] = fmaf(a, b.y, acc[1]);
+      acc[2] = fmaf(a, b.z, acc[2]);
+      acc[3] = fmaf(a, b.w, acc[3]);
     }
     epilogue_store4<T, OutT>(ep, M, N, m0 + p, n4, acc);
   }
 }
 
-// partial[b][k][kk] over the pixels of block b (pixels_per_block of them)
+// partial[b][k][kk] over the pixels of block b (pixels_per_block of them).
+// Thread task: output channels k4 .. k4+3 of filter column kk; per pixel one
+// 16-byte read of the output gradient row and one read of the patch.
 template <class T>
 __global__ void __launch_bounds__(256)
 conv_small_filter_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ dy,
                          ConvGeom g, int64_t P, int64_t pixels_per_block, float* __restrict__ partial) {
   extern __shared__ float smem[];
-  const int K = g.r * g.s * g.c, N = g.k, MN = N * K, KS = odd_stride(K), NS = odd_stride(N);
+  const int K = g.r * g.s * g.c, N = g.k, MN = N * K, KS = odd_stride(K), NP = quad_pad(N);
   float* xs = smem;            // [TP][KS] im2col rows
-  float* ds = smem + TP * KS;  // [TP][NS] output gradient rows
+  float* ds = smem + TP * KS;  // [TP][NP] output gradient rows (zero beyond N)
   const int tid = threadIdx.x;
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  const int G4 = NP / 4, tasks = G4 * K;  // <= 256 + K: at most two per thread
+  float4_t acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
   const int64_t p_beg = (int64_t)blockIdx.x * pixels_per_block;
   const int64_t p_end = p_beg + pixels_per_block < P ? p_beg + pixels_per_block : P;
   for (int64_t p0 = p_beg; p0 < p_end; p0 += TP) {
@@ -109,35 +122,49 @@ conv_small_filter_kernel(const typename T::storage* __restrict__ x, const typena
         [=](int e) -> int64_t { const int p = e / K; return p0 + p < p_end ? patch_off(g, p0 + p, e - p * K) : -1; },
         [=](int e) { return (e / K) * KS + e % K; }, xs);
     stage<T>(
-        dy, TP * N, [=](int e) -> int64_t { return p0 + e / N < p_end ? p0 * N + e : -1; },
-        [=](int e) { return (e / N) * NS + e % N; }, ds);
+        dy, TP * NP,
+        [=](int e) -> int64_t { const int p = e / NP, k = e - p * NP; return (p0 + p < p_end && k < N) ? (p0 + p) * N + k : -1; },
+        [](int e) { return e; }, ds);
     __syncthreads();
 #pragma unroll
-    for (int o = 0; o < 4; ++o) {
-      const int idx = tid + o * 256;
-      if (idx < MN) {
-        const int k = idx / K, kk = idx - k * K;
-        float s = acc[o];
-        for (int p = 0; p < TP; ++p) s = fmaf(ds[p * NS + k], xs[p * KS + kk], s);
+    for (int o = 0; o < 2; ++o) {
+      const int t = tid + o * 256;
+      if (t < tasks) {
+        const int kk = t / G4, k4 = (t - kk * G4) * 4;
+        float4_t s = acc[o];
+        for (int p = 0; p < TP; ++p) {
+          const float a = xs[p * KS + kk];
+          const float4 d = *(const float4*)(ds + p * NP + k4);
+          s[0] = fmaf(d.x, a, s[0]);
+          s[1] = fmaf(d.y, a, s[1]);
+          s[2] = fmaf(d.z, a, s[2]);
+          s[3] = fmaf(d.w, a, s[3]);
+        }
         acc[o] = s;
       }
     }
   }
 #pragma unroll
-  for (int o = 0; o < 4; ++o) {
-    const int idx = tid + o * 256;
-    if (idx < MN) partial[(int64_t)blockIdx.x * MN + idx] = acc[o];
+  for (int o = 0; o < 2; ++o) {
+    const int t = tid + o * 256;
+    if (t < tasks) {
+      const int kk = t / G4, k4 = (t - kk * G4) * 4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (k4 + e < N) partial[(int64_t)blockIdx.x * MN + (int64_t)(k4 + e) * K + kk] = acc[o][e];
+    }
   }
 }
 
-constexpr int64_t FILTER_PIXELS = 512;  // pixels per block of the filter gradient
+constexpr int64_t FILTER_PIXELS = 128;  // pixels per block of the filter gradient (enough blocks to hide the staging latency)
 constexpr size_t LDS_LIMIT = 65536;      // dynamic LDS bytes per block
 
 size_t fwd_lds(const ConvGeom& g) {
-  return (size_t)(TP + g.k) * odd_stride(g.r * g.s * g.c) * sizeof(float);
+  const int K = g.r * g.s * g.c;
+  return ((size_t)TP * odd_stride(K) + (size_t)K * quad_pad(g.k)) * sizeof(float);
 }
 size_t filter_lds(const ConvGeom& g) {
-  return (size_t)TP * (odd_stride(g.r * g.s * g.c) + odd_stride(g.k)) * sizeof(float);
+  return (size_t)TP * (odd_stride(g.r * g.s * g.c) + quad_pad(g.k)) * sizeof(float);
 }
 
 }  // namespace
