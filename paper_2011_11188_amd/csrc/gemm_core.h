@@ -45,6 +45,23 @@ __device__ __forceinline__ uint4 pack8(const uint16_t v[8]) {
   return r;
 }
 
+// Sixteen bytes of zeros in device memory: an out-of-range chunk is loaded
+// from here instead of being skipped or selected away, so every chunk load of
+// a tile is one unconditional instruction and they all stay in flight (a
+// load under a divergent branch, or one whose register another branch writes,
+// is waited for before the code can go on).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __attribute__((aligned(16))) const u32x4_t kZeroChunk = {0u, 0u, 0u, 0u};
+
+__device__ __forceinline__ uint4 load_chunk_or_zero(const void* p, bool ok) {
+  // loaded through a global-address-space pointer: a generic (flat) load
+  // would also count against the LDS wait counter and stall the next LDS
+  // read until it lands
+  typedef const __attribute__((address_space(1))) u32x4_t GlobalChunk;
+  const u32x4_t v = *(GlobalChunk*)(ok ? p : (const void*)&kZeroChunk);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Every source gives elem(mn, k) (bounds-checked, zero outside; mn is the
 // operand's M index for A and N index for B) for any storage type S, the
 // same as an offset from base() (off(mn, k), -1 outside or in padding), and, for
@@ -66,7 +83,10 @@ struct SrcMatK {
   __device__ __forceinline__ const S* base() const { return p; }
   __device__ __forceinline__ int64_t off(int64_t mn, int64_t k) const { return (mn < MN && k < K) ? mn * ld + k : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t mn, int64_t k) const {
-    if (mn < MN && vec && k + 8 <= K) return *(const uint4*)(p + mn * ld + k);
+    if (vec && (k + 8 <= K || k >= K)) {
+      const bool ok = mn < MN && k + 8 <= K;
+      return load_chunk_or_zero(p + (ok ? mn * ld + k : 0), ok);
+    }
     uint16_t v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = elem(mn, k + e);
@@ -88,7 +108,10 @@ struct SrcMatMN {
   __device__ __forceinline__ const S* base() const { return p; }
   __device__ __forceinline__ int64_t off(int64_t mn, int64_t k) const { return (k < K && mn < MN) ? k * ld + mn : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t k, int64_t mn) const {
-    if (k < K && vec && mn + 8 <= MN) return *(const uint4*)(p + k * ld + mn);
+    if (vec && (mn + 8 <= MN || mn >= MN)) {
+      const bool ok = k < K && mn + 8 <= MN;
+      return load_chunk_or_zero(p + (ok ? k * ld + mn : 0), ok);
+    }
     uint16_t v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = elem(mn + e, k);
@@ -133,9 +156,9 @@ struct SrcConvFwdA {
     return (m < MN && kk < K) ? offset(m, kk) : -1;
   }
   __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
-    if (vec && m < MN && kk + 8 <= K) {
-      int64_t o = offset(m, kk);
-      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(x + o);
+    if (vec && (kk + 8 <= K || kk >= K)) {
+      const int64_t o = (m < MN && kk + 8 <= K) ? offset(m, kk) : -1;
+      return load_chunk_or_zero(x + (o < 0 ? 0 : o), o >= 0);
     }
     uint16_t v[8];
 #pragma unroll
@@ -175,9 +198,9 @@ struct SrcConvBwdA {
     return (m < MN && kk < K) ? offset(m, kk) : -1;
   }
   __device__ __forceinline__ uint4 chunk(int64_t m, int64_t kk) const {
-    if (vec && m < MN && kk + 8 <= K) {
-      int64_t o = offset(m, kk);
-      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(dy + o);
+    if (vec && (kk + 8 <= K || kk >= K)) {
+      const int64_t o = (m < MN && kk + 8 <= K) ? offset(m, kk) : -1;
+      return load_chunk_or_zero(dy + (o < 0 ? 0 : o), o >= 0);
     }
     uint16_t v[8];
 #pragma unroll
@@ -206,9 +229,12 @@ struct SrcConvBwdB {
   __device__ __forceinline__ const S* base() const { return wt; }
   __device__ __forceinline__ int64_t off(int64_t c, int64_t kk) const { return (kk < K && c < MN) ? row(kk) + c : -1; }
   __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t c) const {
+    if (vec && (c + 8 <= MN || c >= MN)) {
+      const bool ok = kk < K && c + 8 <= MN;
+      return load_chunk_or_zero(wt + (ok ? row(kk) + c : 0), ok);
+    }
     if (kk >= K) return make_uint4(0, 0, 0, 0);
     const S* p = wt + row(kk);
-    if (vec && c + 8 <= MN) return *(const uint4*)(p + c);
     uint16_t v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = (c + e < MN) ? p[c + e] : (S)0;
@@ -247,9 +273,9 @@ struct SrcConvFiltB {
     return (kk < K && nn < MN) ? offset(kk, nn) : -1;
   }
   __device__ __forceinline__ uint4 chunk(int64_t kk, int64_t nn) const {
-    if (vec && kk < K && nn + 8 <= MN) {
-      int64_t o = offset(kk, nn);
-      return o < 0 ? make_uint4(0, 0, 0, 0) : *(const uint4*)(x + o);
+    if (vec && (nn + 8 <= MN || nn >= MN)) {
+      const int64_t o = (kk < K && nn + 8 <= MN) ? offset(kk, nn) : -1;
+      return load_chunk_or_zero(x + (o < 0 ? 0 : o), o >= 0);
     }
     uint16_t v[8];
 #pragma unroll
