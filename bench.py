@@ -475,7 +475,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only (no collectives); use --gpus 1",
+        print("bench.py: the step runs on one GPU (no collectives are implemented); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
