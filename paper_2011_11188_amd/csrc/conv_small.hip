@@ -19,16 +19,17 @@ constexpr int TP = 64;  // output pixels per staging round
 
 // Offset in x of the im2col element (pixel m of the output grid, column
 // kk = (r*s_ + s)*c + ch), or -1 in the zero padding.
-__device__ __forceinline__ int64_t patch_off(const ConvGeom& g, int64_t m, int kk) {
-  const int64_t hw = (int64_t)g.ho * g.wo;
-  const int64_t n = m / hw;
-  const int rem = (int)(m - n * hw);
+__device__ __forceinline__ int64_t patch_off(const ConvGeom& g, int64_t m64, int kk) {
+  const int m = (int)m64;  // the direct kernels run only while n*ho*wo < 2^31: 32-bit divisions
+  const int hw = g.ho * g.wo;
+  const int n = m / hw;
+  const int rem = m - n * hw;
   const int i = rem / g.wo, j = rem - i * g.wo;
   const int tap = kk / g.c, ch = kk - tap * g.c;
   const int r = tap / g.s, s = tap - r * g.s;
   const int y = i + r - g.pad, xx = j + s - g.pad;
   if (y < 0 || y >= g.h || xx < 0 || xx >= g.w) return -1;
-  return ((n * g.h + y) * g.w + xx) * g.c + ch;
+  return (((int64_t)n * g.h + y) * g.w + xx) * g.c + ch;
 }
 
 // Stage `count` table entries into LDS: entry e comes from src[off(e)] (0
@@ -169,8 +170,10 @@ size_t filter_lds(const ConvGeom& g) {
 
 }  // namespace
 
+static bool pixels_fit(const ConvGeom& g) { return (int64_t)g.n * g.ho * g.wo < ((int64_t)1 << 31); }
+
 bool conv_small_fwd_ok(const ConvGeom& g) {
-  return g.r * g.s * g.c <= 64 && g.k <= 256 && fwd_lds(g) <= LDS_LIMIT;
+  return g.r * g.s * g.c <= 64 && g.k <= 256 && fwd_lds(g) <= LDS_LIMIT && pixels_fit(g);
 }
 
 mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
@@ -195,7 +198,7 @@ mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, co
 
 int64_t conv_small_filter_blocks(const ConvGeom& g) {
   const int K = g.r * g.s * g.c;
-  if (K > 64 || g.k > 256 || (int64_t)g.k * K > 1024 || filter_lds(g) > LDS_LIMIT) return 0;
+  if (K > 64 || g.k > 256 || (int64_t)g.k * K > 1024 || filter_lds(g) > LDS_LIMIT || !pixels_fit(g)) return 0;
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
   return ceil_div(P, FILTER_PIXELS);
 }
