@@ -229,12 +229,21 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
     """The GEMM engine's automatic kernel choice for the step's plain,
     aligned operands (mirrors the library's fixed table)."""
     cd = lambda a, b: -(-a // b)  # noqa: E731
+    if k <= 4:
+        return "skinny depth kernel"
+    if n <= 4 and layout != "TN":
+        return "skinny rows kernel"
+    if n <= 16 and layout == "TN":
+        return "skinny cols kernel"
     mn_contig = {"NN": [n], "NT": [], "TN": [m, n]}[layout]
-    if k % 64 == 0 and all(d % 8 == 0 for d in mn_contig):
-        if cd(m, 256) * cd(n, 256) >= 256:
+    if k % 64 == 0 and all(d % 8 == 0 for d in mn_contig) and cd(m, 128) * cd(n, 128) >= 32:
+        if n <= 64 and m > 64:
+            return "gemm_lds_kernel (256x64 direct-to-LDS pipeline)"
+        if m <= 64 and n > 64:
+            return "gemm_lds_kernel (64x256 direct-to-LDS pipeline)"
+        if n > 128 and m > 128 and cd(m, 256) * cd(n, 256) >= 256:
             return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
-        if cd(m, 128) * cd(n, 128) >= 32:
-            return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
+        return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
     if cd(m, 256) * cd(n, 256) >= 256:
         return "gemm_mfma_kernel 256x256"
     if cd(m, 128) * cd(n, 128) >= 160:

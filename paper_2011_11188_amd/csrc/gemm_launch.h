@@ -204,11 +204,21 @@ inline void launch_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M,
                      grid, dim3(TL::NT), 0, stream, oa, ob, M, N, K, ep);
 }
 
+// Narrow products: a 256 x 64 (64 x 256) tile when N (M) is at most 64, so
+// that a square tile's columns (rows) are not mostly padding.
+typedef lds::Tile<256, 64, 4, 2, 4> TileNarrowN;
+typedef lds::Tile<64, 256, 2, 4, 2> TileNarrowM;
+
 template <class T, class OutT, bool A_KC, bool B_KC>
 inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
                                   int64_t K, const Epilogue& ep, int splits, hipStream_t stream) {
   const int o = gemm_tile_override();
-  if (o == TILE_LDS_PIPE || (o != TILE_LDS_PIPE128 && ceil_div(M, 256) * ceil_div(N, 256) * splits >= 256))
+  if (o == TILE_AUTO && N <= 64 && M > 64)
+    launch_gemm_lds<T, OutT, TileNarrowN, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
+  else if (o == TILE_AUTO && M <= 64 && N > 64)
+    launch_gemm_lds<T, OutT, TileNarrowM, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
+  else if (o == TILE_LDS_PIPE ||
+           (o != TILE_LDS_PIPE128 && N > 128 && M > 128 && ceil_div(M, 256) * ceil_div(N, 256) * splits >= 256))
     launch_gemm_lds<T, OutT, lds::Tile256, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
   else
     launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);

@@ -243,3 +243,24 @@ def test_gemm_sweep_full_size_sampled(mdnn, size, layout):
     assert norm_max_err(got[rows], want_rows) <= TOL
     assert norm_max_err(got[:, cols], want_cols) <= TOL
     assert np.all(np.isfinite(got))
+
+
+# Narrow shapes on the pipelined kernel (automatic choice): N <= 64 takes the
+# 256 x 64 tile, M <= 64 the 64 x 256 tile, N <= 128 the 128 x 128 tile
+# (a 256 x 256 tile would be mostly padding); ragged M / N included.
+NARROW = [(8192, 64, 576), (4000, 48, 256), (64, 8192, 512), (40, 4096, 256), (16384, 128, 320)]
+
+
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_gemm_narrow_shapes_pipelined(mdnn, layout):
+    for i, (m, n, k) in enumerate(NARROW):
+        sa, sb = _shapes(layout, m, n, k)
+        a = W.normal(sa, 36, 10 * i + 1, "f16", 1 / np.sqrt(k))
+        b = W.normal(sb, 36, 10 * i + 2, "f16")
+        got = _run(mdnn, layout, dev(a, "f16"), dev(b, "f16"), "f32", m, n, k)
+        want = ops.gemm(layout, decode(a, "f16"), decode(b, "f16"))
+        assert norm_max_err(got, want) <= TOL, (layout, m, n, k)
+        ai = W.small_ints(sa, 37, 10 * i + 1, dtype="bf16")
+        bi = W.small_ints(sb, 37, 10 * i + 2, dtype="bf16")
+        got = _run(mdnn, layout, dev(ai, "bf16"), dev(bi, "bf16"), "f32", m, n, k)
+        assert np.array_equal(got, ops.gemm(layout, decode(ai, "bf16"), decode(bi, "bf16"))), (layout, m, n, k)
