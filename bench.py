@@ -244,7 +244,9 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
         if n > 128 and m > 128 and cd(m, 256) * cd(n, 256) >= 256:
             return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
         return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
-    if cd(m, 256) * cd(n, 256) >= 256:
+    if m <= 64 or n <= 64:
+        return "gemm_mfma_kernel 64x64"
+    if cd(m, 256) * cd(n, 256) >= 256 and m > 128 and n > 128:
         return "gemm_mfma_kernel 256x256"
     if cd(m, 128) * cd(n, 128) >= 160:
         return "gemm_mfma_kernel 128x128"

@@ -140,8 +140,9 @@ inline TileCfg choose_tile(int64_t M, int64_t N, int splits) {
   int o = gemm_tile_override();
   if (o >= TILE_256x256 && o <= TILE_64x64) return (TileCfg)o;
   if (o >= TILE_LDS_PIPE) return TILE_256x256;  // this path has no pipelined kernel
+  if (M <= 64 || N <= 64) return TILE_64x64;  // a wider tile would be mostly padding
   const int64_t t256 = ceil_div(M, 256) * ceil_div(N, 256) * splits;
-  if (t256 >= 256) return TILE_256x256;
+  if (t256 >= 256 && M > 128 && N > 128) return TILE_256x256;
   const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128) * splits;
   if (t128 >= 160) return TILE_128x128;
   return TILE_64x64;
