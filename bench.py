@@ -555,7 +555,7 @@ def main():
         "data": "synthetic (seeded N(0,1) inputs and targets, He-normal weights)",
         "config": {"workload": f"{cfg.name}: wide regression MLP 1024->4x4096(ReLU)->1, MSE, "
                                "fp16 storage, fp32 accumulate + master weights, dynamic loss "
-                               "scaling (2^16), SGD momentum 0.9, lr 1e-3",
+                               f"scaling (2^16), SGD momentum {cfg.momentum}, lr {cfg.lr:g}",
                    "global_batch": cfg.batch, "parallelism": "single GPU",
                    "step_tflops": round(step_tf, 1),
                    "graph_ms_per_step": round(graph_ms, 4),

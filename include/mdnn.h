@@ -112,7 +112,12 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
  * misaligned workspace, or a shape that does not need splitting, gives
  * exactly mdnn_gemm_mixed.  mdnn_gemm_workspace returns 0 when no split is
  * planned (and for negative sizes).  The workspace is scratch, overwritten;
- * calls that share one must be ordered on one stream. */
+ * calls that share one must be ordered on one stream.
+ * nonfinite (nullable, device int32, d_type MDNN_F32 only, else
+ * MDNN_ERR_DTYPE): the dynamic loss scaler's overflow test done where the
+ * gradients are produced -- every kernel path sets *nonfinite = 1 (atomic
+ * OR) if any value it stores into D is Inf or NaN, and never clears it; for
+ * mdnn_sgd_update's scaler this is scaler->reserved. */
 size_t mdnn_gemm_workspace(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K);
 mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
                                  float alpha, const void* A, int64_t lda, const void* B,
@@ -120,7 +125,7 @@ mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int
                                  int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
                                  const float* bias, mdnn_act_t act, const void* mask_src,
                                  int64_t ldm, void* workspace, size_t ws_bytes,
-                                 mdnn_stream_t stream);
+                                 int32_t* nonfinite, mdnn_stream_t stream);
 
 /* Tuning knob for measurements (process-wide): force the MFMA kernel of the
  * GEMM engine.  0 = automatic (default), 1 = 256x256, 2 = 128x128, 3 = 64x64

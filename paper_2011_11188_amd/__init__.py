@@ -71,7 +71,7 @@ _SIGS = {
     "mdnn_gemm_mixed": [_i, _i64, _i64, _i64, _f, _vp, _i64, _vp, _i64, _i, _f, _vp, _i64, _vp,
                         _i64, _i, _vp, _i, _vp, _i64, _vp],
     "mdnn_gemm_mixed_ws": [_i, _i64, _i64, _i64, _f, _vp, _i64, _vp, _i64, _i, _f, _vp, _i64, _vp,
-                           _i64, _i, _vp, _i, _vp, _i64, _vp, C.c_size_t, _vp],
+                           _i64, _i, _vp, _i, _vp, _i64, _vp, C.c_size_t, _vp, _vp],
     "mdnn_conv2d_fwd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp],
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
@@ -200,10 +200,10 @@ def mdnn_conv2d_bwd_data(shape: ConvShape, dy, w, io_type, mask_src, dx, dx_type
 
 def mdnn_gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, Cm, ldc, D, ldd,
                        d_type, bias=None, act=ACT_NONE, mask_src=None, ldm=0, workspace=None, ws_bytes=0,
-                       stream=None):
+                       stream=None, nonfinite=None):
     return _call("mdnn_gemm_mixed_ws", layout, M, N, K, alpha, _p(A), lda, _p(B), ldb, ab_type, beta,
                  _p(Cm), ldc, _p(D), ldd, d_type, _p(bias), act, _p(mask_src), ldm, _p(workspace), ws_bytes,
-                 _s(stream))
+                 _p(nonfinite), _s(stream))
 
 
 def mdnn_gemm_workspace(ab_type, M, N, K) -> int:

@@ -27,10 +27,13 @@ def torch_dtype(code: int):
 
 
 def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask=None,
-         alpha: float = 1.0, beta: float = 0.0, Cm=None, out=None, stream=None, workspace=None):
+         alpha: float = 1.0, beta: float = 0.0, Cm=None, out=None, stream=None, workspace=None,
+         nonfinite=None):
     """D = epi(alpha op(A) op(B) + beta C) for row-major 2-D tensors A, B.
     workspace: None (mdnn_gemm_mixed), True (allocate what
-    mdnn_gemm_workspace asks for) or a device byte tensor (mdnn_gemm_mixed_ws)."""
+    mdnn_gemm_workspace asks for) or a device byte tensor (mdnn_gemm_mixed_ws).
+    nonfinite: a device int32 tensor set to 1 when a stored value of the fp32
+    D is Inf or NaN (mdnn_gemm_mixed_ws; implies a workspace, empty if None)."""
     import torch
     if layout == TN:
         K, M = A.shape
@@ -42,13 +45,14 @@ def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask
     args = (layout, M, N, K, alpha, A, A.stride(0), B, B.stride(0), dtype_of(A), beta, Cm,
             Cm.stride(0) if Cm is not None else 0, out, out.stride(0), dtype_of(out), bias,
             act, mask, mask.stride(0) if mask is not None else 0)
-    if workspace is None:
+    if workspace is None and nonfinite is None:
         mdnn_gemm_mixed(*args, stream)
         return out
     if workspace is True:
         nb = mdnn_gemm_workspace(dtype_of(A), M, N, K)
         workspace = torch.empty((max(nb, 16),), dtype=torch.uint8, device=A.device)
-    mdnn_gemm_mixed_ws(*args, workspace, workspace.numel(), stream)
+    mdnn_gemm_mixed_ws(*args, workspace, workspace.numel() if workspace is not None else 0, stream,
+                       nonfinite=nonfinite)
     return out
 
 

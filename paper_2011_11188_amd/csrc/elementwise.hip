@@ -383,6 +383,18 @@ __global__ void finite_check_kernel(const float* __restrict__ g, int64_t n,
   if (bad && threadIdx.x == 0) atomicOr(&sc->reserved, 1);
 }
 
+// finite_check_kernel over a few ranges of g: block row y covers range y
+__global__ void finite_check_ranges_kernel(const float* __restrict__ g, CheckRanges r,
+                                           mdnn_scaler_t* __restrict__ sc) {
+  const float* p = g + r.off[blockIdx.y];
+  const int64_t n = r.len[blockIdx.y];
+  int bad = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) bad |= !isfinite(p[i]);
+  bad = __syncthreads_or(bad);
+  if (bad && threadIdx.x == 0) atomicOr(&sc->reserved, 1);
+}
+
 template <class LpT, bool MOM, bool SCALE>
 __global__ void sgd_kernel(int64_t n, float* __restrict__ w, const float* __restrict__ g,
                            float* __restrict__ v, typename LpT::storage* __restrict__ wlp, float lr,
@@ -779,10 +791,39 @@ extern "C" mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const floa
   return MDNN_SUCCESS;
 }
 
+static mdnn_status_t sgd_update_impl(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
+                                     mdnn_dtype_t lp_type, float lr, float momentum, mdnn_scaler_t* scaler,
+                                     mdnn_stream_t stream, bool check);
+
 extern "C" mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v32,
                                          void* w_lp, mdnn_dtype_t lp_type, float lr,
                                          float momentum, mdnn_scaler_t* scaler,
                                          mdnn_stream_t stream) {
+  return sgd_update_impl(n, w32, g32, v32, w_lp, lp_type, lr, momentum, scaler, stream, true);
+}
+
+mdnn_status_t mdnn::sgd_update_prechecked(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
+                                          mdnn_dtype_t lp_type, float lr, float momentum, mdnn_scaler_t* scaler,
+                                          mdnn_stream_t stream) {
+  return sgd_update_impl(n, w32, g32, v32, w_lp, lp_type, lr, momentum, scaler, stream, false);
+}
+
+mdnn_status_t mdnn::finite_check_ranges(const float* g, const CheckRanges& r, mdnn_scaler_t* scaler,
+                                        hipStream_t st) {
+  if (r.n <= 0) return MDNN_SUCCESS;
+  if (r.n > kMaxCheckRanges) return fail(MDNN_ERR_SHAPE, "finite check: too many ranges");
+  int64_t longest = 0;
+  for (int i = 0; i < r.n; ++i) longest = r.len[i] > longest ? r.len[i] : longest;
+  if (longest == 0) return MDNN_SUCCESS;
+  unsigned gx = grid_for(longest, 256);
+  if (gx > 256) gx = 256;
+  hipLaunchKernelGGL(finite_check_ranges_kernel, dim3(gx, (unsigned)r.n), dim3(256), 0, st, g, r, scaler);
+  return check_launch("finite_check_ranges_kernel");
+}
+
+static mdnn_status_t sgd_update_impl(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
+                                     mdnn_dtype_t lp_type, float lr, float momentum, mdnn_scaler_t* scaler,
+                                     mdnn_stream_t stream, bool check) {
   if (n < 0) return fail(MDNN_ERR_SHAPE, "sgd_update: n < 0");
   if (!dtype_ok(lp_type)) return fail(MDNN_ERR_DTYPE, "sgd_update: unknown lp_type");
   if (n > 0 && (!w32 || !g32)) return fail(MDNN_ERR_NULL, "sgd_update: w32 and g32 are required");
@@ -791,7 +832,7 @@ extern "C" mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32
     return fail(MDNN_ERR_MISALIGNED, "sgd_update: w32/g32 need 16-byte alignment");
   clear_error();
   hipStream_t st = as_stream(stream);
-  if (scaler && n > 0) {
+  if (check && scaler && n > 0) {
     unsigned g = grid_for(ceil_div(n, 4), 256);
     if (g > 2048) g = 2048;
     hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);

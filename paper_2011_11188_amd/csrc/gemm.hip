@@ -117,20 +117,32 @@ colsum_partial_kernel(const typename T::storage* __restrict__ x, const typename 
   const int64_t r0 = (int64_t)blockIdx.y * COLSUM_ROWS;
   const int64_t r1 = r0 + COLSUM_ROWS < rows ? r0 + COLSUM_ROWS : rows;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  if (vec && sizeof(typename T::storage) == 2 && c0 + 8 <= cols) {
-    for (int64_t r = r0 + rl; r < r1; r += 32) {
-      const uint4 v = *(const uint4*)(x + r * cols + c0);
-      uint4 m = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
-      if (y) m = *(const uint4*)(y + r * cols + c0);
-      const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
-      const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
+  // adds one row's 8 values (16 bytes of x, and of the mask y) to s
+  auto add8 = [&](const uint4& v, const uint4& m) {
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+    const uint32_t mw[4] = {m.x, m.y, m.z, m.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint16_t xv = (uint16_t)(vw[e >> 1] >> ((e & 1) * 16));
-        const uint16_t yv = (uint16_t)(mw[e >> 1] >> ((e & 1) * 16));
-        if (y == nullptr || to_f<T>((typename T::storage)yv) > 0.0f) s[e] += to_f<T>((typename T::storage)xv);
-      }
+    for (int e = 0; e < 8; ++e) {
+      const uint16_t xv = (uint16_t)(vw[e >> 1] >> ((e & 1) * 16));
+      const uint16_t yv = (uint16_t)(mw[e >> 1] >> ((e & 1) * 16));
+      if (y == nullptr || to_f<T>((typename T::storage)yv) > 0.0f) s[e] += to_f<T>((typename T::storage)xv);
     }
+  };
+  const uint4 ones = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
+  if (vec && sizeof(typename T::storage) == 2 && c0 + 8 <= cols && r1 - r0 == COLSUM_ROWS) {
+    // a whole chunk: all of this thread's rows are loaded before any is added
+    // (same order of additions as the row loop below)
+    constexpr int RPT = COLSUM_ROWS / 32;
+    uint4 v[RPT], m[RPT];
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) v[u] = *(const uint4*)(x + (r0 + rl + 32 * u) * cols + c0);
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) m[u] = y ? *(const uint4*)(y + (r0 + rl + 32 * u) * cols + c0) : ones;
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) add8(v[u], m[u]);
+  } else if (vec && sizeof(typename T::storage) == 2 && c0 + 8 <= cols) {
+    for (int64_t r = r0 + rl; r < r1; r += 32)
+      add8(*(const uint4*)(x + r * cols + c0), y ? *(const uint4*)(y + r * cols + c0) : ones);
   } else {
     for (int64_t r = r0 + rl; r < r1; r += 32)
 #pragma unroll
@@ -446,16 +458,18 @@ extern "C" mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int
                                             mdnn_dtype_t ab_type, float beta, const void* C, int64_t ldc, void* D,
                                             int64_t ldd, mdnn_dtype_t d_type, const float* bias, mdnn_act_t act,
                                             const void* mask_src, int64_t ldm, void* workspace, size_t ws_bytes,
-                                            mdnn_stream_t stream) {
+                                            int32_t* nonfinite, mdnn_stream_t stream) {
+  if (nonfinite && !aligned(nonfinite, 4)) return fail(MDNN_ERR_MISALIGNED, "gemm: nonfinite is misaligned");
   return gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, C, ldc, D, ldd, d_type, bias, act,
-                       mask_src, ldm, workspace, ws_bytes, stream);
+                       mask_src, ldm, workspace, ws_bytes, stream, nonfinite);
 }
 
 mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, float alpha,
                                   const void* A, int64_t lda, const void* B, int64_t ldb, mdnn_dtype_t ab_type,
                                   float beta, const void* C, int64_t ldc, void* D, int64_t ldd,
                                   mdnn_dtype_t d_type, const float* bias, mdnn_act_t act, const void* mask_src,
-                                  int64_t ldm, void* ws, size_t ws_bytes, mdnn_stream_t stream) {
+                                  int64_t ldm, void* ws, size_t ws_bytes, mdnn_stream_t stream,
+                                  int32_t* nonfinite) {
   if (layout != MDNN_NN && layout != MDNN_NT && layout != MDNN_TN)
     return fail(MDNN_ERR_LAYOUT, "gemm: unknown layout %d", (int)layout);
   if (M < 0 || N < 0 || K < 0) return fail(MDNN_ERR_SHAPE, "gemm: negative size");
@@ -481,6 +495,7 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
     return fail(MDNN_ERR_MISALIGNED, "gemm: a base pointer is not aligned to its element size");
   if (ab_type == MDNN_F32 && d_type != MDNN_F32)
     return fail(MDNN_ERR_DTYPE, "gemm: fp32 operands need an fp32 output");
+  if (nonfinite && d_type != MDNN_F32) return fail(MDNN_ERR_DTYPE, "gemm: the finite check needs an fp32 output");
 
   Epilogue ep{};
   ep.alpha = alpha;
@@ -498,6 +513,7 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
   ep.vec4_m = mask_src && (ldm % 4 == 0) && aligned(mask_src, 4 * es);
   ep.partial = nullptr;
   ep.k_per_split = K;
+  ep.nonfinite = nonfinite;
   hipStream_t st = as_stream(stream);
   clear_error();
 

@@ -303,6 +303,7 @@ struct Epilogue {
   float* partial;      // split-K: fp32 [splits][M][N]; null otherwise
   int64_t k_per_split; // multiple of GEMM_BK
   int64_t bstride_d;   // batched products (grid z): elements of D between batch entries
+  int32_t* nonfinite;  // fp32 D only: set to 1 (atomic OR) when a stored value is not finite; or null
 };
 
 // Batched products: grid z selects one matrix of a batch of plain matrices
@@ -380,6 +381,15 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         if (n + e < N && !(to_f<MaskT>(mk[e]) > 0.0f)) v[e] = 0.0f;
+    }
+  }
+  if constexpr (sizeof(typename OutT::storage) == 4) {
+    // the loss scaler's overflow test, on the values as stored
+    if (ep.nonfinite) {
+      bool bad = false;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bad |= (n + e < N) && !isfinite(v[e]);
+      if (bad) atomicOr(ep.nonfinite, 1);
     }
   }
   typename OutT::storage* d = (typename OutT::storage*)ep.D + m * ep.ldd + n;

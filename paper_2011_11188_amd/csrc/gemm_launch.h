@@ -195,12 +195,12 @@ inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t 
   return true;
 }
 
-template <class T, class OutT, class TL, bool A_KC, bool B_KC>
+template <class T, class OutT, class TL, bool A_KC, bool B_KC, int NS = 2>
 inline void launch_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N, int64_t K,
                             const Epilogue& ep, int splits, hipStream_t stream) {
   dim3 grid((unsigned)(ceil_div(M, TL::BM) * ceil_div(N, TL::BN)), (unsigned)splits, 1);
   lds::MatArgs oa{a.p, a.ld, a.MN}, ob{b.p, b.ld, b.MN};
-  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, 2, lds::MatLoader<A_KC, TL::BM, TL::LA>,
+  hipLaunchKernelGGL((lds::gemm_lds_kernel<T, OutT, TL, NS, lds::MatLoader<A_KC, TL::BM, TL::LA>,
                                            lds::MatLoader<B_KC, TL::BN, TL::LB>>),
                      grid, dim3(TL::NT), 0, stream, oa, ob, M, N, K, ep);
 }
@@ -221,6 +221,10 @@ inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int6
   else if (o == TILE_LDS_PIPE ||
            (o != TILE_LDS_PIPE128 && N > 128 && M > 128 && ceil_div(M, 256) * ceil_div(N, 256) * splits >= 256))
     launch_gemm_lds<T, OutT, lds::Tile256, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
+  else if (ceil_div(M, 128) * ceil_div(N, 128) * splits <= 256)
+    // at most one workgroup per CU: the LDS a second one would use holds two
+    // more stages instead, so three tiles are in flight behind the MFMAs
+    launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC, 4>(a, b, M, N, K, ep, splits, stream);
   else
     launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
   return check_launch("gemm_lds_kernel");

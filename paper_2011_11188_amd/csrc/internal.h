@@ -60,6 +60,22 @@ mdnn_status_t gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t 
                             int64_t lda, const void* B, int64_t ldb, mdnn_dtype_t ab_type, float beta,
                             const void* C, int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
                             const float* bias, mdnn_act_t act, const void* mask_src, int64_t ldm, void* ws,
-                            size_t ws_bytes, mdnn_stream_t stream);
+                            size_t ws_bytes, mdnn_stream_t stream, int32_t* nonfinite = nullptr);
+
+// Loss-scaled updates whose gradients were checked where they were produced:
+// gemm_mixed_ws with `nonfinite` = &scaler->reserved covers every fp32 value
+// it stores (all of its kernel paths store through the same epilogue); the
+// ranges no such producer wrote are checked here, one block row per range.
+constexpr int kMaxCheckRanges = 32;
+struct CheckRanges {
+  int32_t n;
+  int64_t off[kMaxCheckRanges], len[kMaxCheckRanges];
+};
+mdnn_status_t finite_check_ranges(const float* g, const CheckRanges& r, mdnn_scaler_t* scaler, hipStream_t st);
+// mdnn_sgd_update without its finite check of g32 (the caller has set
+// scaler->reserved for every non-finite gradient already).
+mdnn_status_t sgd_update_prechecked(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
+                                    mdnn_dtype_t lp_type, float lr, float momentum, mdnn_scaler_t* scaler,
+                                    mdnn_stream_t stream);
 
 }  // namespace mdnn

@@ -47,6 +47,12 @@ struct mdnn_net {
   void* lowp = nullptr;
   char* ws = nullptr;
   mdnn_scaler_t* scaler = nullptr;
+  // loss-scaled steps: the FC weight gradients are checked for non-finite
+  // values by the GEMMs that write them; `unchecked` lists the other
+  // gradient ranges (FC biases, convolution layers) for a separate check.
+  // prechecked is false when they do not fit in one CheckRanges.
+  bool prechecked = false;
+  CheckRanges unchecked{};
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -129,6 +135,23 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
   }
   net->n_params = off;
   net->in_feat = net->layers[0].in_feat;
+  net->prechecked = true;
+  for (const auto& p : net->layers) {
+    int64_t o = 0, len = 0;
+    if (p.L.kind == MDNN_LAYER_FC) o = p.b_off, len = p.nb;
+    if (p.L.kind == MDNN_LAYER_CONV) o = p.w_off, len = p.nw + p.nb;
+    if (len == 0) continue;
+    CheckRanges& r = net->unchecked;
+    if (r.n > 0 && r.off[r.n - 1] + r.len[r.n - 1] == o) {
+      r.len[r.n - 1] += len;  // adjacent to the previous range
+    } else if (r.n < kMaxCheckRanges) {
+      r.off[r.n] = o;
+      r.len[r.n] = len;
+      ++r.n;
+    } else {
+      net->prechecked = false;
+    }
+  }
   const LayerPlan& last = net->layers.back();
   if (cfg->loss == MDNN_LOSS_XENT && (last.out_feat != cfg->n_classes || cfg->n_classes > 1024)) {
     delete net;
@@ -282,7 +305,8 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
                            stream));
   }
 
-  // backward
+  // backward (FC weight gradients checked for the loss scaler as they are stored)
+  int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
   for (size_t ii = net->layers.size(); ii-- > 0;) {
     const LayerPlan& p = net->layers[ii];
     const char* a_in = act_ptr(ii);
@@ -293,7 +317,8 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
       const int64_t in = p.L.c_in, o = p.L.c_out;
       // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
       MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
-                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream));
+                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
+                             nonfinite));
       MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp,
                                  ws + net->fws_off, net->fws_bytes, stream));
       if (ii > 0) {
@@ -320,6 +345,11 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
   if (async)
     return mdnn_sgd_update_async(net->n_params, net->master, net->grads, net->mom, net->cfg.lr,
                                  net->cfg.momentum, net->scaler, stream);
+  if (nonfinite) {
+    MDNN_TRY(finite_check_ranges(net->grads, net->unchecked, net->scaler, as_stream(stream)));
+    return sgd_update_prechecked(net->n_params, net->master, net->grads, net->mom, net->lowp, lp, net->cfg.lr,
+                                 net->cfg.momentum, net->scaler, stream);
+  }
   return mdnn_sgd_update(net->n_params, net->master, net->grads, net->mom, net->lowp, lp,
                          net->cfg.lr, net->cfg.momentum, net->scaler, stream);
 }

@@ -148,6 +148,11 @@ def test_gemm_workspace_plan(m):
         m.mdnn_gemm_mixed_ws(7, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0, None, 0, None, 0,
                              FAKE, 1024, stream=0)
     assert e.value.status == m.ERR_LAYOUT
+    # the overflow flag: a 4-byte aligned device int32 (checked before anything runs)
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_gemm_mixed_ws(0, 4, 4, 4, 1.0, FAKE, 4, FAKE, 4, 1, 0.0, None, 0, FAKE, 4, 0, None, 0, None, 0,
+                             None, 0, stream=0, nonfinite=FAKE + 2)
+    assert e.value.status == m.ERR_MISALIGNED
 
 
 def test_split_entry_points_reject_bad_arguments(m):
