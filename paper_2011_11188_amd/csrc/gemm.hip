@@ -179,6 +179,29 @@ colsum_final_kernel(const float* __restrict__ partial, int64_t chunks, int64_t c
   }
 }
 
+// colsum_final_kernel over a batch of matrices (block row y = entry y), with
+// the loss scaler's overflow flag on the stored sums.
+__global__ void __launch_bounds__(256)
+colsum_final_batch_kernel(ColsumBatch b, int32_t* __restrict__ nonfinite) {
+  __shared__ float red[8][33];
+  const int cx = threadIdx.x & 31, ln = threadIdx.x >> 5;
+  const int64_t cols = b.cols[blockIdx.y], chunks = b.chunks[blockIdx.y];
+  const float* __restrict__ partial = b.part[blockIdx.y];
+  const int64_t c = (int64_t)blockIdx.x * 32 + cx;
+  float s = 0.0f;
+  if (c < cols)
+    for (int64_t k = ln; k < chunks; k += 8) s += partial[k * cols + c];
+  red[ln][cx] = s;
+  __syncthreads();
+  if (ln == 0 && c < cols) {
+    float t = red[0][cx];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += red[k][cx];
+    b.out[blockIdx.y][c] = t;
+    if (nonfinite && !isfinite(t)) atomicOr(nonfinite, 1);
+  }
+}
+
 template <class T>
 __global__ void __launch_bounds__(256)
 colsum_single_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ y,
@@ -235,6 +258,43 @@ mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t 
     default: colsum_launch<BF16>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
   }
   return check_launch("column sums");
+}
+
+int64_t column_sums_chunks(int64_t rows) { return ceil_div(rows, COLSUM_ROWS); }
+
+mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* partial,
+                                  hipStream_t st) {
+  const int64_t chunks = column_sums_chunks(rows);
+  if (cols == 0 || chunks == 0) return MDNN_SUCCESS;
+  if (chunks > 65535 || ceil_div(cols, 64) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "column sums: too many rows");
+  const dim3 grid((unsigned)ceil_div(cols, 64), (unsigned)chunks);
+  const bool vec = aligned(x, 16) && cols % 8 == 0;
+  switch (t) {
+    case MDNN_F32:
+      hipLaunchKernelGGL(colsum_partial_kernel<F32>, grid, dim3(256), 0, st, (const float*)x, nullptr, rows, cols,
+                         vec, partial);
+      break;
+    case MDNN_F16:
+      hipLaunchKernelGGL(colsum_partial_kernel<F16>, grid, dim3(256), 0, st, (const uint16_t*)x, nullptr, rows,
+                         cols, vec, partial);
+      break;
+    default:
+      hipLaunchKernelGGL(colsum_partial_kernel<BF16>, grid, dim3(256), 0, st, (const uint16_t*)x, nullptr, rows,
+                         cols, vec, partial);
+  }
+  return check_launch("column sums (partials)");
+}
+
+mdnn_status_t column_sums_final(const ColsumBatch& b, int32_t* nonfinite, hipStream_t st) {
+  if (b.n <= 0) return MDNN_SUCCESS;
+  if (b.n > kMaxColsumBatch) return fail(MDNN_ERR_SHAPE, "column sums: batch too large");
+  int64_t widest = 0;
+  for (int i = 0; i < b.n; ++i) widest = b.cols[i] > widest ? b.cols[i] : widest;
+  if (widest == 0) return MDNN_SUCCESS;
+  if (ceil_div(widest, 32) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "column sums: too many columns");
+  hipLaunchKernelGGL(colsum_final_batch_kernel, dim3((unsigned)ceil_div(widest, 32), (unsigned)b.n), dim3(256), 0,
+                     st, b, nonfinite);
+  return check_launch("column sums (final)");
 }
 
 // ---------------------------------------------------------------------------

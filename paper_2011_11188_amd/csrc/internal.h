@@ -50,6 +50,22 @@ mdnn_status_t cast_any(int64_t n, const void* src, mdnn_dtype_t s, void* dst, md
 size_t column_sums_ws_bytes(int64_t rows, int64_t cols);
 mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
                           float* out, void* ws, size_t ws_bytes, hipStream_t stream);
+// The two passes apart, for a caller that finishes several matrices' sums in
+// one launch: pass 1 writes partial[column_sums_chunks(rows)][cols] (fp32,
+// 4-byte aligned); pass 2 sums each entry's partials in the same fixed order
+// as column_sums and, when nonfinite is given, ORs 1 into it for every
+// non-finite sum (the loss scaler's overflow test of the sums it stores).
+int64_t column_sums_chunks(int64_t rows);
+mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* partial,
+                                  hipStream_t stream);
+constexpr int kMaxColsumBatch = 32;
+struct ColsumBatch {
+  int32_t n;
+  const float* part[kMaxColsumBatch];
+  float* out[kMaxColsumBatch];
+  int64_t chunks[kMaxColsumBatch], cols[kMaxColsumBatch];
+};
+mdnn_status_t column_sums_final(const ColsumBatch& b, int32_t* nonfinite, hipStream_t stream);
 
 // mdnn_gemm_mixed with an optional workspace (NULL / too small: same as
 // mdnn_gemm_mixed).  With one, fp32 problems whose grid would be a handful of

@@ -27,6 +27,7 @@ struct LayerPlan {
   int64_t in_feat = 0, out_feat = 0;  // per sample
   size_t out_off = 0;                 // act[i+1]
   size_t arg_off = 0;                 // pool argmax
+  size_t cs_off = 0;                  // FC: bias-gradient partial column sums
   bool input_relu = false;            // input produced by a ReLU (directly or through pooling)
   bool last = false;
 };
@@ -48,8 +49,9 @@ struct mdnn_net {
   char* ws = nullptr;
   mdnn_scaler_t* scaler = nullptr;
   // loss-scaled steps: the FC weight gradients are checked for non-finite
-  // values by the GEMMs that write them; `unchecked` lists the other
-  // gradient ranges (FC biases, convolution layers) for a separate check.
+  // values by the GEMMs that write them and the FC bias gradients by the
+  // pass that finishes their column sums; `unchecked` lists the other
+  // gradient ranges (convolution layers) for a separate check.
   // prechecked is false when they do not fit in one CheckRanges.
   bool prechecked = false;
   CheckRanges unchecked{};
@@ -138,7 +140,6 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
   net->prechecked = true;
   for (const auto& p : net->layers) {
     int64_t o = 0, len = 0;
-    if (p.L.kind == MDNN_LAYER_FC) o = p.b_off, len = p.nb;
     if (p.L.kind == MDNN_LAYER_CONV) o = p.w_off, len = p.nw + p.nb;
     if (len == 0) continue;
     CheckRanges& r = net->unchecked;
@@ -178,6 +179,8 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
     }
     if (p.L.kind == MDNN_LAYER_FC) {
       const int64_t in = p.L.c_in, o = p.L.c_out;
+      p.cs_off = w;
+      w = align256(w + (size_t)column_sums_chunks(batch) * o * 4);
       const size_t needs[4] = {mdnn_bias_act_bwd_workspace(batch, o), gemm_ws_bytes(net->lp, batch, o, in),
                                gemm_ws_bytes(net->lp, in, o, batch), gemm_ws_bytes(net->lp, batch, in, o)};
       for (size_t need : needs)
@@ -307,6 +310,9 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
 
   // backward (FC weight gradients checked for the loss scaler as they are stored)
   int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
+  // loss-scaled FC bias gradients: partial column sums per layer now, all
+  // layers finished (and checked) in one launch after the loop
+  ColsumBatch bias_sums{};
   for (size_t ii = net->layers.size(); ii-- > 0;) {
     const LayerPlan& p = net->layers[ii];
     const char* a_in = act_ptr(ii);
@@ -319,8 +325,22 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
       MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
                              nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
                              nonfinite));
-      MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp,
-                                 ws + net->fws_off, net->fws_bytes, stream));
+      if (nonfinite) {
+        float* part = (float*)(ws + p.cs_off);
+        MDNN_TRY(column_sums_partial(gcur, lp, B, o, part, as_stream(stream)));
+        if (bias_sums.n == kMaxColsumBatch) {
+          MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
+          bias_sums.n = 0;
+        }
+        const int e = bias_sums.n++;
+        bias_sums.part[e] = part;
+        bias_sums.out[e] = gb;
+        bias_sums.chunks[e] = column_sums_chunks(B);
+        bias_sums.cols[e] = o;
+      } else {
+        MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, ws + net->fws_off,
+                                   net->fws_bytes, stream));
+      }
       if (ii > 0) {
         // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
         MDNN_TRY(gemm_mixed_ws(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0, gnxt, in, lp,
@@ -340,6 +360,8 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     gcur = gnxt;
     gnxt = t;
   }
+
+  MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
 
   // update (and the low-precision working copy)
   if (async)
