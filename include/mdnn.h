@@ -404,6 +404,14 @@ mdnn_status_t mdnn_train_step_async(mdnn_net_t* net, const float* x, const void*
 /* Device pointer of stored activation i (0 = the low-precision input, i = output
  * of layer i-1) inside the bound workspace, for inspection; NULL if invalid. */
 const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i);
+/* Device pointer of one of the two buffers (which = 0 or 1) that hold the
+ * output gradients of the backward pass (the low-precision storage type,
+ * batch x features of the layer), for inspection; NULL if invalid.  The
+ * loss gradient (last layer, L - 1) goes to buffer 0 and each layer's input
+ * gradient to the other buffer, so the gradient with respect to the output
+ * of layer i is in buffer (L - 1 - i) % 2; after a step the buffers hold
+ * those of layers 0 and 1 (the last two written). */
+const void* mdnn_net_output_grad(const mdnn_net_t* net, int32_t which);
 void mdnn_net_destroy(mdnn_net_t* net);
 
 /* Recorded steps.  Section 3.1's SGD step for a small network is a few

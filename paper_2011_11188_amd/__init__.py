@@ -115,6 +115,8 @@ _lib.mdnn_last_error.restype = C.c_char_p
 _lib.mdnn_version.restype = C.c_char_p
 _lib.mdnn_net_activation.argtypes = [_vp, C.c_int32]
 _lib.mdnn_net_activation.restype = _vp
+_lib.mdnn_net_output_grad.argtypes = [_vp, C.c_int32]
+_lib.mdnn_net_output_grad.restype = _vp
 _lib.mdnn_net_destroy.argtypes = [_vp]
 _lib.mdnn_net_destroy.restype = None
 _lib.mdnn_graph_destroy.argtypes = [_vp]
@@ -170,7 +172,7 @@ def exported_symbols():
                                  "mdnn_gemm_split3_workspace", "mdnn_gemm_workspace",
                                  "mdnn_conv2d_fwd_winograd_workspace",
                                  "mdnn_last_error",
-                                 "mdnn_version", "mdnn_net_activation", "mdnn_net_destroy",
+                                 "mdnn_version", "mdnn_net_activation", "mdnn_net_output_grad", "mdnn_net_destroy",
                                  "mdnn_graph_destroy", "mdnn_set_gemm_tile"])
 
 
@@ -324,6 +326,10 @@ def mdnn_train_step(net, x, target, loss_out, stream=None):
 
 def mdnn_net_activation(net, i: int) -> Optional[int]:
     return _lib.mdnn_net_activation(net, i)
+
+
+def mdnn_net_output_grad(net, which: int) -> Optional[int]:
+    return _lib.mdnn_net_output_grad(net, which)
 
 
 def mdnn_net_destroy(net) -> None:

@@ -12,7 +12,7 @@ from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, L
                NN, NT, TN, ConvShape, LayerDesc, Scaler, TrainCfg, dtype_of, mdnn_conv2d_bwd_data,
                mdnn_conv2d_bwd_filter, mdnn_conv2d_bwd_filter_workspace, mdnn_conv2d_fwd,
                mdnn_gemm_mixed, mdnn_gemm_mixed_ws, mdnn_gemm_workspace, mdnn_gemm_split3,
-               mdnn_gemm_split3_workspace, mdnn_net_activation, mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
+               mdnn_gemm_split3_workspace, mdnn_net_activation, mdnn_net_output_grad, mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
                mdnn_split_f16, mdnn_train_step, mdnn_train_step_async, mdnn_train_graph_create,
                mdnn_graph_launch, mdnn_graph_destroy, mdnn_conv2d_fwd_winograd,
                mdnn_conv2d_fwd_winograd_workspace)
@@ -223,6 +223,9 @@ class Net:
 
     def activation_ptr(self, i: int) -> Optional[int]:
         return mdnn_net_activation(self.handle, i)
+
+    def output_grad_ptr(self, which: int) -> Optional[int]:
+        return mdnn_net_output_grad(self.handle, which)
 
     def close(self):
         if getattr(self, "handle", None):

@@ -30,19 +30,40 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
           "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
+RESOURCE_REMARK = "kernel-resource-usage"
+
+
+def _spills(lines) -> list:
+    """Kernels whose resource-usage remarks report vector registers spilled
+    to scratch memory (scalar spills go to vector-register lanes: cheap)."""
+    out, name = [], None
+    for line in lines:
+        if "Function Name:" in line:
+            name = line.split("Function Name:")[1].split()[0]
+        elif "VGPRs Spill:" in line and name is not None:
+            n = int(line.split("Spill:")[1].split()[0])
+            if n > 0:
+                out.append(f"{name}: {line.split('remark:')[1].split('[')[0].strip()}")
+    return out
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OUT_DIR, os.path.basename(src) + ".o")
     if src.endswith(".hip"):
-        cmd = [HIPCC, "-x", "hip", *DEVICE, *COMMON, "-c", src, "-o", obj]
+        cmd = [HIPCC, "-x", "hip", *DEVICE, *COMMON, f"-Rpass-analysis={RESOURCE_REMARK}", "-c", src, "-o", obj]
     else:
         cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
-    msgs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
-                     if "packed-fp32-ops" not in l and l.strip())
+    lines = (r.stdout + r.stderr).splitlines()
+    msgs = "\n".join(l for l in lines
+                     if "packed-fp32-ops" not in l and RESOURCE_REMARK not in l and l.strip())
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{msgs}")
     if msgs:
         print(msgs, file=sys.stderr)
+    # a kernel that spills vector registers to scratch has outgrown its budget
+    for s in _spills(lines):
+        print(f"warning: {os.path.basename(src)}: register spill in {s}", file=sys.stderr)
     return obj
 
 

@@ -209,6 +209,9 @@ inline void launch_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M,
 // that a square tile's columns (rows) are not mostly padding.
 typedef lds::Tile<256, 64, 4, 2, 4> TileNarrowN;
 typedef lds::Tile<64, 256, 2, 4, 2> TileNarrowM;
+// 128 x 128 with four LDS stages (128 KB): one workgroup per CU, so the
+// register budget is that of two waves per SIMD
+typedef lds::Tile<128, 128, 2, 4, 2> Tile128Deep;
 
 template <class T, class OutT, bool A_KC, bool B_KC>
 inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
@@ -224,7 +227,7 @@ inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int6
   else if (ceil_div(M, 128) * ceil_div(N, 128) * splits <= 256)
     // at most one workgroup per CU: the LDS a second one would use holds two
     // more stages instead, so three tiles are in flight behind the MFMAs
-    launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC, 4>(a, b, M, N, K, ep, splits, stream);
+    launch_gemm_lds<T, OutT, Tile128Deep, A_KC, B_KC, 4>(a, b, M, N, K, ep, splits, stream);
   else
     launch_gemm_lds<T, OutT, lds::Tile128, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
   return check_launch("gemm_lds_kernel");

@@ -246,6 +246,11 @@ extern "C" const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i) {
   return net->ws + net->layers[i - 1].out_off;
 }
 
+extern "C" const void* mdnn_net_output_grad(const mdnn_net_t* net, int32_t which) {
+  if (!net || !net->bound || (which != 0 && which != 1)) return nullptr;
+  return net->ws + (which == 0 ? net->g0_off : net->g1_off);
+}
+
 extern "C" void mdnn_net_destroy(mdnn_net_t* net) { delete net; }
 
 // One step; `async`: section 4.1's asynchronous variant, for nets that share

@@ -189,3 +189,48 @@ def test_train_step_reproducible(mdnn):
     gl2, n2 = _trajectory(mdnn, cfg, 3)
     assert gl1 == gl2
     assert bool((n1.master == n2.master).all()) and bool((n1.lowp == n2.lowp).all())
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("size", [(512, 1024), (4096, 4096)], ids=["b512_w1024", "full_b4096_w4096"])
+def test_wide_mlp_first_layer_gradients_from_stored_values(mdnn, size):
+    """Weight and bias gradients of the two first layers after one loss-scaled
+    step, against their definitions (dW = X^T dZ, db = column sums of dZ)
+    evaluated in fp64 on the GPU's own stored X and dZ (the same bits in, so a
+    rounding difference earlier in the chain -- a ReLU mask decided the other
+    way -- cannot show up here); bar: fp32 accumulation of B exact products,
+    gamma_B * sum |terms|.  In this step the weight-gradient GEMMs carry the
+    overflow test in their epilogue (256x256 tiles at full size, split K over
+    the workspace at width 1024) and the bias gradients' column sums are
+    finished for all layers, with the overflow test, in one pass.  Also: the
+    stored dZ of layer 0 is zero wherever the layer's ReLU output is not
+    positive."""
+    import torch
+    from tests.helpers import accum_bound
+    batch, width = size
+    cfg = W.wide_mlp_fp16(batch=batch, width=width)
+    net = _gpu_net(mdnn, cfg)
+    x, t = W.batch_inputs(cfg, 0)
+    net.step(dev(x, "f32"), _target(cfg, t))
+    torch.cuda.synchronize()
+    g = net.grads.cpu().numpy().astype(np.float64)
+    L = len(cfg.layers)
+
+    def stored(ptr, n):
+        off = ptr - net.ws.data_ptr()
+        return net.ws[off:off + 2 * n].clone().view(torch.float16).float().cpu().numpy().astype(np.float64)
+
+    dz = {}
+    for i, (wo, bo) in enumerate(cfg.param_offsets()[:2]):
+        l = cfg.layers[i]
+        a = stored(net.activation_ptr(i), batch * l.c_in).reshape(batch, l.c_in)
+        d = stored(net.output_grad_ptr((L - 1 - i) % 2), batch * l.c_out).reshape(batch, l.c_out)
+        dz[i] = d
+        dw = g[wo:wo + l.c_in * l.c_out].reshape(l.c_in, l.c_out)
+        db = g[bo:bo + l.c_out]
+        assert np.all(np.abs(dw - a.T @ d) <= accum_bound(np.abs(a).T @ np.abs(d), batch)), f"layer {i} dW"
+        assert np.all(np.abs(db - d.sum(axis=0)) <= accum_bound(np.abs(d).sum(axis=0), batch)), f"layer {i} db"
+        assert np.any(db != 0)
+    act1 = stored(net.activation_ptr(1), batch * cfg.layers[0].c_out).reshape(batch, -1)
+    assert np.all(dz[0][act1 <= 0] == 0)
+    assert mdnn.read_scaler(net.scaler)["good_steps"] == 1
