@@ -186,10 +186,19 @@ def _time_graph_steps(net, xs, ts, steps, warmup, check=None):
     return tm.ms / steps
 
 
+def _under_profiler() -> bool:
+    """True inside rocprofv3: its preloaded library would initialise the GPU
+    in every child process too, so no helper programs are started then."""
+    return "rocprof" in os.environ.get("LD_PRELOAD", "") or any(k.startswith("ROCPROF") for k in os.environ)
+
+
 def _clocks():
-    """Current shader / memory clocks (MHz) as rocm-smi reports them, or None."""
+    """Current shader / memory clocks (MHz) as rocm-smi reports them, or None
+    (also when running under the profiler)."""
     import re
     import subprocess
+    if _under_profiler():
+        return None
     try:
         out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True,
                              timeout=30).stdout
@@ -243,6 +252,8 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
             return "gemm_lds_kernel (64x256 direct-to-LDS pipeline)"
         if n > 128 and m > 128 and cd(m, 256) * cd(n, 256) >= 256:
             return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
+        if cd(m, 128) * cd(n, 128) <= 256:
+            return "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 4 stages)"
         return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
     if m <= 64 or n <= 64:
         return "gemm_mfma_kernel 64x64"
@@ -430,6 +441,8 @@ def _async_bench(mdnn, steps=40):
 def _traffic_key(kernel_desc: str) -> str:
     """'NN f16 -> f16 256x256' style key of a step kernel description."""
     tile = "256x256" if "256x256" in kernel_desc else "128x128"
+    if "4 stages" in kernel_desc:
+        tile += " (4 stages)"
     parts = kernel_desc.split(", ")
     return f"{parts[1]} {tile}"
 
