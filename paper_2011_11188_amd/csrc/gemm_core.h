@@ -331,20 +331,24 @@ __device__ __forceinline__ void load4(const typename T::storage* p, float (&o)[4
   }
 }
 
-template <class MaskT, class OutT>
+// FULL: the caller guarantees m < M, n + 4 <= N and 4-element vector access
+// to every operand the epilogue touches (vec4, vec4_c when beta != 0, vec4_m
+// with a mask, a 16-byte aligned bias), so no per-lane bound is tested and
+// the code is straight-line.
+template <class MaskT, class OutT, bool FULL = false>
 __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, int64_t N, int64_t m,
                                                 int64_t n, float4_t acc) {
-  if (m >= M) return;
+  if (!FULL && m >= M) return;
   float v[4] = {acc[0], acc[1], acc[2], acc[3]};
-  const bool in4 = n + 4 <= N;
-  const bool full = ep.vec4 && in4;
+  const bool in4 = FULL || n + 4 <= N;
+  const bool full = FULL || (ep.vec4 && in4);
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     v[e] *= ep.alpha;
   }
   if (ep.beta != 0.0f) {
     const typename OutT::storage* c = (const typename OutT::storage*)ep.C + m * ep.ldc + n;
-    if (ep.vec4_c && in4) {
+    if (FULL || (ep.vec4_c && in4)) {
       float cv[4];
       load4<OutT>(c, cv);
 #pragma unroll
@@ -356,7 +360,7 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
     }
   }
   if (ep.bias) {
-    if (in4 && ((uintptr_t)(ep.bias + n) & 15) == 0) {
+    if (FULL || (in4 && ((uintptr_t)(ep.bias + n) & 15) == 0)) {
       const float4 b = *(const float4*)(ep.bias + n);
       v[0] += b.x, v[1] += b.y, v[2] += b.z, v[3] += b.w;
     } else {
@@ -371,7 +375,7 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
   }
   if (ep.mask) {
     const typename MaskT::storage* mk = (const typename MaskT::storage*)ep.mask + m * ep.ldm + n;
-    if (ep.vec4_m && in4) {
+    if (FULL || (ep.vec4_m && in4)) {
       float mv[4];
       load4<MaskT>(mk, mv);
 #pragma unroll
@@ -388,7 +392,7 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
     if (ep.nonfinite) {
       bool bad = false;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) bad |= (n + e < N) && !isfinite(v[e]);
+      for (int e = 0; e < 4; ++e) bad |= (FULL || n + e < N) && !isfinite(v[e]);
       if (bad) atomicOr(ep.nonfinite, 1);
     }
   }
