@@ -331,6 +331,14 @@ __device__ __forceinline__ void load4(const typename T::storage* p, float (&o)[4
   }
 }
 
+// Whether a tile (every row < M and column < N: `inside`) can take the
+// straight-line epilogue (FULL below): 4-aligned rows of D, C and the mask,
+// a 16-byte aligned bias.
+__device__ __forceinline__ bool full_tile_epilogue(const Epilogue& ep, bool inside, int64_t N) {
+  return inside && ep.vec4 && (N & 3) == 0 && (ep.beta == 0.0f || ep.vec4_c) &&
+         (!ep.bias || ((uintptr_t)ep.bias & 15) == 0) && (!ep.mask || ep.vec4_m);
+}
+
 // FULL: the caller guarantees m < M, n + 4 <= N and 4-element vector access
 // to every operand the epilogue touches (vec4, vec4_c when beta != 0, vec4_m
 // with a mask, a 16-byte aligned bias), so no per-lane bound is tested and
@@ -618,6 +626,14 @@ gemm_mfma_kernel(SrcA srcA, SrcB srcB, int64_t M, int64_t N, int64_t K, Epilogue
             if (n + e < N) p[e] = acc[i][j][e];
         }
       }
+    return;
+  }
+  if (full_tile_epilogue(ep, m0 + BM <= M && n0 + BN <= N, N)) {
+#pragma unroll
+    for (int i = 0; i < TS::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < TS::FN; ++j)
+        epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j]);
     return;
   }
 #pragma unroll

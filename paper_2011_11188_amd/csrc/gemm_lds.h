@@ -714,10 +714,7 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
     return;
   }
   // interior tiles with 4-aligned rows everywhere take the straight-line store
-  const bool full_tile = m0 + TL::BM <= M && n0 + TL::BN <= N && ep.vec4 && (N & 3) == 0 &&
-                         (ep.beta == 0.0f || ep.vec4_c) && (!ep.bias || ((uintptr_t)ep.bias & 15) == 0) &&
-                         (!ep.mask || ep.vec4_m);
-  if (full_tile) {
+  if (full_tile_epilogue(ep, m0 + TL::BM <= M && n0 + TL::BN <= N, N)) {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll

@@ -268,6 +268,8 @@ skinny_depth_kernel(mdnn_layout_t layout, const typename T::storage* __restrict_
   // rows, grid-stride, so each thread reuses its B over several rows
   const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (n >= N) return;
+  // this thread's eight columns inside N with vector access (rows m < M by the loop)
+  const bool full = full_tile_epilogue(ep, n + 8 <= N, N);
   float b[8][KT];
 #pragma unroll
   for (int e = 0; e < 8; ++e)
@@ -287,8 +289,13 @@ skinny_depth_kernel(mdnn_layout_t layout, const typename T::storage* __restrict_
         hi[e] = fmaf(a[k], b[4 + e][k], hi[e]);
       }
     }
-    epilogue_store4<T, OutT>(ep, M, N, m, n, lo);
-    if (n + 4 < N) epilogue_store4<T, OutT>(ep, M, N, m, n + 4, hi);
+    if (full) {
+      epilogue_store4<T, OutT, true>(ep, M, N, m, n, lo);
+      epilogue_store4<T, OutT, true>(ep, M, N, m, n + 4, hi);
+    } else {
+      epilogue_store4<T, OutT>(ep, M, N, m, n, lo);
+      if (n + 4 < N) epilogue_store4<T, OutT>(ep, M, N, m, n + 4, hi);
+    }
   }
 }
 
