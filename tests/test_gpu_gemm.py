@@ -104,6 +104,37 @@ def test_gemm_pipelined_kernel_ragged(mdnn, dt, layout, tile):
         mdnn.mdnn_set_gemm_tile(0)
 
 
+@pytest.mark.parametrize("tile", [1, 2, 4, 5])
+@pytest.mark.parametrize("out_dt", ["f32", "f16"])
+def test_gemm_every_epilogue_term_interior_and_edge_tiles(mdnn, tile, out_dt):
+    """alpha, beta * C, bias, ReLU and the ReLU mask together, on a shape whose
+    interior tiles take the straight-line store (4-aligned rows of D, C and
+    the mask, aligned bias) and whose edge tiles take the bounded one, in the
+    general (tile 1, 2) and pipelined (4, 5) kernels."""
+    dt = "f16"
+    m, n, k = 520, 776, 320
+    mdnn.mdnn_set_gemm_tile(tile)
+    try:
+        a = W.normal((m, k), 12, 1, dt, 1 / np.sqrt(k))
+        b = W.normal((k, n), 12, 2, dt)
+        c = W.normal((m, n), 12, 3, out_dt)
+        bias = W.normal((n,), 12, 4, "f32", 0.5)
+        y_in = W.normal((m, n), 12, 5, dt)
+        got = _run(mdnn, "NN", dev(a, dt), dev(b, dt), out_dt, m, n, k, bias=dev(bias, "f32"), act=1,
+                   mask=dev(y_in, dt), alpha=0.75, beta=-0.5, Cm=dev(c, out_dt))
+        a64, b64, c64 = decode(a, dt), decode(b, dt), decode(c, out_dt)
+        pre = 0.75 * ops.gemm("NN", a64, b64) - 0.5 * c64
+        exact = np.where(decode(y_in, dt) > 0, ops.bias_act(pre, bias.astype(np.float64), "relu"), 0.0)
+        err = accum_bound(0.75 * (np.abs(a64) @ np.abs(b64)) + 0.5 * np.abs(c64) + np.abs(bias), k + 2)
+        if out_dt == "f32":
+            assert np.all(np.abs(got - exact) <= err + 2.0 ** -23 * np.abs(exact))
+        else:
+            assert lowp_close(got, exact, dt, err)
+        assert np.all(got[decode(y_in, dt) <= 0] == 0)
+    finally:
+        mdnn.mdnn_set_gemm_tile(0)
+
+
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 def test_gemm_small_integers_bit_exact(mdnn, dt, layout):
