@@ -10,7 +10,9 @@
 namespace mdnn {
 
 // Forward: y = epilogue(im2col(x) . w^T), M = n*ho*wo, N = c_out, K = r*s*c_in.
-// Needs c_in % 64 == 0, 16-byte aligned x and w, x below 2^31 bytes.
+// Needs c_in % 32 == 0 (one tap per K step when c_in % 64 == 0, else two
+// 32-channel half blocks per step with K padded), 16-byte aligned x and w,
+// x (and, for c_in % 64 != 0, w) below 2^31 bytes.
 mdnn_status_t conv_pipe_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep,
                             mdnn_dtype_t io, mdnn_dtype_t out, hipStream_t st, bool* done);
 

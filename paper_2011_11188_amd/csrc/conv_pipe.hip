@@ -60,12 +60,44 @@ mdnn_status_t rows_typed(const lds::ConvRowsArgs& a, const void* w, int32_t ldw,
 
 }  // namespace
 
+// Forward with c_in % 32 == 0 (not 64): K padded to whole steps of two
+// 32-channel half blocks, the filter read range-checked.
+template <class T, class OutT>
+mdnn_status_t rows32_dispatch(const lds::ConvRowsArgs& a, const lds::MatRCArgs& b, int64_t M, int64_t N, int64_t Kp,
+                              const Epilogue& ep, hipStream_t st) {
+  if (N <= 64)
+    return run_pipe<T, OutT, TileTall, 2, lds::ConvRows32Loader<256, TileTall::LA>,
+                    lds::MatLoaderRC<64, TileTall::LB>>(a, b, M, N, Kp, ep, 1, st);
+  return run_pipe<T, OutT, TileSquare, 2, lds::ConvRows32Loader<128, TileSquare::LA>,
+                  lds::MatLoaderRC<128, TileSquare::LB>>(a, b, M, N, Kp, ep, 1, st);
+}
+
+mdnn_status_t conv_pipe_fwd32(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
+                              mdnn_dtype_t out, hipStream_t st, bool* done) {
+  const int64_t M = (int64_t)g.n * g.ho * g.wo, N = g.k, K = (int64_t)g.r * g.s * g.c;
+  const int64_t x_bytes = (int64_t)g.n * g.h * g.w * g.c * 2, w_bytes = N * K * 2;
+  if (x_bytes > BUF_MAX || w_bytes > BUF_MAX || M > BUF_MAX) return MDNN_SUCCESS;
+  const int64_t Kp = ceil_div(K, (int64_t)lds::BK) * lds::BK;
+  lds::ConvRowsArgs a{x, (uint32_t)x_bytes, g.h, g.w, g.c, g.ho, g.wo, g.s, g.pad, 0, M};
+  a.r = g.r;
+  const lds::MatRCArgs b{w, (uint32_t)w_bytes, K, N};
+  if (io == MDNN_F16)
+    MDNN_TRY((out == MDNN_F32 ? rows32_dispatch<F16, F32>(a, b, M, N, Kp, ep, st)
+                              : rows32_dispatch<F16, F16>(a, b, M, N, Kp, ep, st)));
+  else
+    MDNN_TRY((out == MDNN_F32 ? rows32_dispatch<BF16, F32>(a, b, M, N, Kp, ep, st)
+                              : rows32_dispatch<BF16, BF16>(a, b, M, N, Kp, ep, st)));
+  *done = true;
+  return MDNN_SUCCESS;
+}
+
 mdnn_status_t conv_pipe_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep,
                             mdnn_dtype_t io, mdnn_dtype_t out, hipStream_t st, bool* done) {
   *done = false;
   const int64_t M = (int64_t)g.n * g.ho * g.wo, N = g.k, K = (int64_t)g.r * g.s * g.c;
   const int64_t x_bytes = (int64_t)g.n * g.h * g.w * g.c * 2;
-  if (io == MDNN_F32 || g.c % 64 != 0 || !aligned(x, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
+  if (io == MDNN_F32 || !aligned(x, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
+  if (g.c % 64 != 0) return g.c % 32 == 0 ? conv_pipe_fwd32(g, x, w, ep, io, out, st, done) : MDNN_SUCCESS;
   if (x_bytes > BUF_MAX || M > BUF_MAX || N * K * 2 >= ((int64_t)1 << 32)) return MDNN_SUCCESS;
   const lds::ConvRowsArgs a{x, (uint32_t)x_bytes, g.h, g.w, g.c, g.ho, g.wo, g.s, g.pad, 0, M};
   MDNN_TRY(rows_typed<false>(a, w, (int32_t)K, g, M, N, K, ep, io, out, st));

@@ -16,6 +16,9 @@
 //   ConvRowsLoader   im2col rows of a convolution input (forward: x, backward
 //                    data: dy with mirrored taps); one K step is 64 channels of
 //                    one filter tap, so the tap shift is uniform per step.
+//   ConvRows32Loader forward im2col rows when c_in is a multiple of 32 only:
+//                    a K step is 32 channels of two taps (per-lane tap state),
+//                    with MatLoaderRC reading the filter range-checked.
 //   TapWeightLoader  the filter read as [tap, c_out] x [c_in] (backward data).
 //   ConvColsLoader   shifted input columns of the backward-filter GEMM
 //                    (K = output pixels, N = (tap, c_in)).
@@ -204,6 +207,7 @@ struct ConvRowsArgs {
   int32_t ho, wo;     // GEMM row grid
   int32_t s, pad, flip;
   int64_t M;
+  int32_t r;          // filter rows (ConvRows32Loader only)
 };
 template <int W, int L>
 struct ConvRowsLoader {
@@ -256,6 +260,116 @@ struct ConvRowsLoader {
         ++tr;
       }
     }
+  }
+};
+
+// im2col rows for a forward convolution whose input channel count is a
+// multiple of 32 but not of 64: a K step is two 32-channel half blocks,
+// half block h = tap * (c / 32) + b holding channels 32b .. 32b + 31 of one
+// tap, so GEMM column kk = tap * c + ch as in the filter's own layout.  The
+// K range is padded to whole steps: a half block past the last tap reads
+// zeros (its filter columns are then multiplied by zero).
+template <int W, int L>
+struct ConvRows32Loader {
+  static constexpr bool KC = true;
+  static constexpr bool SPLIT_ISSUE = false;  // the per-step state advances once per tile
+  typedef ConvRowsArgs Args;
+  // A lane's k offset within a step (load_pos) depends on its load index
+  // only through the index's parity when L is even (block wave * L + i), so
+  // the tap state is kept for P = 2 loads, not L.
+  static_assert(L == 1 || L % 2 == 0, "tap state per load parity");
+  static constexpr int P = L >= 2 ? 2 : 1;
+  int4_t rsrc;
+  int32_t hs, ws, c, s, r, pad, cpb;
+  uint32_t base[L];
+  int32_t ii[L], jj[L];
+  int32_t tr[P], ts[P], chb[P], ch[P];
+
+  __device__ __forceinline__ void init(const ConvRowsArgs& a, int64_t mn0, int64_t kbeg, int wave, int lane) {
+    rsrc = make_rsrc(a.p, a.bytes);
+    hs = a.hs, ws = a.ws, c = a.c, s = a.s, r = a.r, pad = a.pad;
+    cpb = a.c / 32;
+    const int32_t kt = (int32_t)(kbeg / BK);
+    const int32_t hw = a.ho * a.wo;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const LoadPos q = load_pos<true, W, L>(wave, lane, i);
+      if (i < P) {
+        const int32_t h = 2 * kt + q.c / 32, tap = h / cpb;
+        chb[i] = h - tap * cpb;
+        tr[i] = tap / a.s;
+        ts[i] = tap - tr[i] * a.s;
+        ch[i] = q.c % 32;
+      }
+      const int64_t m = mn0 + q.r;
+      if (m < a.M) {
+        const int32_t mi = (int32_t)m, n = mi / hw, rem = mi - n * hw, i0 = rem / a.wo, j0 = rem - i0 * a.wo;
+        ii[i] = i0;
+        jj[i] = j0;
+        base[i] = (uint32_t)(((n * a.hs + i0) * a.ws + j0) * a.c * 2);
+      } else {
+        ii[i] = -(1 << 20);  // outside the grid for every tap
+        jj[i] = 0;
+        base[i] = 0;
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(int, uint32_t dst) {
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int p = i % P;
+      const int32_t dh = tr[p] - pad, dw = ts[p] - pad;
+      const bool ok = tr[p] < r && (uint32_t)(ii[i] + dh) < (uint32_t)hs && (uint32_t)(jj[i] + dw) < (uint32_t)ws;
+      const uint32_t off = base[i] + (uint32_t)(((dh * ws + dw) * c + chb[p] * 32 + ch[p]) * 2);
+      dma_buffer(rsrc, ok ? off : OOB, dst + (uint32_t)i * 1024u);
+    }
+    // two half blocks on: at most two tap advances (cpb >= 1)
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      chb[p] += 2;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (chb[p] >= cpb) {
+          chb[p] -= cpb;
+          if (++ts[p] == s) {
+            ts[p] = 0;
+            ++tr[p];
+          }
+        }
+      }
+    }
+  }
+};
+
+// A K-contiguous matrix [MN][ld] read through a range-checked buffer
+// resource: columns past the end of the last row (a K range padded to whole
+// steps) read as zero instead of past the allocation.
+struct MatRCArgs {
+  const void* p;
+  uint32_t bytes;
+  int64_t ld, MN;
+};
+template <int W, int L>
+struct MatLoaderRC {
+  static constexpr bool KC = true;
+  static constexpr bool SPLIT_ISSUE = false;
+  typedef MatRCArgs Args;
+  int4_t rsrc;
+  uint32_t off[L];
+
+  __device__ __forceinline__ void init(const MatRCArgs& a, int64_t mn0, int64_t kbeg, int wave, int lane) {
+    rsrc = make_rsrc(a.p, a.bytes);
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const LoadPos q = load_pos<true, W, L>(wave, lane, i);
+      int64_t row = mn0 + q.r;
+      if (row >= a.MN) row = a.MN - 1;
+      off[i] = (uint32_t)((row * a.ld + kbeg + q.c) * 2);
+    }
+  }
+  __device__ __forceinline__ void issue(int t, uint32_t dst) {
+#pragma unroll
+    for (int i = 0; i < L; ++i) dma_buffer(rsrc, off[i] + (uint32_t)t * (BK * 2), dst + (uint32_t)i * 1024u);
   }
 };
 

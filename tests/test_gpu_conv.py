@@ -140,6 +140,52 @@ def test_conv_pipelined_against_oracle(mdnn, shape, dt):
     assert norm_max_err(db, dy.sum(axis=(0, 1, 2))) <= TOL
 
 
+# Forward on the pipelined kernel with c_in a multiple of 32 but not of 64:
+# two 32-channel half blocks per K step, the K range padded to whole steps
+# (odd half-block counts: 3x3, 1x1, 5x3 taps at c_in = 32), several half
+# blocks per tap (c_in = 96, 160), both tile shapes, ragged M, valid and
+# wider padding.
+PIPE32 = [  # n, h, w, c_in, c_out, r, s, pad
+    (2, 14, 14, 32, 64, 5, 5, 2),    # LeNet conv2 shape at batch 2 (25 taps: a padded half block)
+    (3, 7, 9, 32, 40, 3, 3, 1),      # 9 taps, 256 x 64 tile, ragged M = 189
+    (2, 6, 5, 32, 72, 1, 1, 0),      # 1x1: one real half block per step, 128 x 128 tile
+    (2, 9, 7, 96, 24, 3, 3, 0),      # three half blocks per tap, valid padding
+    (1, 8, 11, 160, 136, 5, 3, 2),   # five half blocks per tap, 5x3 taps, N = 136
+]
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("shape", PIPE32)
+def test_conv_fwd_32_channel_blocks_against_oracle(mdnn, shape, dt):
+    n, h, w, ci, co, r, s, pad = shape
+    (x, wt, dy), (y, dx, dw, db) = _ops(mdnn, shape, dt, 23)
+    assert norm_max_err(y, ops.conv2d_fwd(x, wt, pad)) <= TOL
+    assert norm_max_err(dx, ops.conv2d_bwd_data(dy, wt, pad, h, w)) <= TOL
+    assert norm_max_err(dw, ops.conv2d_bwd_filter(x, dy, pad, r, s)) <= TOL
+
+
+def test_conv_fwd_32_channel_blocks_epilogue_and_integers(mdnn):
+    """The same path with bias + ReLU into bf16 (bound as for the other
+    pipelined forward), and bit-exact on small integers (the padded half
+    block contributes exact zeros)."""
+    import torch
+    n, h, w, ci, co, r, s, pad = 3, 9, 7, 32, 48, 3, 3, 1
+    x = W.normal((n, h, w, ci), 24, 1, "bf16", 0.3)
+    wt = W.normal((co, r, s, ci), 24, 2, "bf16", 0.1)
+    b = W.normal((co,), 24, 3, "f32", 0.2)
+    y = mdnn.conv2d_fwd(dev(x, "bf16"), dev(wt, "bf16"), pad, bias=dev(b, "f32"), act=mdnn.ACT_RELU)
+    torch.cuda.synchronize()
+    x64, w64 = decode(x, "bf16"), decode(wt, "bf16")
+    exact = ops.bias_act(ops.conv2d_fwd(x64, w64, pad), b.astype(np.float64), "relu")
+    err = accum_bound(ops.conv2d_fwd(np.abs(x64), np.abs(w64), pad) + np.abs(b), r * s * ci + 1)
+    assert lowp_close(host64(y), exact, "bf16", err)
+    xi = W.small_ints((n, h, w, ci), 25, 1, dtype="f16")
+    wi = W.small_ints((co, r, s, ci), 25, 2, dtype="f16")
+    yi = mdnn.conv2d_fwd(dev(xi, "f16"), dev(wi, "f16"), pad, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert np.array_equal(host64(yi), ops.conv2d_fwd(xi.astype(np.float64), wi.astype(np.float64), pad))
+
+
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 def test_conv_pipelined_epilogues_lowp(mdnn, dt):
     """Pipelined forward with bias+ReLU stored in the storage type, pipelined
