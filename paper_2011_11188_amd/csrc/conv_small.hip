@@ -3,9 +3,12 @@
 // the GEMM engine would spend almost all of a tile on padding, so these run
 // as direct kernels on the vector ALUs, fp32 accumulation.
 //
-//   forward (K = r*s*c_in <= 64): a block stages the im2col rows of 64
-//     output pixels and the whole filter in LDS; each thread produces four
-//     consecutive output channels of one pixel through the shared epilogue.
+//   forward (K = r*s*c_in <= 64): with c_out <= 32 a thread owns one output
+//     pixel (its im2col row gathered once into LDS, the filter staged once per
+//     256 pixels, all channels from broadcast filter reads); wider outputs:
+//     a block stages the im2col rows of 64 output pixels and the whole filter
+//     in LDS, and each thread produces four consecutive output channels of
+//     one pixel.  Both end in the shared epilogue.
 //   backward filter (c_out * r*s*c_in <= 1024 outputs, r*s*c_in <= 64): each
 //     block accumulates every filter element over its chunk of output pixels
 //     into fp32 partials, which the split reduction then sums in a fixed
@@ -100,6 +103,84 @@ conv_small_fwd_kernel(const typename T::storage* __restrict__ x, const typename 
   }
 }
 
+// Narrow outputs (c_out <= 32): one output pixel per thread.  The thread
+// decomposes its pixel once and gathers its own im2col row (taps walked with
+// counters, eight loads in flight) into LDS, the block stages the filter
+// once for 256 pixels, and the thread then produces all c_out channels from
+// its row and broadcast reads of the filter.
+constexpr int PX = 256;         // output pixels per block (one per thread)
+constexpr int PX_QUADS = 8;     // c_out <= 32
+
+template <class T, class OutT>
+__global__ void __launch_bounds__(256)
+conv_small_fwd_px_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ w,
+                         ConvGeom g, int64_t M, Epilogue ep) {
+  extern __shared__ float smem[];
+  const int K = g.r * g.s * g.c, N = g.k, KS = odd_stride(K), NP = quad_pad(N), nq = NP / 4;
+  float* xs = smem;            // [PX][KS] im2col rows
+  float* wt = smem + PX * KS;  // [K][NP] filter, transposed (zero beyond N)
+  const int tid = threadIdx.x;
+  stage<T>(w, K * NP, [=](int e) -> int64_t { const int kk = e / NP, n = e - kk * NP; return n < N ? (int64_t)n * K + kk : -1; },
+           [](int e) { return e; }, wt);
+  const int64_t m = (int64_t)blockIdx.x * PX + tid;
+  float* row = xs + tid * KS;
+  if (m < M) {
+    const int mi = (int)m, hw = g.ho * g.wo;  // pixel counts below 2^31 on this path
+    const int n = mi / hw, rem = mi - n * hw, i = rem / g.wo, j = rem - i * g.wo;
+    const typename T::storage* xn = x + (int64_t)n * g.h * g.w * g.c;
+    int tr = 0, ts = 0, ch = 0;  // tap row, tap column, channel of element kk
+    for (int kb = 0; kb < K; kb += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int y = i + tr - g.pad, xx = j + ts - g.pad;
+        const bool ok = kb + u < K && (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
+        const float val = to_f<T>(xn[ok ? ((int64_t)y * g.w + xx) * g.c + ch : 0]);
+        v[u] = ok ? val : 0.0f;
+        if (++ch == g.c) {
+          ch = 0;
+          if (++ts == g.s) {
+            ts = 0;
+            ++tr;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (kb + u < K) row[kb + u] = v[u];
+    }
+  }
+  __syncthreads();
+  if (m >= M) return;
+  float4_t acc[PX_QUADS];
+#pragma unroll
+  for (int q = 0; q < PX_QUADS; ++q) acc[q] = (float4_t){0.f, 0.f, 0.f, 0.f};
+  for (int kk = 0; kk < K; ++kk) {
+    const float a = row[kk];
+    const float* wk = wt + kk * NP;
+#pragma unroll
+    for (int q = 0; q < PX_QUADS; ++q) {
+      if (q < nq) {
+        const float4 b = *(const float4*)(wk + 4 * q);
+        acc[q][0] = fmaf(a, b.x, acc[q][0]);
+        acc[q][1] = fmaf(a, b.y, acc[q][1]);
+        acc[q][2] = fmaf(a, b.z, acc[q][2]);
+        acc[q][3] = fmaf(a, b.w, acc[q][3]);
+      }
+    }
+  }
+  const bool full = full_tile_epilogue(ep, 4 * nq <= N, N);
+#pragma unroll
+  for (int q = 0; q < PX_QUADS; ++q) {
+    if (q < nq) {
+      if (full)
+        epilogue_store4<T, OutT, true>(ep, M, N, m, 4 * q, acc[q]);
+      else
+        epilogue_store4<T, OutT>(ep, M, N, m, 4 * q, acc[q]);
+    }
+  }
+}
+
 // partial[b][k][kk] over the pixels of block b (pixels_per_block of them).
 // Thread task: output channels k4 .. k4+3 of filter column kk; per pixel one
 // 16-byte read of the output gradient row and one read of the patch.
@@ -164,6 +245,11 @@ size_t fwd_lds(const ConvGeom& g) {
   const int K = g.r * g.s * g.c;
   return ((size_t)TP * odd_stride(K) + (size_t)K * quad_pad(g.k)) * sizeof(float);
 }
+size_t fwd_px_lds(const ConvGeom& g) {
+  const int K = g.r * g.s * g.c;
+  return ((size_t)PX * odd_stride(K) + (size_t)K * quad_pad(g.k)) * sizeof(float);
+}
+bool fwd_px_ok(const ConvGeom& g) { return quad_pad(g.k) <= 4 * PX_QUADS && fwd_px_lds(g) <= LDS_LIMIT; }
 size_t filter_lds(const ConvGeom& g) {
   return (size_t)TP * (odd_stride(g.r * g.s * g.c) + quad_pad(g.k)) * sizeof(float);
 }
@@ -176,23 +262,34 @@ bool conv_small_fwd_ok(const ConvGeom& g) {
   return g.r * g.s * g.c <= 64 && g.k <= 256 && fwd_lds(g) <= LDS_LIMIT && pixels_fit(g);
 }
 
+template <class T, class OutT>
+static void small_fwd_launch(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, int64_t M,
+                             bool px, hipStream_t st) {
+  typedef typename T::storage S;
+  if (px)
+    hipLaunchKernelGGL((conv_small_fwd_px_kernel<T, OutT>), dim3((unsigned)ceil_div(M, PX)), dim3(256),
+                       fwd_px_lds(g), st, (const S*)x, (const S*)w, g, M, ep);
+  else
+    hipLaunchKernelGGL((conv_small_fwd_kernel<T, OutT>), dim3((unsigned)ceil_div(M, TP)), dim3(256), fwd_lds(g),
+                       st, (const S*)x, (const S*)w, g, M, ep);
+}
+
 mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
                              mdnn_dtype_t out, hipStream_t st) {
   const int64_t M = (int64_t)g.n * g.ho * g.wo;
   if (M == 0) return MDNN_SUCCESS;
   if (ceil_div(M, TP) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: too many output pixels");
-  const dim3 grid((unsigned)ceil_div(M, TP));
-#define MDNN_SMALL_FWD(T, O)                                                                                   \
-  hipLaunchKernelGGL((conv_small_fwd_kernel<T, O>), grid, dim3(256), fwd_lds(g), st, (const T::storage*)x,            \
-                     (const T::storage*)w, g, M, ep)
+  // one pixel per thread when c_out fits its registers
+  const bool px = fwd_px_ok(g);
   if (io == MDNN_F16) {
-    if (out == MDNN_F32) MDNN_SMALL_FWD(F16, F32); else MDNN_SMALL_FWD(F16, F16);
+    if (out == MDNN_F32) small_fwd_launch<F16, F32>(g, x, w, ep, M, px, st);
+    else small_fwd_launch<F16, F16>(g, x, w, ep, M, px, st);
   } else if (io == MDNN_BF16) {
-    if (out == MDNN_F32) MDNN_SMALL_FWD(BF16, F32); else MDNN_SMALL_FWD(BF16, BF16);
+    if (out == MDNN_F32) small_fwd_launch<BF16, F32>(g, x, w, ep, M, px, st);
+    else small_fwd_launch<BF16, BF16>(g, x, w, ep, M, px, st);
   } else {
-    MDNN_SMALL_FWD(F32, F32);
+    small_fwd_launch<F32, F32>(g, x, w, ep, M, px, st);
   }
-#undef MDNN_SMALL_FWD
   return check_launch("conv_small_fwd_kernel");
 }
 
