@@ -238,6 +238,84 @@ conv_small_filter_kernel(const typename T::storage* __restrict__ x, const typena
   }
 }
 
+// Filter gradient, one output pixel per thread for the staging: the thread
+// gathers its pixel's im2col row and output-gradient row into LDS (pixel
+// decomposed once, taps walked with counters, eight loads in flight), then
+// each thread accumulates four filter elements over the block's PX pixels.
+// partial[b][k][kk] as conv_small_filter_kernel, PX pixels per block.
+template <class T>
+__global__ void __launch_bounds__(256)
+conv_small_filter_px_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ dy,
+                            ConvGeom g, int64_t P, float* __restrict__ partial) {
+  extern __shared__ float smem[];
+  const int K = g.r * g.s * g.c, N = g.k, MN = N * K, KS = odd_stride(K), NP = quad_pad(N);
+  float* xs = smem;            // [PX][KS] im2col rows
+  float* ds = smem + PX * KS;  // [PX][NP] output gradient rows (zero beyond N)
+  const int tid = threadIdx.x;
+  const int64_t pix = (int64_t)blockIdx.x * PX + tid;
+  float* xrow = xs + tid * KS;
+  float* drow = ds + tid * NP;
+  if (pix < P) {
+    const int mi = (int)pix, hw = g.ho * g.wo;  // pixel counts below 2^31 on this path
+    const int n = mi / hw, rem = mi - n * hw, i = rem / g.wo, j = rem - i * g.wo;
+    const typename T::storage* xn = x + (int64_t)n * g.h * g.w * g.c;
+    int tr = 0, ts = 0, ch = 0;
+    for (int kb = 0; kb < K; kb += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int y = i + tr - g.pad, xx = j + ts - g.pad;
+        const bool ok = kb + u < K && (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
+        const float val = to_f<T>(xn[ok ? ((int64_t)y * g.w + xx) * g.c + ch : 0]);
+        v[u] = ok ? val : 0.0f;
+        if (++ch == g.c) {
+          ch = 0;
+          if (++ts == g.s) {
+            ts = 0;
+            ++tr;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (kb + u < K) xrow[kb + u] = v[u];
+    }
+    const typename T::storage* drp = dy + pix * N;
+    for (int kb = 0; kb < NP; kb += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bool ok = kb + u < N;
+        const float val = to_f<T>(drp[ok ? kb + u : 0]);
+        v[u] = ok ? val : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (kb + u < NP) drow[kb + u] = v[u];
+    }
+  } else {
+    for (int kk = 0; kk < K; ++kk) xrow[kk] = 0.0f;
+    for (int k = 0; k < NP; ++k) drow[k] = 0.0f;
+  }
+  __syncthreads();
+  const int G4 = NP / 4, tasks = G4 * K;
+  for (int t = tid; t < tasks; t += 256) {
+    const int kk = t / G4, k4 = (t - kk * G4) * 4;
+    float4_t s = {0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < PX; ++p) {
+      const float a = xs[p * KS + kk];
+      const float4 d = *(const float4*)(ds + p * NP + k4);
+      s[0] = fmaf(d.x, a, s[0]);
+      s[1] = fmaf(d.y, a, s[1]);
+      s[2] = fmaf(d.z, a, s[2]);
+      s[3] = fmaf(d.w, a, s[3]);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (k4 + e < N) partial[(int64_t)blockIdx.x * MN + (int64_t)(k4 + e) * K + kk] = s[e];
+  }
+}
+
 constexpr int64_t FILTER_PIXELS = 128;  // pixels per block of the filter gradient (enough blocks to hide the staging latency)
 constexpr size_t LDS_LIMIT = 65536;      // dynamic LDS bytes per block
 
@@ -253,6 +331,10 @@ bool fwd_px_ok(const ConvGeom& g) { return quad_pad(g.k) <= 4 * PX_QUADS && fwd_
 size_t filter_lds(const ConvGeom& g) {
   return (size_t)TP * (odd_stride(g.r * g.s * g.c) + quad_pad(g.k)) * sizeof(float);
 }
+size_t filter_px_lds(const ConvGeom& g) {
+  return (size_t)PX * (odd_stride(g.r * g.s * g.c) + quad_pad(g.k)) * sizeof(float);
+}
+bool filter_px_ok(const ConvGeom& g) { return filter_px_lds(g) <= LDS_LIMIT; }
 
 }  // namespace
 
@@ -297,7 +379,21 @@ int64_t conv_small_filter_blocks(const ConvGeom& g) {
   const int K = g.r * g.s * g.c;
   if (K > 64 || g.k > 256 || (int64_t)g.k * K > 1024 || filter_lds(g) > LDS_LIMIT || !pixels_fit(g)) return 0;
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
-  return ceil_div(P, FILTER_PIXELS);
+  return ceil_div(P, filter_px_ok(g) ? (int64_t)PX : FILTER_PIXELS);
+}
+
+// one pixel per thread when the block's rows fit in LDS (the block count
+// conv_small_filter_blocks gives matches the kernel chosen here)
+template <class T>
+static void small_filter_launch(const ConvGeom& g, const void* x, const void* dy, int64_t P, int64_t blocks,
+                                float* part, hipStream_t st) {
+  typedef typename T::storage S;
+  if (filter_px_ok(g))
+    hipLaunchKernelGGL((conv_small_filter_px_kernel<T>), dim3((unsigned)blocks), dim3(256), filter_px_lds(g), st,
+                       (const S*)x, (const S*)dy, g, P, part);
+  else
+    hipLaunchKernelGGL((conv_small_filter_kernel<T>), dim3((unsigned)blocks), dim3(256), filter_lds(g), st,
+                       (const S*)x, (const S*)dy, g, P, FILTER_PIXELS, part);
 }
 
 mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
@@ -306,13 +402,9 @@ mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
   if (blocks <= 0 || blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: filter gradient shape");
   float* part = (float*)ws;
-#define MDNN_SMALL_FILT(T)                                                                                      \
-  hipLaunchKernelGGL((conv_small_filter_kernel<T>), dim3((unsigned)blocks), dim3(256), filter_lds(g), st,               \
-                     (const T::storage*)x, (const T::storage*)dy, g, P, FILTER_PIXELS, part)
-  if (io == MDNN_F16) MDNN_SMALL_FILT(F16);
-  else if (io == MDNN_BF16) MDNN_SMALL_FILT(BF16);
-  else MDNN_SMALL_FILT(F32);
-#undef MDNN_SMALL_FILT
+  if (io == MDNN_F16) small_filter_launch<F16>(g, x, dy, P, blocks, part, st);
+  else if (io == MDNN_BF16) small_filter_launch<BF16>(g, x, dy, P, blocks, part, st);
+  else small_filter_launch<F32>(g, x, dy, P, blocks, part, st);
   MDNN_TRY(check_launch("conv_small_filter_kernel"));
   return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st);
 }
