@@ -382,6 +382,10 @@ static SplitPlan lp_split_plan(int64_t M, int64_t N, int64_t K, int64_t tile) {
   if (tiles >= 128 || K < 256 || gemm_tile_override() != TILE_AUTO) return p;
   int64_t sp = ceil_div(256, tiles);
   if (sp > K / 128) sp = K / 128;
+  // the fp32 partials are written and read back once more: keep them within
+  // about 8 MiB unless the output is larger than that (then two splits)
+  const int64_t cap = ceil_div((int64_t)8 << 20, M * N * 4);
+  if (sp > (cap > 2 ? cap : 2)) sp = cap > 2 ? cap : 2;
   if (sp < 2) return p;
   const int64_t kps = ceil_div(ceil_div(K, sp), 64) * 64;
   p.splits = (int)ceil_div(K, kps);
