@@ -388,7 +388,12 @@ mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* grads, floa
 mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream);
 /* One SGD step.  x: fp32 [batch, in_features] (NHWC-flattened images);
  * target: int32 labels [batch] (XENT) or fp32 [batch, out] (MSE);
- * loss_out: device fp32 scalar, the unscaled loss of this step's forward pass. */
+ * loss_out: device fp32 scalar, the unscaled loss of this step's forward pass.
+ * With loss scaling the update is skipped when any gradient is Inf or NaN,
+ * as in mdnn_sgd_update; the step tests the gradients where it produces
+ * them (GEMM epilogues, the bias column sums) plus one pass over the ranges
+ * no such producer covers, instead of a second pass over all gradients.
+ * grads holds this step's scaled gradients afterwards. */
 mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
                               float* loss_out, mdnn_stream_t stream);
 /* Asynchronous step (section 4.1): for several nets bound to the same

@@ -52,7 +52,9 @@ struct mdnn_net {
   // values by the GEMMs that write them and the FC bias gradients by the
   // pass that finishes their column sums; `unchecked` lists the other
   // gradient ranges (convolution layers) for a separate check.
-  // prechecked is false when they do not fit in one CheckRanges.
+  // prechecked is false when they do not fit in one CheckRanges (or the
+  // batch is too tall for the batched column sums): then the update runs the
+  // full check.
   bool prechecked = false;
   CheckRanges unchecked{};
 };
@@ -137,7 +139,8 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
   }
   net->n_params = off;
   net->in_feat = net->layers[0].in_feat;
-  net->prechecked = true;
+  // (the batched bias column sums take at most 65535 row chunks)
+  net->prechecked = column_sums_chunks(batch) <= 65535;
   for (const auto& p : net->layers) {
     int64_t o = 0, len = 0;
     if (p.L.kind == MDNN_LAYER_CONV) o = p.w_off, len = p.nw + p.nb;
