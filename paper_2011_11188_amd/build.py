@@ -11,6 +11,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 import time
@@ -31,6 +32,30 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
 
 
 RESOURCE_REMARK = "kernel-resource-usage"
+
+
+def _diagnostics(lines) -> list:
+    """Compiler output without the resource-usage remarks (read by _spills)
+    and their include-chain and source-excerpt lines, and without the host
+    pass's note that it does not know the packed-fp32 target feature."""
+    out, pending, in_remark = [], [], False
+    for line in lines:
+        if not line.strip() or "packed-fp32-ops" in line:
+            continue
+        if line.startswith("In file included from"):
+            pending.append(line)
+            continue
+        excerpt = re.match(r"^\s*(\d+\s*)?\|", line) is not None
+        if RESOURCE_REMARK in line:
+            pending, in_remark = [], True
+            continue
+        if excerpt and in_remark:
+            continue
+        in_remark = False
+        out.extend(pending)
+        pending = []
+        out.append(line)
+    return out + pending
 
 
 def _spills(lines) -> list:
@@ -55,8 +80,7 @@ def _compile(src: str) -> str:
         cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     lines = (r.stdout + r.stderr).splitlines()
-    msgs = "\n".join(l for l in lines
-                     if "packed-fp32-ops" not in l and RESOURCE_REMARK not in l and l.strip())
+    msgs = "\n".join(_diagnostics(lines))
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{msgs}")
     if msgs:
