@@ -160,6 +160,55 @@ colsum_partial_kernel(const typename T::storage* __restrict__ x, const typename 
   }
 }
 
+// Pass 1 of the split API for 16-bit rows whose width is a multiple of 512
+// (the train step's bias gradients): chunks of COLSUM_STRIP_ROWS rows; a
+// block reduces one chunk x 512 columns, each wave reading whole 1 KB runs
+// of its rows (wave w: rows w, w + 4, ...; 8 columns per lane), then the
+// four waves' sums are combined in a fixed order.
+constexpr int64_t COLSUM_STRIP_ROWS = 64;
+static bool colsum_strip(mdnn_dtype_t t, int64_t cols) { return t != MDNN_F32 && cols % 512 == 0; }
+
+template <class T>
+__global__ void __launch_bounds__(256)
+colsum_strip_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols, float* __restrict__ partial) {
+  __shared__ float4 red[4][2][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t c0 = (int64_t)blockIdx.x * 512 + lane * 8;
+  const int64_t r0 = (int64_t)blockIdx.y * COLSUM_STRIP_ROWS;
+  const int64_t nr = rows - r0 < COLSUM_STRIP_ROWS ? rows - r0 : COLSUM_STRIP_ROWS;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  auto add8 = [&](const uint4& v) {
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] += to_f<T>((uint16_t)(vw[e >> 1] >> ((e & 1) * 16)));
+  };
+  const uint16_t* base = x + (r0 + w) * cols + c0;
+  if (nr == COLSUM_STRIP_ROWS) {
+    // a whole chunk: all of this lane's rows are loaded before any is added
+    constexpr int RPW = COLSUM_STRIP_ROWS / 4;
+    uint4 v[RPW];
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) v[u] = *(const uint4*)(base + (int64_t)(4 * u) * cols);
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) add8(v[u]);
+  } else {
+    for (int64_t r = w; r < nr; r += 4) add8(*(const uint4*)(base + (r - w) * cols));
+  }
+  red[w][0][lane] = make_float4(s[0], s[1], s[2], s[3]);
+  red[w][1][lane] = make_float4(s[4], s[5], s[6], s[7]);
+  __syncthreads();
+  // thread t: columns 2t and 2t + 1 of the block's 512 (lane t / 4's values)
+  const int l = threadIdx.x >> 2, h = (threadIdx.x >> 1) & 1, q = threadIdx.x & 1;
+  float2 t = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float4 v = red[k][h][l];
+    t.x += q ? v.z : v.x;
+    t.y += q ? v.w : v.y;
+  }
+  *(float2*)(partial + blockIdx.y * cols + (int64_t)blockIdx.x * 512 + 2 * threadIdx.x) = t;
+}
+
 __global__ void __launch_bounds__(256)
 colsum_final_kernel(const float* __restrict__ partial, int64_t chunks, int64_t cols,
                     float* __restrict__ out) {
@@ -260,13 +309,25 @@ mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t 
   return check_launch("column sums");
 }
 
-int64_t column_sums_chunks(int64_t rows) { return ceil_div(rows, COLSUM_ROWS); }
+int64_t column_sums_chunks(int64_t rows, int64_t cols, mdnn_dtype_t t) {
+  return ceil_div(rows, colsum_strip(t, cols) ? COLSUM_STRIP_ROWS : COLSUM_ROWS);
+}
 
 mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* partial,
                                   hipStream_t st) {
-  const int64_t chunks = column_sums_chunks(rows);
+  const int64_t chunks = column_sums_chunks(rows, cols, t);
   if (cols == 0 || chunks == 0) return MDNN_SUCCESS;
   if (chunks > 65535 || ceil_div(cols, 64) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "column sums: too many rows");
+  if (colsum_strip(t, cols)) {
+    if (!aligned(x, 16) || !aligned(partial, 8))
+      return fail(MDNN_ERR_MISALIGNED, "column sums: rows of 512k 16-bit columns need 16-byte alignment");
+    const dim3 sgrid((unsigned)(cols / 512), (unsigned)chunks);
+    if (t == MDNN_F16)
+      hipLaunchKernelGGL(colsum_strip_kernel<F16>, sgrid, dim3(256), 0, st, (const uint16_t*)x, rows, cols, partial);
+    else
+      hipLaunchKernelGGL(colsum_strip_kernel<BF16>, sgrid, dim3(256), 0, st, (const uint16_t*)x, rows, cols, partial);
+    return check_launch("column sums (partials)");
+  }
   const dim3 grid((unsigned)ceil_div(cols, 64), (unsigned)chunks);
   const bool vec = aligned(x, 16) && cols % 8 == 0;
   switch (t) {

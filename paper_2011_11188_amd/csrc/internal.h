@@ -51,11 +51,15 @@ size_t column_sums_ws_bytes(int64_t rows, int64_t cols);
 mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
                           float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 // The two passes apart, for a caller that finishes several matrices' sums in
-// one launch: pass 1 writes partial[column_sums_chunks(rows)][cols] (fp32,
-// 4-byte aligned); pass 2 sums each entry's partials in the same fixed order
-// as column_sums and, when nonfinite is given, ORs 1 into it for every
-// non-finite sum (the loss scaler's overflow test of the sums it stores).
-int64_t column_sums_chunks(int64_t rows);
+// one launch: pass 1 writes partial[column_sums_chunks(rows, cols, t)][cols]
+// (fp32, 8-byte aligned; 16-bit rows whose width is a multiple of 512 are
+// read in 64-row chunks of whole 1 KB runs and need 16-byte aligned x, other
+// shapes take column_sums' 256-row chunks); pass 2 sums each entry's
+// partials in a fixed order and, when nonfinite is given, ORs 1 into it for
+// every non-finite sum (the loss scaler's overflow test of the sums it
+// stores).  Deterministic, but not bitwise the same as column_sums where
+// the chunks differ.
+int64_t column_sums_chunks(int64_t rows, int64_t cols, mdnn_dtype_t t);
 mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* partial,
                                   hipStream_t stream);
 constexpr int kMaxColsumBatch = 32;

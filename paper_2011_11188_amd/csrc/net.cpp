@@ -140,7 +140,9 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
   net->n_params = off;
   net->in_feat = net->layers[0].in_feat;
   // (the batched bias column sums take at most 65535 row chunks)
-  net->prechecked = column_sums_chunks(batch) <= 65535;
+  net->prechecked = true;
+  for (const auto& p : net->layers)
+    if (p.L.kind == MDNN_LAYER_FC && column_sums_chunks(batch, p.L.c_out, net->lp) > 65535) net->prechecked = false;
   for (const auto& p : net->layers) {
     int64_t o = 0, len = 0;
     if (p.L.kind == MDNN_LAYER_CONV) o = p.w_off, len = p.nw + p.nb;
@@ -183,7 +185,7 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
     if (p.L.kind == MDNN_LAYER_FC) {
       const int64_t in = p.L.c_in, o = p.L.c_out;
       p.cs_off = w;
-      w = align256(w + (size_t)column_sums_chunks(batch) * o * 4);
+      w = align256(w + (size_t)column_sums_chunks(batch, o, net->lp) * o * 4);
       const size_t needs[4] = {mdnn_bias_act_bwd_workspace(batch, o), gemm_ws_bytes(net->lp, batch, o, in),
                                gemm_ws_bytes(net->lp, in, o, batch), gemm_ws_bytes(net->lp, batch, in, o)};
       for (size_t need : needs)
@@ -343,7 +345,7 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
         const int e = bias_sums.n++;
         bias_sums.part[e] = part;
         bias_sums.out[e] = gb;
-        bias_sums.chunks[e] = column_sums_chunks(B);
+        bias_sums.chunks[e] = column_sums_chunks(B, o, lp);
         bias_sums.cols[e] = o;
       } else {
         MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, ws + net->fws_off,

@@ -192,7 +192,8 @@ def test_train_step_reproducible(mdnn):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("size", [(512, 1024), (4096, 4096)], ids=["b512_w1024", "full_b4096_w4096"])
+@pytest.mark.parametrize("size", [(512, 1024, "f16"), (4096, 4096, "f16"), (100, 512, "bf16")],
+                         ids=["b512_w1024", "full_b4096_w4096", "b100_w512_bf16"])
 def test_wide_mlp_first_layer_gradients_from_stored_values(mdnn, size):
     """Weight and bias gradients of the two first layers after one loss-scaled
     step, against their definitions (dW = X^T dZ, db = column sums of dZ)
@@ -204,11 +205,13 @@ def test_wide_mlp_first_layer_gradients_from_stored_values(mdnn, size):
     the workspace at width 1024) and the bias gradients' column sums are
     finished for all layers, with the overflow test, in one pass.  Also: the
     stored dZ of layer 0 is zero wherever the layer's ReLU output is not
-    positive."""
+    positive.  The bias sums read the 16-bit dZ in 64-row chunks of whole
+    rows; batch 100 leaves a ragged chunk of 36 rows."""
+    import dataclasses
     import torch
     from tests.helpers import accum_bound
-    batch, width = size
-    cfg = W.wide_mlp_fp16(batch=batch, width=width)
+    batch, width, dt = size
+    cfg = dataclasses.replace(W.wide_mlp_fp16(batch=batch, width=width), dtype=dt)
     net = _gpu_net(mdnn, cfg)
     x, t = W.batch_inputs(cfg, 0)
     net.step(dev(x, "f32"), _target(cfg, t))
@@ -218,7 +221,8 @@ def test_wide_mlp_first_layer_gradients_from_stored_values(mdnn, size):
 
     def stored(ptr, n):
         off = ptr - net.ws.data_ptr()
-        return net.ws[off:off + 2 * n].clone().view(torch.float16).float().cpu().numpy().astype(np.float64)
+        st = torch.float16 if dt == "f16" else torch.bfloat16
+        return net.ws[off:off + 2 * n].clone().view(st).float().cpu().numpy().astype(np.float64)
 
     dz = {}
     for i, (wo, bo) in enumerate(cfg.param_offsets()[:2]):
