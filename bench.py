@@ -447,12 +447,24 @@ def _traffic_key(kernel_desc: str) -> str:
     return f"{parts[1]} {tile}"
 
 
+TRAFFIC_SOURCES = ("gemm_lds.h", "gemm_core.h", "common.h")
+
+
+def gemm_lds_source_digest() -> str:
+    """SHA-256 over the pipelined GEMM kernel's sources, in TRAFFIC_SOURCES order."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2011_11188_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def _traffic_record(kernel_desc: str):
     """HBM bytes per launch of a step kernel measured with rocprofv3 counters
-    (profiles/), used only while the kernel source is unchanged."""
+    (profiles/), used only while the kernel's source (the pipeline, its
+    epilogue and the shared device helpers) is unchanged."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "gemm_lds_kernel_traffic.txt")
-    src = os.path.join(ROOT, "paper_2011_11188_amd", "csrc", "gemm_lds.h")
     if not os.path.exists(path) or "gemm_lds_kernel" not in kernel_desc:
         return None
     sha, recs = None, {}
@@ -462,8 +474,7 @@ def _traffic_record(kernel_desc: str):
         elif ln.startswith("record:"):
             f = [x.strip() for x in ln.split(":", 1)[1].split("|")]
             recs[f[0]] = float(f[-1].split()[-1])
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if sha != digest:
+    if sha != gemm_lds_source_digest():
         return None
     return recs.get(_traffic_key(kernel_desc))
 
