@@ -1,0 +1,94 @@
+"""Host logic of the build script and of bench.py (no GPU): the compiler-output
+filter and spill detection of the build, the benchmark's mirror of the GEMM
+engine's kernel choice for the step's shapes, the HBM-traffic record lookup
+and its source digest, and the one-GPU guard."""
+import importlib.util
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+# the package's build script as a module of its own (importing the package
+# would load the library)
+_spec = importlib.util.spec_from_file_location("mdnn_build_script",
+                                               os.path.join(ROOT, "paper_2011_11188_amd", "build.py"))
+build = importlib.util.module_from_spec(_spec)
+_spec.loader.exec_module(build)
+
+R = build.RESOURCE_REMARK
+
+
+def test_diagnostics_drop_resource_remarks_with_their_context():
+    lines = [
+        "In file included from a.hip:6:",
+        f"k.h:555:1: remark: k: VGPRs: 128 [-Rpass-analysis={R}]",
+        "  555 | kernel(int x) {",
+        "      | ^",
+        "warning: unknown target feature 'packed-fp32-ops'",
+        "In file included from b.hip:2:",
+        "w.h:7:3: warning: unused variable 'q'",
+        "    7 |   int q;",
+        "      |       ^",
+        "",
+    ]
+    assert build._diagnostics(lines) == [
+        "In file included from b.hip:2:", "w.h:7:3: warning: unused variable 'q'", "    7 |   int q;",
+        "      |       ^"]
+
+
+def test_spills_report_only_vector_register_spills():
+    lines = [
+        f"x.hip:1:1: remark: Function Name: kern_a [-Rpass-analysis={R}]",
+        f"x.hip:1:1: remark:     SGPRs Spill: 4 [-Rpass-analysis={R}]",
+        f"x.hip:1:1: remark:     VGPRs Spill: 0 [-Rpass-analysis={R}]",
+        f"x.hip:9:1: remark: Function Name: kern_b [-Rpass-analysis={R}]",
+        f"x.hip:9:1: remark:     VGPRs Spill: 12 [-Rpass-analysis={R}]",
+    ]
+    assert build._spills(lines) == ["kern_b: VGPRs Spill: 12"]
+
+
+@pytest.mark.parametrize("shape,kernel", [
+    (("NN", 4096, 4096, 4096), "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"),
+    (("NN", 4096, 4096, 1024), "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"),
+    (("TN", 1024, 4096, 4096), "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 4 stages)"),
+    (("NN", 4096, 1, 4096), "skinny rows kernel"),
+    (("TN", 4096, 1, 4096), "skinny cols kernel"),
+    (("NT", 4096, 4096, 1), "skinny depth kernel"),
+    (("NN", 100, 136, 100), "gemm_mfma_kernel 64x64"),
+])
+def test_kernel_choice_for_the_step_shapes(shape, kernel):
+    assert bench._kernel_choice(*shape) == kernel
+
+
+def test_traffic_record_matches_committed_profile_and_sources():
+    desc = "gemm_lds_kernel (256x256 direct-to-LDS pipeline), {} f16 -> {}, 3 launches per step"
+    for lay, out in (("NN", "f16"), ("NT", "f16"), ("TN", "f32")):
+        rec = bench._traffic_record(desc.format(lay, out))
+        assert rec is not None and rec > 0, lay
+    assert bench._traffic_record("skinny rows kernel, NN f16 -> f32, 1 launches per step") is None
+
+
+def test_traffic_record_dropped_when_a_kernel_source_changes(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2011_11188_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    for f in bench.TRAFFIC_SOURCES:
+        shutil.copy(os.path.join(ROOT, "paper_2011_11188_amd", "csrc", f), csrc / f)
+    shutil.copytree(os.path.join(ROOT, "profiles"), tmp_path / "profiles")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    desc = "gemm_lds_kernel (256x256 direct-to-LDS pipeline), NN f16 -> f16, 4 launches per step"
+    assert bench._traffic_record(desc) is not None
+    with open(csrc / "gemm_core.h", "a") as fh:   # the epilogue's header, not the pipeline's own
+        fh.write("\n")
+    assert bench._traffic_record(desc) is None
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stdout + r.stderr
