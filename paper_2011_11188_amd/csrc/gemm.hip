@@ -209,6 +209,23 @@ colsum_strip_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols, 
   *(float2*)(partial + blockIdx.y * cols + (int64_t)blockIdx.x * 512 + 2 * threadIdx.x) = t;
 }
 
+// sum of partial[k][c] over k = ln, ln + 8, ... < chunks, in that order,
+// eight loads in flight at a time
+__device__ __forceinline__ float strided_sum8(const float* __restrict__ partial, int64_t chunks, int64_t cols,
+                                              int64_t c, int ln) {
+  float s = 0.0f;
+  int64_t k = ln;
+  for (; k + 56 < chunks; k += 64) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = partial[(k + 8 * u) * cols + c];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; k < chunks; k += 8) s += partial[k * cols + c];
+  return s;
+}
+
 __global__ void __launch_bounds__(256)
 colsum_final_kernel(const float* __restrict__ partial, int64_t chunks, int64_t cols,
                     float* __restrict__ out) {
@@ -216,8 +233,7 @@ colsum_final_kernel(const float* __restrict__ partial, int64_t chunks, int64_t c
   const int cx = threadIdx.x & 31, ln = threadIdx.x >> 5;
   const int64_t c = (int64_t)blockIdx.x * 32 + cx;
   float s = 0.0f;
-  if (c < cols)
-    for (int64_t k = ln; k < chunks; k += 8) s += partial[k * cols + c];
+  if (c < cols) s = strided_sum8(partial, chunks, cols, c, ln);
   red[ln][cx] = s;
   __syncthreads();
   if (ln == 0 && c < cols) {
@@ -238,8 +254,7 @@ colsum_final_batch_kernel(ColsumBatch b, int32_t* __restrict__ nonfinite) {
   const float* __restrict__ partial = b.part[blockIdx.y];
   const int64_t c = (int64_t)blockIdx.x * 32 + cx;
   float s = 0.0f;
-  if (c < cols)
-    for (int64_t k = ln; k < chunks; k += 8) s += partial[k * cols + c];
+  if (c < cols) s = strided_sum8(partial, chunks, cols, c, ln);
   red[ln][cx] = s;
   __syncthreads();
   if (ln == 0 && c < cols) {
