@@ -315,10 +315,77 @@ SplitPlan cols_plan(int64_t M, int64_t K, int mb) {
 
 int cols_mb(int64_t N) { return N <= 4 ? 8 : 2; }
 
+// ---------------------------------------------------------------------------
+// cols with N = 1 (the weight gradient of a one-output head), 16-bit A with
+// M % 512 == 0: D[m] = sum_k A[k][m] B[k] is a column sum of A's rows
+// weighted by B.  Chunks of COLS1_ROWS k; a block reduces one chunk x 512 m,
+// each wave reading whole 1 KB runs of its rows (wave w: k = w, w + 4, ...;
+// eight m per lane), the four waves combined in a fixed order, into
+// partial[chunk][m] for the split reduction's epilogue.
+// ---------------------------------------------------------------------------
+constexpr int64_t COLS1_ROWS = 64;
+
+template <class T>
+__global__ void __launch_bounds__(256)
+skinny_cols1_strip_kernel(const uint16_t* __restrict__ A, int64_t lda, const uint16_t* __restrict__ B, int64_t ldb,
+                          int64_t M, int64_t K, float* __restrict__ partial) {
+  __shared__ float4 red[4][2][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t m0 = (int64_t)blockIdx.x * 512 + lane * 8;
+  const int64_t k0 = (int64_t)blockIdx.y * COLS1_ROWS;
+  const int64_t nk = K - k0 < COLS1_ROWS ? K - k0 : COLS1_ROWS;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  auto fma8 = [&](const uint4& v, float b) {
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = fmaf(to_f<T>((uint16_t)(vw[e >> 1] >> ((e & 1) * 16))), b, s[e]);
+  };
+  const uint16_t* base = A + (k0 + w) * lda + m0;
+  if (nk == COLS1_ROWS) {
+    // a whole chunk: all of this lane's rows (and their weights) are loaded
+    // before any is added
+    constexpr int RPW = COLS1_ROWS / 4;
+    uint4 v[RPW];
+    float bw[RPW];
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      v[u] = *(const uint4*)(base + (int64_t)(4 * u) * lda);
+      bw[u] = to_f<T>(B[(k0 + w + 4 * u) * ldb]);
+    }
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) fma8(v[u], bw[u]);
+  } else {
+    for (int64_t r = w; r < nk; r += 4) fma8(*(const uint4*)(base + (r - w) * lda), to_f<T>(B[(k0 + r) * ldb]));
+  }
+  red[w][0][lane] = make_float4(s[0], s[1], s[2], s[3]);
+  red[w][1][lane] = make_float4(s[4], s[5], s[6], s[7]);
+  __syncthreads();
+  // thread t: m = 2t and 2t + 1 of the block's 512 (lane t / 4's values)
+  const int l = threadIdx.x >> 2, h = (threadIdx.x >> 1) & 1, q = threadIdx.x & 1;
+  float2 t = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float4 v = red[k][h][l];
+    t.x += q ? v.z : v.x;
+    t.y += q ? v.w : v.y;
+  }
+  *(float2*)(partial + blockIdx.y * M + (int64_t)blockIdx.x * 512 + 2 * threadIdx.x) = t;
+}
+
 template <class T, class OutT>
 mdnn_status_t launch_cols(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t M, int64_t N, int64_t K,
                           const Epilogue& ep_in, void* ws, size_t ws_bytes, hipStream_t st) {
   typedef typename T::storage S;
+  if constexpr (sizeof(S) == 2) {
+    const int64_t chunks = ceil_div(K, COLS1_ROWS);
+    if (N == 1 && M % 512 == 0 && K >= 512 && chunks <= 65535 && M / 512 <= 0x7fffffffLL && aligned(A, 16) &&
+        lda % 8 == 0 && ws && aligned(ws, 16) && ws_bytes >= (size_t)chunks * M * sizeof(float)) {
+      hipLaunchKernelGGL(skinny_cols1_strip_kernel<T>, dim3((unsigned)(M / 512), (unsigned)chunks), dim3(256), 0, st,
+                         (const uint16_t*)A, lda, (const uint16_t*)B, ldb, M, K, (float*)ws);
+      MDNN_TRY(check_launch("skinny_cols1_strip_kernel"));
+      return reduce_splits_epilogue(ws, (int)chunks, M, N, ep_in, code_of<T>(), code_of<OutT>(), st);
+    }
+  }
   const int mb = cols_mb(N);
   const SplitPlan plan = cols_plan(M, K, mb);
   Epilogue ep = ep_in;
