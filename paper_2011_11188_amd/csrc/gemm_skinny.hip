@@ -316,6 +316,57 @@ SplitPlan cols_plan(int64_t M, int64_t K, int mb) {
 int cols_mb(int64_t N) { return N <= 4 ? 8 : 2; }
 
 // ---------------------------------------------------------------------------
+// rows with N = 1, 16-bit, both operands k-contiguous and 16-byte aligned (a
+// one-output head's forward product): D[m] = sum_k A[m][k] B[k], one wave per
+// row; each lane loads its 16-byte runs of A and of B together (no staging
+// of B through LDS), a row's runs eight at a time.
+// ---------------------------------------------------------------------------
+template <class T>
+__device__ __forceinline__ void dot8(const uint4& a, const uint4& b, float& acc) {
+  const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    acc = fmaf(to_f<T>((uint16_t)(aw[e >> 1] >> ((e & 1) * 16))), to_f<T>((uint16_t)(bw[e >> 1] >> ((e & 1) * 16))),
+               acc);
+}
+
+template <class T, class OutT>
+__global__ void __launch_bounds__(256)
+skinny_rows1_kernel(const uint16_t* __restrict__ A, int64_t lda, const uint16_t* __restrict__ B, int64_t M, int K,
+                    Epilogue ep) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t m = (int64_t)blockIdx.x * 4 + wave;
+  if (m >= M) return;  // whole waves; the kernel has no barrier
+  const uint16_t* a_row = A + m * lda;
+  float acc = 0.0f;
+  int base = 0;
+  for (; base + 8 * 512 <= K; base += 8 * 512) {
+    uint4 va[8], vb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      va[u] = *(const uint4*)(a_row + base + u * 512 + lane * 8);
+      vb[u] = *(const uint4*)(B + base + u * 512 + lane * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) dot8<T>(va[u], vb[u], acc);
+  }
+  for (; base + 512 <= K; base += 512)
+    dot8<T>(*(const uint4*)(a_row + base + lane * 8), *(const uint4*)(B + base + lane * 8), acc);
+  if (base < K) {
+    const int k0 = base + lane * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (k0 + e < K) acc = fmaf(to_f<T>(a_row[k0 + e]), to_f<T>(B[k0 + e]), acc);
+  }
+  acc = wave_sum64(acc);
+  if (lane == 0) {
+    float r[NMAX] = {};
+    r[0] = acc;
+    store_row<T, OutT>(ep, M, 1, m, r);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // cols with N = 1 (the weight gradient of a one-output head), 16-bit A with
 // M % 512 == 0: D[m] = sum_k A[k][m] B[k] is a column sum of A's rows
 // weighted by B.  Chunks of COLS1_ROWS k; a block reduces one chunk x 512 m,
@@ -435,6 +486,15 @@ mdnn_status_t launch_skinny(mdnn_layout_t layout, const void* A, int64_t lda, co
     return check_launch("skinny_depth_kernel");
   }
   if (layout == MDNN_TN) return launch_cols<T, OutT>(A, lda, B, ldb, M, N, K, ep, ws, ws_bytes, st);
+  if constexpr (sizeof(S) == 2) {
+    // B's one column (NN, ldb = 1) or one row (NT) is k-contiguous
+    if (N == 1 && K >= 512 && aligned(A, 16) && lda % 8 == 0 && aligned(B, 16) && (layout == MDNN_NT || ldb == 1) &&
+        ceil_div(M, 4) <= 0x7fffffffLL) {
+      hipLaunchKernelGGL((skinny_rows1_kernel<T, OutT>), dim3((unsigned)ceil_div(M, 4)), dim3(256), 0, st,
+                         (const uint16_t*)A, lda, (const uint16_t*)B, M, (int)K, ep);
+      return check_launch("skinny_rows1_kernel");
+    }
+  }
   const int kp = (int)ceil_div(K, 8) * 8;
   const size_t lds = (size_t)N * kp * sizeof(float);
   const bool vec = K % 8 == 0 && lda % 8 == 0 && aligned(A, 16);

@@ -25,9 +25,9 @@ pytestmark = pytest.mark.gpu
 LAYOUT = {"NN": 0, "NT": 1, "TN": 2}
 TOL = 1e-4
 SHAPES = {  # layout -> (m, n, k) list
-    "NN": [(4096, 1, 4096), (256, 10, 1024), (64, 10, 128), (77, 16, 301), (5, 3, 40), (300, 2, 17),
+    "NN": [(4096, 1, 4096), (1001, 1, 1000), (256, 10, 1024), (64, 10, 128), (77, 16, 301), (5, 3, 40), (300, 2, 17),
            (129, 4, 700), (333, 50, 3)],
-    "NT": [(256, 10, 1024), (131, 3, 500), (9, 1, 23), (1000, 4096, 1), (70, 33, 10), (64, 128, 4)],
+    "NT": [(256, 10, 1024), (130, 1, 4600), (131, 3, 500), (9, 1, 23), (1000, 4096, 1), (70, 33, 10), (64, 128, 4)],
     "TN": [(4096, 1, 4096), (1536, 1, 1000), (1024, 10, 256), (128, 10, 64), (1001, 3, 300), (37, 16, 1000), (9, 5, 20),
            (700, 9, 16), (500, 64, 2)],
 }
