@@ -409,7 +409,28 @@ reduce_splits_epilogue_kernel(const float* __restrict__ part, int splits, int64_
   float4_t acc = {0.f, 0.f, 0.f, 0.f};
   if (valid) {
     const float* p = part + m * N + n;
-    for (int s = g; s < splits; s += 16) {
+    int s = g;
+    // four of this thread's splits in flight at a time (same order of additions)
+    for (; s + 48 < splits; s += 64) {
+      float4_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float* ps = p + (int64_t)(s + 16 * u) * MN;
+        if (vec) {
+          const float4 t = *(const float4*)ps;
+          v[u] = (float4_t){t.x, t.y, t.z, t.w};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[u][e] = n + e < N ? ps[e] : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (vec || n + e < N) acc[e] += v[u][e];
+    }
+    for (; s < splits; s += 16) {
       const float* ps = p + (int64_t)s * MN;
       if (vec) {
         const float4 v = *(const float4*)ps;
