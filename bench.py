@@ -266,17 +266,17 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
 
 def _replay_group(mdnn, net, cfg, group, reps):
     """Replay the launches of one kernel instantiation exactly as the step
-    issues them (same shapes, leading dimensions, epilogues and buffers);
-    returns (mean ms per launch, mean FLOP per launch)."""
-    import torch
+    issues them (same shapes, leading dimensions, epilogues and buffers),
+    `reps` times; returns (mean ms per launch, mean FLOP per launch)."""
     lp = {"f32": 0, "f16": 1, "bf16": 2}[cfg.dtype]
     es = 2 if lp else 4
     offs = cfg.param_offsets()
     wbase = net.lowp.data_ptr() if net.lowp is not None else net.master.data_ptr()
-    widest = max([cfg.in_features] + [l.c_out for l in cfg.layers])
-    # stand-ins for the step's activation-gradient buffers (same shapes)
-    g0 = torch.empty((cfg.batch, widest), dtype=torch.float16, device="cuda").normal_(0, 1e-2)
-    g1 = torch.empty_like(g0)
+    # the step's own activation-gradient buffers ([batch, widest] each), holding
+    # the last step's gradients: the replayed products see the step's data
+    # (masked, partly zero), which the GPU's power and clock depend on
+    g0, g1 = net.output_grad_ptr(0), net.output_grad_ptr(1)
+    assert g0 and g1
     calls = []
     for (layout, M, N, K, out_t, i) in group:
         l = cfg.layers[i]
@@ -288,23 +288,35 @@ def _replay_group(mdnn, net, cfg, group, reps):
             calls.append((0, M, N, K, a_in, K, wptr, N, a_out, N, 0 if out_t == "f32" else lp,
                           bias, l.act, None, 0))
         elif layout == "TN":
-            calls.append((2, M, N, K, a_in, M, g0.data_ptr(), N, net.grads.data_ptr() + offs[i][0] * 4,
+            calls.append((2, M, N, K, a_in, M, g0, N, net.grads.data_ptr() + offs[i][0] * 4,
                           N, 0, None, 0, None, 0))
         else:
-            calls.append((1, M, N, K, g0.data_ptr(), K, wptr, K, g1.data_ptr(), N, lp, None, 0,
+            calls.append((1, M, N, K, g0, K, wptr, K, g1, N, lp, None, 0,
                           a_in, N))
     flops = sum(2.0 * c[1] * c[2] * c[3] for c in calls) / len(calls)
-    for c in calls:  # warm
-        mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0, None, 0,
-                             c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    # one event pair around `reps` back-to-back replays: launches are queued
-    # ahead of the GPU, so the mean is the kernels' own duration plus the
-    # (microsecond) dispatch gaps between them
-    def replay():
+    # one event pair around each replayed launch (the launches are queued
+    # ahead of the GPU, so each pair brackets that kernel's execution alone,
+    # as a kernel trace reports it, not the gaps between kernels)
+    import torch
+
+    def launch(c):
+        mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
+                             None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
+    for _ in range(3):
         for c in calls:
-            mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
-                                 None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
-    return _measure(replay, min_ms=max(50.0, reps)) / len(calls), flops
+            launch(c)
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(reps * len(calls))]
+    k = 0
+    for _ in range(reps):
+        for c in calls:
+            pairs[k][0].record()
+            launch(c)
+            pairs[k][1].record()
+            k += 1
+    torch.cuda.synchronize()
+    return sum(e0.elapsed_time(e1) for e0, e1 in pairs) / len(pairs), flops
 
 
 def _gemm_sweep(mdnn, reps_scale=1.0):
