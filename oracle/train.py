@@ -138,8 +138,12 @@ class OracleNet:
             loss, dz = ops.mse_loss(out, np.asarray(target, np.float64).reshape(out.shape), scale)
         return loss, self.R(dz)
 
-    def backward(self, acts, args, dz: np.ndarray, wl: Optional[np.ndarray] = None) -> np.ndarray:
-        """Gradient of the loss (times the loss scale) w.r.t. the flat params."""
+    def backward(self, acts, args, dz: np.ndarray, wl: Optional[np.ndarray] = None,
+                 trace: Optional[list] = None) -> np.ndarray:
+        """Gradient of the loss (times the loss scale) w.r.t. the flat params.
+        ``trace``, when given, receives each stored backward-data result (the
+        gradient w.r.t. a layer's input, after the ReLU mask and the storage
+        rounding), last layer first."""
         wl = self.w_lp() if wl is None else wl
         b = self.batch
         g = np.zeros(self.n_params)
@@ -173,6 +177,8 @@ class OracleNet:
                 if self.input_relu[i]:
                     dx = np.where(a_in > 0.0, dx, 0.0)
                 dz = self.R(dx)
+                if trace is not None:
+                    trace.append(dz)
         return g
 
     def step(self, x: np.ndarray, target: np.ndarray) -> float:
