@@ -21,7 +21,7 @@ Also on the same JSON line:
   gemm_fp32_split3  fp32 GEMMs (4096, 8192) through three fp16 MFMA
                 products of the Eq. (1) splits, next to the native fp32 kernel;
   workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step;
-  async_sgd     the same two nets trained asynchronously (section 4.1) by
+  async_sgd     the same two nets trained asynchronously (section 3.1) by
                 several workers on separate streams sharing one parameter
                 vector, samples/s over all workers.
 Every timed region follows sustained untimed load (about a second of the
@@ -408,7 +408,7 @@ def _conv_bench(mdnn, reps=20):
 
 
 def _async_bench(mdnn, steps=40):
-    """Asynchronous SGD (section 4.1): W workers on W streams share one fp32
+    """Asynchronous SGD (section 3.1): W workers on W streams share one fp32
     parameter vector (mdnn_train_step_async), next to the synchronous step of
     the same net; samples/s over all workers' steps."""
     import torch

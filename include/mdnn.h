@@ -319,7 +319,7 @@ mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v3
                               mdnn_dtype_t lp_type, float lr, float momentum,
                               mdnn_scaler_t* scaler, mdnn_stream_t stream);
 
-/* Asynchronous variant (section 4.1: asynchronous SGD with lock-free updates
+/* Asynchronous variant (section 3.1: asynchronous SGD with lock-free updates
  * of a shared parameter vector): the same check and state machine, but the
  * step -lr*v (or -lr*g) is added to w32 with fp32 atomics, so several streams
  * may update one w32 concurrently without losing updates; no working copy is
@@ -396,7 +396,7 @@ mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream);
  * grads holds this step's scaled gradients afterwards. */
 mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
                               float* loss_out, mdnn_stream_t stream);
-/* Asynchronous step (section 4.1): for several nets bound to the same
+/* Asynchronous step (section 3.1): for several nets bound to the same
  * master_w (each with its own grads, momentum, lowp_w, workspace and scaler)
  * stepping concurrently on different streams.  The step first re-derives its
  * working copy from the shared master weights (fp32 nets read them directly),

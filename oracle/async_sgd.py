@@ -1,6 +1,6 @@
 """Asynchronous SGD in the bounded-staleness model (test infrastructure only).
 
-Section 4.1 describes asynchronous SGD: workers compute gradients from the
+Section 3.1 describes asynchronous SGD: workers compute gradients from the
 parameter values they happen to read, while other workers keep updating the
 shared parameters without locks (Hogwild!-style), so each applied gradient
 may be stale.  The execution is non-deterministic; the oracle fixes the

@@ -215,7 +215,7 @@ class Net:
         return StepGraph(mdnn_train_graph_create(self.handle, x, target, out), (self, x, target, out))
 
     def step_async(self, x, target, loss_out=None, stream=None):
-        """Asynchronous step (section 4.1) on a master vector shared with other
+        """Asynchronous step (section 3.1) on a master vector shared with other
         workers: see mdnn_train_step_async."""
         out = self.loss if loss_out is None else loss_out
         mdnn_train_step_async(self.handle, x, target, out, stream)

@@ -1,4 +1,4 @@
-// Implicit-GEMM convolutions (section 3.1's convolution layers, stride 1,
+// Implicit-GEMM convolutions (section 2.1's convolution layers, stride 1,
 // zero padding) on the pipelined mainloop of gemm_lds.h.  The im2col
 // operands are gathered straight into LDS by the convolution loaders; no
 // im2col buffer exists.

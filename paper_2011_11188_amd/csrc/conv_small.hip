@@ -1,4 +1,4 @@
-// Convolutions with a tiny reduction (section 3.1's convolution layers; the
+// Convolutions with a tiny reduction (section 2.1's convolution layers; the
 // first layer of an image network, e.g. one input channel and a 5x5 filter):
 // the GEMM engine would spend almost all of a tile on padding, so these run
 // as direct kernels on the vector ALUs, fp32 accumulation.

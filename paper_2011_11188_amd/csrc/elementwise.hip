@@ -428,7 +428,7 @@ __global__ void sgd_kernel(int64_t n, float* __restrict__ w, const float* __rest
   }
 }
 
-// Asynchronous variant (section 4.1): the step -lr*v (or -lr*g) is added to
+// Asynchronous variant (section 3.1): the step -lr*v (or -lr*g) is added to
 // the shared weights with hardware fp32 atomics, so concurrent updates from
 // other streams are never lost; reads of w by other work may see any mix of
 // old and new values (Hogwild!-style inconsistent reads).

@@ -1,7 +1,7 @@
 // Pipelined GEMM mainloop for gfx950: direct global->LDS loads, swizzled LDS
 // tiles and transposing LDS reads, for section 3.2's D = C + A*B on the CDNA4
 // matrix cores (v_mfma_f32_16x16x32_{f16,bf16}, fp32 accumulation), and for
-// the implicit-GEMM convolutions of section 3.1 (im2col never materialised).
+// the implicit-GEMM convolutions of section 2.1 (im2col never materialised).
 //
 // A block tile is BM x BN x 64 (Tile<>): WM x WN waves, each owning a
 // (BM/WM) x (BN/WN) wave tile of 16 x 16 fragments, accumulators in VGPRs.

@@ -258,7 +258,7 @@ extern "C" const void* mdnn_net_output_grad(const mdnn_net_t* net, int32_t which
 
 extern "C" void mdnn_net_destroy(mdnn_net_t* net) { delete net; }
 
-// One step; `async`: section 4.1's asynchronous variant, for nets that share
+// One step; `async`: section 3.1's asynchronous variant, for nets that share
 // their master weights with other nets stepping concurrently: the working
 // copy is re-derived from the shared weights at the start of the step (an
 // inconsistent snapshot while others update them), and the update is added

@@ -1,4 +1,4 @@
-"""Asynchronous SGD on one GPU (section 4.1): workers on separate streams
+"""Asynchronous SGD on one GPU (section 3.1): workers on separate streams
 share one fp32 parameter vector and add their updates to it with atomics.
 
 The execution is non-deterministic by design, so parity is:

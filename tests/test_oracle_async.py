@@ -1,4 +1,4 @@
-"""Pins of the oracle's asynchronous-SGD model (section 4.1, bounded staleness).
+"""Pins of the oracle's asynchronous-SGD model (section 3.1, bounded staleness).
 
 * Staleness 0 is plain SGD: the model's trajectory equals OracleNet.step's,
   bit for bit.
