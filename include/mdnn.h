@@ -148,12 +148,19 @@ int mdnn_set_gemm_tile(int code);
  * a2 = 2^-11 a1).  x is rows x cols fp32 with leading dimension ldx; hi and lo
  * are fp16 with leading dimensions ldh, ldl (each >= cols).  |x| / s must stay
  * below 65504 (larger values give inf / NaN); values below 2^-14 * s lose bits
- * to fp16 subnormals.  Errors: MDNN_ERR_SHAPE for negative sizes or a scale
- * that is not a positive power of two, MDNN_ERR_NULL, MDNN_ERR_LAYOUT,
- * MDNN_ERR_MISALIGNED (x 4-byte, hi / lo 2-byte aligned).
+ * to fp16 subnormals.
+ * The section gives a1 only for well-scaled data.  scale == 0 asks the
+ * library to choose it on the device: s = 2^(floor(log2 max|x|) - 14), so
+ * that max|x| / s lies in [2^14, 2^15) (s = 1 when max|x| is 0, Inf or NaN;
+ * s >= 2^-126); the chosen s is written to the device fp32 scalar scale_out
+ * (required then, ignored and may be NULL otherwise).  No host read-back.
+ * Errors: MDNN_ERR_SHAPE for negative sizes or a scale that is neither 0 nor
+ * a positive power of two, MDNN_ERR_NULL, MDNN_ERR_LAYOUT,
+ * MDNN_ERR_MISALIGNED (x, scale_out 4-byte, hi / lo 2-byte aligned).
  */
 mdnn_status_t mdnn_split_f16(int64_t rows, int64_t cols, const float* x, int64_t ldx, float scale,
-                             void* hi, int64_t ldh, void* lo, int64_t ldl, mdnn_stream_t stream);
+                             float* scale_out, void* hi, int64_t ldh, void* lo, int64_t ldl,
+                             mdnn_stream_t stream);
 
 /* D = alpha * op(A) op(B) + beta * C for fp32 A, B, C, D through three fp16
  * MFMA products of the Eq. (1) splits of A (scale a_scale) and B (scale
@@ -161,9 +168,12 @@ mdnn_status_t mdnn_split_f16(int64_t rows, int64_t cols, const float* x, int64_t
  * (the A2 B2 product, 2^-22 below the leading one, is dropped).  Layouts,
  * leading dimensions and the beta == 0 rule as mdnn_gemm_mixed; scales are
  * positive powers of two chosen so that |A| / a_scale and |B| / b_scale stay
- * below 65504 (1 for data of moderate magnitude).  The caller provides
+ * below 65504 (1 for data of moderate magnitude), or 0: chosen on the device
+ * by the rule of mdnn_split_f16 (the products' epilogues then read a_scale *
+ * b_scale from the workspace; no host read-back).  The caller provides
  * mdnn_gemm_split3_workspace(M, N, K) bytes of 256-byte aligned device
- * workspace (the split operands and one fp32 M x N product); C may alias D.
+ * workspace (the split operands, one fp32 M x N product and the scales);
+ * C may alias D.
  * Four or more launches on `stream`, no host synchronisation.
  */
 size_t mdnn_gemm_split3_workspace(int64_t M, int64_t N, int64_t K);
@@ -301,7 +311,12 @@ mdnn_status_t mdnn_mse_loss(int64_t B, int64_t O, const float* y, const float* t
  * The scaler lives in device memory; its overflow field is written by the
  * call (1 when the step was skipped).  With a scaler the call enqueues three
  * kernels (finite check, update, scaler state update), otherwise one.
- * w32 and g32 must be 16-byte aligned.
+ * Pointers need only their element alignment (fp32: 4 bytes); when w32, g32,
+ * v32 are 16-byte aligned and w_lp 4-element aligned the passes use 16-byte
+ * vectors, otherwise one element per thread (same arithmetic).
+ * Errors: MDNN_ERR_SHAPE (n < 0), MDNN_ERR_DTYPE, MDNN_ERR_NULL (w32 / g32
+ * missing with n > 0), MDNN_ERR_MISALIGNED (a pointer below its element
+ * alignment), MDNN_ERR_LAUNCH.
  * ------------------------------------------------------------------------- */
 typedef struct {
   float scale;
@@ -325,7 +340,7 @@ mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v3
  * may update one w32 concurrently without losing updates; no working copy is
  * written.  The order of concurrent updates (hence the rounding of w32) is
  * not deterministic.  v32 and the scaler belong to the caller of this update
- * (one per worker).  g32 16-byte aligned when a scaler is given. */
+ * (one per worker).  Pointers need only 4-byte alignment. */
 mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const float* g32, float* v32, float lr,
                                     float momentum, mdnn_scaler_t* scaler, mdnn_stream_t stream);
 
@@ -379,7 +394,11 @@ mdnn_status_t mdnn_net_sizes(const mdnn_net_t* net, int64_t* n_params, size_t* w
  * caller), grads fp32[n_params], momentum fp32[n_params] (NULL iff momentum
  * is 0; caller zeroes it), lowp_w cfg.dtype[n_params] (NULL for fp32 nets;
  * filled by mdnn_net_sync_lowp), workspace (>= workspace_bytes, 256-byte
- * aligned), scaler (NULL iff loss scaling is off; caller initialises it). */
+ * aligned), scaler (NULL iff loss scaling is off; caller initialises it).
+ * The parameter buffers need only their element alignment (4 bytes; lowp_w
+ * 2 bytes); each kernel of the step picks its vector or element-wise form
+ * from the alignment it is given.  MDNN_ERR_MISALIGNED otherwise, or for a
+ * workspace that is not 256-byte aligned. */
 mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* grads, float* momentum,
                             void* lowp_w, void* workspace, size_t workspace_bytes,
                             mdnn_scaler_t* scaler);

@@ -86,7 +86,7 @@ _SIGS = {
     "mdnn_cast": [_i64, _vp, _i, _vp, _i, _vp],
     "mdnn_sgd_update_async": [_i64, _vp, _vp, _vp, _f, _f, _vp, _vp],
     "mdnn_train_step_async": [_vp, _vp, _vp, _vp, _vp],
-    "mdnn_split_f16": [_i64, _i64, _vp, _i64, _f, _vp, _i64, _vp, _i64, _vp],
+    "mdnn_split_f16": [_i64, _i64, _vp, _i64, _f, _vp, _vp, _i64, _vp, _i64, _vp],
     "mdnn_gemm_split3": [_i, _i64, _i64, _i64, _f, _vp, _i64, _f, _vp, _i64, _f, _f, _vp, _i64, _vp,
                          _i64, _vp, C.c_size_t, _vp],
     "mdnn_net_create": [_vp, C.c_int32, _i64, _vp, _vp],
@@ -283,8 +283,9 @@ def mdnn_train_step_async(net, x, target, loss_out, stream=None):
     return _call("mdnn_train_step_async", net, _p(x), _p(target), _p(loss_out), _s(stream))
 
 
-def mdnn_split_f16(rows, cols, x, ldx, scale, hi, ldh, lo, ldl, stream=None):
-    return _call("mdnn_split_f16", rows, cols, _p(x), ldx, scale, _p(hi), ldh, _p(lo), ldl, _s(stream))
+def mdnn_split_f16(rows, cols, x, ldx, scale, scale_out, hi, ldh, lo, ldl, stream=None):
+    return _call("mdnn_split_f16", rows, cols, _p(x), ldx, scale, _p(scale_out), _p(hi), ldh, _p(lo), ldl,
+                 _s(stream))
 
 
 def mdnn_gemm_split3_workspace(M, N, K) -> int:

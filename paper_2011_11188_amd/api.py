@@ -17,7 +17,7 @@ from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, L
                mdnn_graph_launch, mdnn_graph_destroy, mdnn_conv2d_fwd_winograd,
                mdnn_conv2d_fwd_winograd_workspace)
 
-__all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "pow2_scale", "conv_shape", "conv2d_fwd",
+__all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "conv_shape", "conv2d_fwd",
            "conv2d_fwd_winograd", "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net", "StepGraph"]
 
 
@@ -56,19 +56,25 @@ def gemm(layout: int, A, B, out_dtype=None, bias=None, act: int = ACT_NONE, mask
     return out
 
 
-def split_f16(x, scale: float = 1.0, stream=None):
-    """(hi, lo) fp16 tensors of the two-term split of a 2-D fp32 tensor."""
+def split_f16(x, scale: float = 1.0, stream=None, scale_out=None):
+    """(hi, lo) fp16 tensors of the two-term split of a 2-D fp32 tensor.
+    scale 0 lets the library choose the power of two on the device; it is
+    written to ``scale_out`` (a one-element fp32 device tensor, allocated when
+    not given, returned as the third value)."""
     import torch
     rows, cols = x.shape
     hi = torch.empty((rows, cols), dtype=torch.float16, device=x.device)
     lo = torch.empty_like(hi)
-    mdnn_split_f16(rows, cols, x, x.stride(0), scale, hi, cols, lo, cols, stream)
-    return hi, lo
+    if scale == 0.0 and scale_out is None:
+        scale_out = torch.empty((1,), dtype=torch.float32, device=x.device)
+    mdnn_split_f16(rows, cols, x, x.stride(0), scale, scale_out, hi, cols, lo, cols, stream)
+    return (hi, lo, scale_out) if scale == 0.0 else (hi, lo)
 
 
 def gemm_split3(layout: int, A, B, a_scale: float = 1.0, b_scale: float = 1.0, alpha: float = 1.0,
                 beta: float = 0.0, Cm=None, out=None, stream=None):
-    """fp32 D = alpha op(A) op(B) + beta C through three fp16 MFMA products."""
+    """fp32 D = alpha op(A) op(B) + beta C through three fp16 MFMA products
+    (a scale of 0: chosen on the device from the operand's largest magnitude)."""
     import torch
     if layout == TN:
         K, M = A.shape
@@ -82,17 +88,6 @@ def gemm_split3(layout: int, A, B, a_scale: float = 1.0, b_scale: float = 1.0, a
     mdnn_gemm_split3(layout, M, N, K, alpha, A, A.stride(0), a_scale, B, B.stride(0), b_scale, beta, Cm,
                      Cm.stride(0) if Cm is not None else 0, out, out.stride(0), ws, ws_bytes, stream)
     return out
-
-
-def pow2_scale(x) -> float:
-    """A power-of-two split scale that puts max|x| in [2^14, 2^15): convenience
-    for callers whose data is not of moderate magnitude (reads max|x| back to
-    the host)."""
-    import math
-    m = float(x.abs().max().item()) if x.numel() else 0.0
-    if not math.isfinite(m) or m == 0.0:
-        return 1.0
-    return 2.0 ** (math.floor(math.log2(m)) - 14)
 
 
 def conv_shape(x_shape: Sequence[int], c_out: int, r: int, s: int, pad: int) -> ConvShape:

@@ -536,12 +536,27 @@ __global__ void sgd_vec_kernel(int64_t n, float* __restrict__ w, const float* __
   }
 }
 
+// scaler->reserved |= any non-finite g[0..n): 16-byte vectors when g allows,
+// else the element-wise ranged pass over one range
+static mdnn_status_t finite_check_all(const float* g32, int64_t n, mdnn_scaler_t* scaler, hipStream_t st) {
+  if (aligned(g32, 16)) {
+    const unsigned g = stream_grid(ceil_div(n, 4));
+    hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);
+    return check_launch("finite_check_kernel");
+  }
+  CheckRanges r{};
+  r.n = 1;
+  r.off[0] = 0;
+  r.len[0] = n;
+  return finite_check_ranges(g32, r, scaler, st);
+}
+
 template <class LpT, bool MOM, bool SCALE>
 static void sgd_launch_t(int64_t n, float* w, const float* g, float* v, void* wlp, float lr, float mu,
                          const mdnn_scaler_t* sc, hipStream_t st) {
   typedef typename LpT::storage L;
-  // w and g are 16-byte aligned (checked by the entry point)
-  const bool vec = (!v || aligned(v, 16)) && (!wlp || aligned(wlp, 4 * sizeof(L)));
+  // 16-byte vectors when every buffer allows them, else one element per thread
+  const bool vec = aligned(w, 16) && aligned(g, 16) && (!v || aligned(v, 16)) && (!wlp || aligned(wlp, 4 * sizeof(L)));
   const unsigned grid = stream_grid(vec ? ceil_div(n, 4) : n);
   if (vec)
     hipLaunchKernelGGL((sgd_vec_kernel<LpT, MOM, SCALE>), dim3(grid), dim3(256), 0, st, n, w, g, v, (L*)wlp, lr, mu,
@@ -764,15 +779,9 @@ extern "C" mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const floa
   if ((w32 && !aligned(w32, 4)) || (g32 && !aligned(g32, 4)) || (v32 && !aligned(v32, 4)) ||
       (scaler && !aligned(scaler, 4)))
     return fail(MDNN_ERR_MISALIGNED, "sgd_update_async: misaligned pointer");
-  if (scaler && n > 0 && !aligned(g32, 16))
-    return fail(MDNN_ERR_MISALIGNED, "sgd_update_async: g32 needs 16-byte alignment with a scaler");
   clear_error();
   hipStream_t st = as_stream(stream);
-  if (scaler && n > 0) {
-    const unsigned g = stream_grid(ceil_div(n, 4));
-    hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);
-    MDNN_TRY(check_launch("finite_check_kernel"));
-  }
+  if (scaler && n > 0) MDNN_TRY(finite_check_all(g32, n, scaler, st));
   if (n > 0) {
     const unsigned g = stream_grid(n);
     const bool mom = v32 != nullptr, sc = scaler != nullptr;
@@ -829,16 +838,12 @@ static mdnn_status_t sgd_update_impl(int64_t n, float* w32, const float* g32, fl
   if (n < 0) return fail(MDNN_ERR_SHAPE, "sgd_update: n < 0");
   if (!dtype_ok(lp_type)) return fail(MDNN_ERR_DTYPE, "sgd_update: unknown lp_type");
   if (n > 0 && (!w32 || !g32)) return fail(MDNN_ERR_NULL, "sgd_update: w32 and g32 are required");
-  if ((w32 && !aligned(w32, 16)) || (g32 && !aligned(g32, 16)) || (v32 && !aligned(v32, 4)) ||
+  if ((w32 && !aligned(w32, 4)) || (g32 && !aligned(g32, 4)) || (v32 && !aligned(v32, 4)) ||
       (w_lp && !aligned(w_lp, dtype_size(lp_type))) || (scaler && !aligned(scaler, 4)))
-    return fail(MDNN_ERR_MISALIGNED, "sgd_update: w32/g32 need 16-byte alignment");
+    return fail(MDNN_ERR_MISALIGNED, "sgd_update: a pointer is not aligned to its element size");
   clear_error();
   hipStream_t st = as_stream(stream);
-  if (check && scaler && n > 0) {
-    const unsigned g = stream_grid(ceil_div(n, 4));
-    hipLaunchKernelGGL(finite_check_kernel, dim3(g), dim3(256), 0, st, g32, n, scaler);
-    MDNN_TRY(check_launch("finite_check_kernel"));
-  }
+  if (check && scaler && n > 0) MDNN_TRY(finite_check_all(g32, n, scaler, st));
   if (n > 0) {
     switch (lp_type) {
       case MDNN_F32: sgd_launch<F32>(n, w32, g32, v32, w_lp, lr, momentum, scaler, st); break;

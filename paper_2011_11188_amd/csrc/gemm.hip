@@ -630,7 +630,7 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
                                   float beta, const void* C, int64_t ldc, void* D, int64_t ldd,
                                   mdnn_dtype_t d_type, const float* bias, mdnn_act_t act, const void* mask_src,
                                   int64_t ldm, void* ws, size_t ws_bytes, mdnn_stream_t stream,
-                                  int32_t* nonfinite) {
+                                  int32_t* nonfinite, const float* alpha_dev) {
   if (layout != MDNN_NN && layout != MDNN_NT && layout != MDNN_TN)
     return fail(MDNN_ERR_LAYOUT, "gemm: unknown layout %d", (int)layout);
   if (M < 0 || N < 0 || K < 0) return fail(MDNN_ERR_SHAPE, "gemm: negative size");
@@ -675,6 +675,7 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
   ep.partial = nullptr;
   ep.k_per_split = K;
   ep.nonfinite = nonfinite;
+  ep.alpha_dev = alpha_dev;
   hipStream_t st = as_stream(stream);
   clear_error();
 

@@ -304,6 +304,7 @@ struct Epilogue {
   int64_t k_per_split; // multiple of GEMM_BK
   int64_t bstride_d;   // batched products (grid z): elements of D between batch entries
   int32_t* nonfinite;  // fp32 D only: set to 1 (atomic OR) when a stored value is not finite; or null
+  const float* alpha_dev;  // device scalar multiplied into alpha (scales chosen on the device), or null
 };
 
 // Batched products: grid z selects one matrix of a batch of plain matrices
@@ -350,9 +351,10 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
   float v[4] = {acc[0], acc[1], acc[2], acc[3]};
   const bool in4 = FULL || n + 4 <= N;
   const bool full = FULL || (ep.vec4 && in4);
+  const float alpha = ep.alpha_dev ? ep.alpha * *ep.alpha_dev : ep.alpha;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    v[e] *= ep.alpha;
+    v[e] *= alpha;
   }
   if (ep.beta != 0.0f) {
     const typename OutT::storage* c = (const typename OutT::storage*)ep.C + m * ep.ldc + n;

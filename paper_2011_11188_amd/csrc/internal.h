@@ -80,7 +80,8 @@ mdnn_status_t gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t 
                             int64_t lda, const void* B, int64_t ldb, mdnn_dtype_t ab_type, float beta,
                             const void* C, int64_t ldc, void* D, int64_t ldd, mdnn_dtype_t d_type,
                             const float* bias, mdnn_act_t act, const void* mask_src, int64_t ldm, void* ws,
-                            size_t ws_bytes, mdnn_stream_t stream, int32_t* nonfinite = nullptr);
+                            size_t ws_bytes, mdnn_stream_t stream, int32_t* nonfinite = nullptr,
+                            const float* alpha_dev = nullptr);
 
 // Loss-scaled updates whose gradients were checked where they were produced:
 // gemm_mixed_ws with `nonfinite` = &scaler->reserved covers every fp32 value

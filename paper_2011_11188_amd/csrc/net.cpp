@@ -224,9 +224,10 @@ extern "C" mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* 
   if (net->lp != MDNN_F32 && !lowp_w) return fail(MDNN_ERR_NULL, "net_bind: lowp_w required for a low-precision net");
   if (net->cfg.loss_scaling && !scaler) return fail(MDNN_ERR_NULL, "net_bind: scaler required with loss scaling");
   if (workspace_bytes < net->ws_bytes) return fail(MDNN_ERR_WORKSPACE, "net_bind: workspace needs %zu bytes", net->ws_bytes);
-  if (!aligned(workspace, 256) || !aligned(master_w, 16) || !aligned(grads, 16) ||
-      (momentum && !aligned(momentum, 4)) || (lowp_w && !aligned(lowp_w, 16)) || (scaler && !aligned(scaler, 4)))
-    return fail(MDNN_ERR_MISALIGNED, "net_bind: workspace must be 256-byte and parameter buffers 16-byte aligned");
+  if (!aligned(workspace, 256) || !aligned(master_w, 4) || !aligned(grads, 4) || (momentum && !aligned(momentum, 4)) ||
+      (lowp_w && !aligned(lowp_w, dtype_size(net->lp))) || (scaler && !aligned(scaler, 4)))
+    return fail(MDNN_ERR_MISALIGNED,
+                "net_bind: workspace must be 256-byte aligned and parameter buffers aligned to their element size");
   net->master = master_w;
   net->grads = grads;
   net->mom = net->cfg.momentum != 0.0f ? momentum : nullptr;

@@ -119,8 +119,11 @@ def test_other_entry_points_reject_bad_arguments(m):
     with pytest.raises(m.MdnnError) as e:
         m.mdnn_softmax_xent(4, 10, FAKE, 8, FAKE, None, FAKE, FAKE, 10, 0, stream=0)
     assert e.value.status == m.ERR_LAYOUT
+    with pytest.raises(m.MdnnError) as e:   # below fp32's element alignment (4-byte alignment is accepted)
+        m.mdnn_sgd_update(10, FAKE + 2, FAKE, None, None, 0, 0.1, 0.0, None, stream=0)
+    assert e.value.status == m.ERR_MISALIGNED
     with pytest.raises(m.MdnnError) as e:
-        m.mdnn_sgd_update(10, FAKE + 4, FAKE, None, None, 0, 0.1, 0.0, None, stream=0)
+        m.mdnn_sgd_update(10, FAKE, FAKE + 6, None, None, 0, 0.1, 0.0, None, stream=0)
     assert e.value.status == m.ERR_MISALIGNED
     with pytest.raises(m.MdnnError) as e:
         m.mdnn_bias_act_bwd(4, 4, FAKE, None, 1, None, FAKE, 1, stream=0)   # ReLU needs y
@@ -157,13 +160,22 @@ def test_gemm_workspace_plan(m):
 
 def test_split_entry_points_reject_bad_arguments(m):
     with pytest.raises(m.MdnnError) as e:                    # scale not a power of two
-        m.mdnn_split_f16(4, 4, FAKE, 4, 3.0, FAKE, 4, FAKE, 4, stream=0)
+        m.mdnn_split_f16(4, 4, FAKE, 4, 3.0, None, FAKE, 4, FAKE, 4, stream=0)
     assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:                    # negative scale
+        m.mdnn_split_f16(4, 4, FAKE, 4, -2.0, None, FAKE, 4, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+    with pytest.raises(m.MdnnError) as e:                    # scale 0 (chosen on the device) needs scale_out
+        m.mdnn_split_f16(4, 4, FAKE, 4, 0.0, None, FAKE, 4, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_NULL
+    with pytest.raises(m.MdnnError) as e:                    # misaligned scale_out
+        m.mdnn_split_f16(4, 4, FAKE, 4, 0.0, FAKE + 2, FAKE, 4, FAKE, 4, stream=0)
+    assert e.value.status == m.ERR_MISALIGNED
     with pytest.raises(m.MdnnError) as e:                    # ldh < cols
-        m.mdnn_split_f16(4, 4, FAKE, 4, 1.0, FAKE, 2, FAKE, 4, stream=0)
+        m.mdnn_split_f16(4, 4, FAKE, 4, 1.0, None, FAKE, 2, FAKE, 4, stream=0)
     assert e.value.status == m.ERR_LAYOUT
     with pytest.raises(m.MdnnError) as e:                    # misaligned x
-        m.mdnn_split_f16(4, 4, FAKE + 2, 4, 1.0, FAKE, 4, FAKE, 4, stream=0)
+        m.mdnn_split_f16(4, 4, FAKE + 2, 4, 1.0, None, FAKE, 4, FAKE, 4, stream=0)
     assert e.value.status == m.ERR_MISALIGNED
     need = m.mdnn_gemm_split3_workspace(64, 32, 16)
     assert need >= 2 * 64 * 16 * 2 + 2 * 16 * 32 * 2 + 64 * 32 * 4

@@ -77,19 +77,61 @@ def test_gemm_split3_against_oracle(mdnn, layout):
         assert np.max(np.abs(got - exact)) * 64 < err16
 
 
-def test_gemm_split3_alpha_beta_scales_and_aliasing(mdnn):
+def _auto_scale(x):
+    """The header's rule for a scale chosen on the device: 2^(floor(log2
+    max|x|) - 14), 1 for a zero or non-finite maximum, at least 2^-126."""
+    mx = float(np.max(np.abs(x.astype(np.float64)))) if x.size else 0.0
+    if mx == 0.0 or not np.isfinite(mx):
+        return 1.0
+    return 2.0 ** max(int(np.floor(np.log2(mx))) - 14, -126)
+
+
+@pytest.mark.parametrize("case", ["large", "small", "subnormal", "zeros", "inf", "nan", "ragged"])
+def test_split_scale_chosen_on_device(mdnn, case):
+    """scale 0: the library picks the power of two from max|x| on the device
+    and writes it out; the split is then bit-exact at that scale."""
+    import torch
+    rows, cols = (37, 129) if case == "ragged" else (64, 200)
+    x = {"large": lambda: _fp32((rows, cols), 23, 1, 18, 22),
+         "small": lambda: _fp32((rows, cols), 23, 2, -30, -26),
+         "subnormal": lambda: _fp32((rows, cols), 23, 3, -140, -130),
+         "zeros": lambda: np.zeros((rows, cols), np.float32),
+         "inf": lambda: _fp32((rows, cols), 23, 4),
+         "nan": lambda: _fp32((rows, cols), 23, 5),
+         "ragged": lambda: _fp32((rows, cols), 23, 6, -3, 9)}[case]()
+    if case == "inf":
+        x[5, 7] = np.inf
+    if case == "nan":
+        x[rows - 1, cols - 1] = np.nan
+    want = _auto_scale(x)
+    assert {"large": 2.0 ** 7, "small": 2.0 ** -41, "zeros": 1.0, "inf": 1.0, "nan": 1.0,
+            "subnormal": 2.0 ** -126}.get(case, want) == want
+    hi, lo, s = mdnn.split_f16(dev(x, "f32"), 0.0)
+    torch.cuda.synchronize()
+    assert float(s.item()) == want
+    h, l = ops.split_f16(x.astype(np.float64), want)
+    fin = np.isfinite(x)
+    assert np.array_equal(host64(hi)[fin], h[fin]) and np.array_equal(host64(lo)[fin], l[fin])
+
+
+@pytest.mark.parametrize("auto", [False, True])
+def test_gemm_split3_alpha_beta_scales_and_aliasing(mdnn, auto):
     """alpha / beta with C aliasing D, power-of-two scales that bring data of
-    large and small magnitude into fp16's range, and K = 0."""
+    large and small magnitude into fp16's range (given, or chosen on the
+    device), and K = 0."""
     import torch
     m, n, k = 200, 136, 320
     a = _fp32((m, k), 40, 1, 18, 22)                    # |a| ~ 2^18 .. 2^22: beyond fp16
     b = _fp32((k, n), 40, 2, -30, -26)                  # |b| ~ 2^-30: below fp16's normals
     c = _fp32((m, n), 40, 3)
     A, B = dev(a, "f32"), dev(b, "f32")
-    sa, sb = mdnn.pow2_scale(A), mdnn.pow2_scale(B)
+    sa, sb = _auto_scale(a), _auto_scale(b)
     assert sa == 2.0 ** 7 and sb == 2.0 ** -41
     D = dev(c, "f32")
-    mdnn.gemm_split3(mdnn.NN, A, B, sa, sb, alpha=0.75, beta=-1.5, Cm=D, out=D)
+    if auto:
+        mdnn.gemm_split3(mdnn.NN, A, B, 0.0, 0.0, alpha=0.75, beta=-1.5, Cm=D, out=D)
+    else:
+        mdnn.gemm_split3(mdnn.NN, A, B, sa, sb, alpha=0.75, beta=-1.5, Cm=D, out=D)
     torch.cuda.synchronize()
     a64, b64, c64 = a.astype(np.float64), b.astype(np.float64), c.astype(np.float64)
     absprod = ops.gemm("NN", np.abs(a64), np.abs(b64))
