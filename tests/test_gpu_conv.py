@@ -310,6 +310,28 @@ def test_resnet_layers_full_size(mdnn, layer):
     assert norm_max_err(host64(db), dy64.sum(axis=(0, 1, 2))) <= TOL
 
 
+@pytest.mark.parametrize("layer", range(3))
+def test_resnet_layers_full_size_fp16_out(mdnn, layer):
+    """The same layers with fp16 outputs, the instantiations the benchmark
+    times: each stored value is the fp16 rounding of a value within the fp32
+    accumulation bound of the exact convolution (one fp16 rounding alone
+    exceeds 1e-4 of the maximum, so the bar is one ulp plus that bound)."""
+    import torch
+    sh = W.RESNET_LAYERS[layer]
+    x, wt, dy = W.conv_operands(sh)
+    X, Wt, DY = dev(x, "f16"), dev(wt, "f16"), dev(dy, "f16")
+    y = mdnn.conv2d_fwd(X, Wt, sh.pad)
+    dx = mdnn.conv2d_bwd_data(DY, Wt, sh.pad, sh.h, sh.w)
+    torch.cuda.synchronize()
+    assert y.dtype == torch.float16 and dx.dtype == torch.float16
+    x64, w64, dy64 = x.astype(np.float64), wt.astype(np.float64), dy.astype(np.float64)
+    kk = sh.r * sh.s * sh.c_in
+    err = accum_bound(ops.conv2d_fwd(np.abs(x64), np.abs(w64), sh.pad), kk)
+    assert lowp_close(host64(y), ops.conv2d_fwd(x64, w64, sh.pad), "f16", err)
+    err = accum_bound(ops.conv2d_bwd_data(np.abs(dy64), np.abs(w64), sh.pad, sh.h, sh.w), kk)
+    assert lowp_close(host64(dx), ops.conv2d_bwd_data(dy64, w64, sh.pad, sh.h, sh.w), "f16", err)
+
+
 @pytest.mark.parametrize("which", ["conv1", "conv2"])
 def test_lenet_conv_layers(mdnn, which):
     """LeNet-style convolutions at batch 256 in bf16 (conv1: Cin = 1, the

@@ -223,6 +223,8 @@ def test_gemm_fp32_path(mdnn, mnk):
         # fp32 inputs: each product rounds too, gamma_{k+1} covers it
         err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)) + np.abs(bias), k + 1)
         assert np.all(np.abs(got - want) <= err)
+        # and the per-output parity metric of fp32 results
+        assert norm_max_err(got, want) <= 1e-4, layout
 
 
 def test_gemm_fp32_k_groups_integer_exact(mdnn):

