@@ -221,6 +221,26 @@ mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void*
                                      mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
                                      size_t ws_bytes, mdnn_stream_t stream);
 
+/* mdnn_conv2d_bwd_filter for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc): the same computation and result, with the workspace taken
+ * from one fixed array in device memory per GPU instead of a caller buffer.
+ * The array holds mdnn_conv2d_bwd_filter_noalloc_max_workspace() bytes
+ * (48 MiB; every GPU the library runs on keeps it until the process ends);
+ * a shape whose mdnn_conv2d_bwd_filter_workspace() exceeds that returns
+ * MDNN_ERR_WORKSPACE before anything runs.  The call allocates nothing: no
+ * hipMalloc, hipFree or allocating library routine.  It runs on the current
+ * device's array (stream must belong to the current device).  Every call on
+ * one GPU shares that GPU's array and leaves its contents behind: calls that
+ * overlap on one GPU (other streams, other host threads) race and must be
+ * serialised by the caller.  Nothing in the array needs to start at zero
+ * (every partial sum the reduction reads is written first by the same call).
+ * Other arguments and errors as mdnn_conv2d_bwd_filter. */
+size_t mdnn_conv2d_bwd_filter_noalloc_max_workspace(void);
+mdnn_status_t mdnn_conv2d_bwd_filter_noalloc(const mdnn_conv_shape_t* shape, const void* x, const void* dy,
+                                             mdnn_dtype_t io_type, float* dw, float* db,
+                                             mdnn_stream_t stream);
+
 /* Alternative forward algorithm for 3x3 filters (section 2.1: the
  * convolution algorithm is swappable per layer): Winograd minimal filtering
  * F(2x2, 3x3) (Lavin and Gray).  Same operands, output, bias and activation

@@ -75,6 +75,7 @@ _SIGS = {
     "mdnn_conv2d_fwd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp],
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
+    "mdnn_conv2d_bwd_filter_noalloc": [_vp, _vp, _vp, _i, _vp, _vp, _vp],
     "mdnn_conv2d_fwd_winograd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp, C.c_size_t, _vp],
     "mdnn_bias_act_fwd": [_i64, _i64, _vp, _vp, _i, _vp, _i, _vp],
     "mdnn_bias_act_bwd": [_i64, _i64, _vp, _vp, _i, _vp, _vp, _i, _vp, C.c_size_t, _vp],
@@ -103,6 +104,8 @@ for _name, _args in _SIGS.items():
     _fn.restype = C.c_int
 _lib.mdnn_conv2d_bwd_filter_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_bwd_filter_workspace.restype = C.c_size_t
+_lib.mdnn_conv2d_bwd_filter_noalloc_max_workspace.argtypes = []
+_lib.mdnn_conv2d_bwd_filter_noalloc_max_workspace.restype = C.c_size_t
 _lib.mdnn_conv2d_fwd_winograd_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_fwd_winograd_workspace.restype = C.c_size_t
 _lib.mdnn_gemm_workspace.argtypes = [_i, _i64, _i64, _i64]
@@ -169,6 +172,7 @@ def last_error() -> str:
 
 def exported_symbols():
     return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
+                                 "mdnn_conv2d_bwd_filter_noalloc_max_workspace",
                                  "mdnn_gemm_split3_workspace", "mdnn_gemm_workspace",
                                  "mdnn_conv2d_fwd_winograd_workspace",
                                  "mdnn_last_error",
@@ -230,6 +234,15 @@ def mdnn_conv2d_bwd_filter(shape: ConvShape, x, dy, io_type, dw, db, workspace, 
                            stream=None):
     return _call("mdnn_conv2d_bwd_filter", _p(shape), _p(x), _p(dy), io_type, _p(dw), _p(db),
                  _p(workspace), ws_bytes, _s(stream))
+
+
+def mdnn_conv2d_bwd_filter_noalloc_max_workspace() -> int:
+    return _lib.mdnn_conv2d_bwd_filter_noalloc_max_workspace()
+
+
+def mdnn_conv2d_bwd_filter_noalloc(shape: ConvShape, x, dy, io_type, dw, db, stream=None):
+    return _call("mdnn_conv2d_bwd_filter_noalloc", _p(shape), _p(x), _p(dy), io_type, _p(dw), _p(db),
+                 _s(stream))
 
 
 def mdnn_bias_act_fwd(rows, cols, x, bias, act, y, y_type, stream=None):

@@ -3,6 +3,8 @@
 //   bwd_data:   M = n*h*w,   N = c_in,  K = r*s*c_out  (A = im2col of dy with flipped taps, B = w)
 //   bwd_filter: M = c_out,   N = r*s*c_in, K = n*Ho*Wo (A = dy^T, B = shifted x), split over K
 // No im2col buffer is materialised: the operand sources compute addresses.
+#include <mutex>
+
 #include "conv_pipe.h"
 #include "conv_small.h"
 #include "gemm_launch.h"
@@ -193,6 +195,56 @@ extern "C" size_t mdnn_conv2d_bwd_filter_workspace(const mdnn_conv_shape_t* shap
   ConvGeom g;
   if (check_conv_shape(shape, g) != MDNN_SUCCESS || !dtype_ok(io_type)) return 0;
   return filter_ws_split_bytes(g) + column_sums_ws_bytes((int64_t)g.n * g.ho * g.wo, g.k);
+}
+
+// Workspace of mdnn_conv2d_bwd_filter_noalloc: one fixed array per GPU, held
+// until the process ends.  Host code never passes the array's name to a
+// kernel or a copy (in host code it is not a device address): it uses the
+// address hipGetSymbolAddress returns for the current device, looked up on
+// the entry point's first call on that device.
+constexpr size_t kNoAllocScratchBytes = (size_t)48 << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+mdnn_status_t scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(MDNN_ERR_LAUNCH, "bwd_filter_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MDNN_ERR_LAUNCH, "bwd_filter_noalloc: device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(MDNN_ERR_LAUNCH, "bwd_filter_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return MDNN_SUCCESS;
+}
+}  // namespace
+
+extern "C" size_t mdnn_conv2d_bwd_filter_noalloc_max_workspace(void) { return kNoAllocScratchBytes; }
+
+extern "C" mdnn_status_t mdnn_conv2d_bwd_filter_noalloc(const mdnn_conv_shape_t* shape, const void* x,
+                                                        const void* dy, mdnn_dtype_t io_type, float* dw,
+                                                        float* db, mdnn_stream_t stream) {
+  ConvGeom g;
+  MDNN_TRY(check_conv_shape(shape, g));
+  if (!dtype_ok(io_type)) return fail(MDNN_ERR_DTYPE, "conv bwd_filter_noalloc: unknown io_type");
+  const size_t need = mdnn_conv2d_bwd_filter_workspace(shape, io_type);
+  if (need > kNoAllocScratchBytes)
+    return fail(MDNN_ERR_WORKSPACE,
+                "conv bwd_filter_noalloc: this shape needs %zu bytes of workspace, above the fixed %zu; "
+                "use mdnn_conv2d_bwd_filter with a caller workspace",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) MDNN_TRY(scratch_of_current_device(&ws));
+  return mdnn_conv2d_bwd_filter(shape, x, dy, io_type, dw, db, ws, need, stream);
 }
 
 extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x,

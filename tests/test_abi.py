@@ -158,6 +158,21 @@ def test_gemm_workspace_plan(m):
     assert e.value.status == m.ERR_MISALIGNED
 
 
+def test_noalloc_bwd_filter_rejects_shapes_beyond_its_array(m):
+    """The filter gradient without a caller workspace takes at most the fixed
+    48 MiB per GPU; a larger need fails before anything runs (the pointers
+    are never touched)."""
+    assert m.mdnn_conv2d_bwd_filter_noalloc_max_workspace() == 48 << 20
+    cs = m.ConvShape(256, 28, 28, 384, 768, 5, 5, 2)
+    assert m.mdnn_conv2d_bwd_filter_workspace(cs, m.F16) > 48 << 20
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_conv2d_bwd_filter_noalloc(cs, FAKE, FAKE, m.F16, FAKE, None, stream=0)
+    assert e.value.status == m.ERR_WORKSPACE
+    with pytest.raises(m.MdnnError) as e:
+        m.mdnn_conv2d_bwd_filter_noalloc(cs, FAKE, FAKE, 7, FAKE, None, stream=0)
+    assert e.value.status == m.ERR_DTYPE
+
+
 def test_split_entry_points_reject_bad_arguments(m):
     with pytest.raises(m.MdnnError) as e:                    # scale not a power of two
         m.mdnn_split_f16(4, 4, FAKE, 4, 3.0, None, FAKE, 4, FAKE, 4, stream=0)
