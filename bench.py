@@ -386,15 +386,19 @@ def _conv_bench(mdnn, reps=20):
         dw = torch.empty(w.shape, dtype=torch.float32, device="cuda")
         wsb = mdnn.mdnn_conv2d_bwd_filter_workspace(cs, 1)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
-        wgb = mdnn.mdnn_conv2d_fwd_winograd_workspace(cs, 1)
-        wgws = torch.empty(max(wgb, 256), dtype=torch.uint8, device="cuda")
+        # one workspace big enough for every forward algorithm
+        awb = max(mdnn.mdnn_conv2d_fwd_algo_workspace(cs, 1, a) for a in (mdnn.CONV_IM2COL_GEMM, mdnn.CONV_WINOGRAD))
+        aws = torch.empty(max(awb, 256), dtype=torch.uint8, device="cuda")
         fns = {
             "fwd": lambda: mdnn.mdnn_conv2d_fwd(cs, X, Wt, 1, None, 0, y, 1),
             "bwd_data": lambda: mdnn.mdnn_conv2d_bwd_data(cs, DY, Wt, 1, None, dx, 1),
             "bwd_filter": lambda: mdnn.mdnn_conv2d_bwd_filter(cs, X, DY, 1, dw, None, ws, wsb),
-            # the alternative forward algorithm (Winograd F(2x2,3x3)); its
-            # "tflops" counts the direct convolution's FLOP (equivalent rate)
-            "fwd_winograd": lambda: mdnn.mdnn_conv2d_fwd_winograd(cs, X, Wt, 1, None, 0, y, 1, wgws, wgb),
+            # the alternative forward algorithms (section 2.1); their "tflops"
+            # count the direct convolution's FLOP (equivalent rate)
+            "fwd_im2col_gemm": lambda: mdnn.mdnn_conv2d_fwd_algo(cs, X, Wt, 1, None, 0, y, 1, mdnn.CONV_IM2COL_GEMM,
+                                                                 aws, awb),
+            "fwd_winograd": lambda: mdnn.mdnn_conv2d_fwd_algo(cs, X, Wt, 1, None, 0, y, 1, mdnn.CONV_WINOGRAD,
+                                                              aws, awb),
         }
         for op, fn in fns.items():
             ms = _measure(fn, min_ms=30.0)
@@ -402,8 +406,9 @@ def _conv_bench(mdnn, reps=20):
             res[f"L{li + 1}_{sh.c_in}x{sh.h}_{op}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
                                                        "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
         key = f"L{li + 1}_{sh.c_in}x{sh.h}"
-        res[f"{key}_fwd_selected"] = ("winograd" if res[f"{key}_fwd_winograd"]["ms"] < res[f"{key}_fwd"]["ms"]
-                                      else "implicit_gemm")
+        # the library's own per-layer choice given room for every algorithm
+        res[f"{key}_fwd_selected"] = {mdnn.CONV_IMPLICIT_GEMM: "implicit_gemm", mdnn.CONV_IM2COL_GEMM: "im2col_gemm",
+                                      mdnn.CONV_WINOGRAD: "winograd"}[mdnn.mdnn_conv2d_fwd_choose(cs, 1, awb)]
     return res
 
 

@@ -263,6 +263,39 @@ mdnn_status_t mdnn_conv2d_fwd_winograd(const mdnn_conv_shape_t* shape, const voi
                                        mdnn_dtype_t y_type, void* workspace, size_t ws_bytes,
                                        mdnn_stream_t stream);
 
+/* Forward convolution with the algorithm chosen per layer (section 2.1: the
+ * convolution algorithm behind the operation is interchangeable).  Same
+ * operands, output, bias and activation as mdnn_conv2d_fwd.
+ *   MDNN_CONV_IMPLICIT_GEMM  mdnn_conv2d_fwd (no workspace);
+ *   MDNN_CONV_IM2COL_GEMM    the im2col matrix [n*Ho*Wo][r*s*c_in] (io_type)
+ *                            is written to the workspace, then one GEMM
+ *                            y = col * w^T with the bias / ReLU epilogue;
+ *                            same accuracy as the implicit GEMM;
+ *   MDNN_CONV_WINOGRAD       mdnn_conv2d_fwd_winograd (3x3 only; its error
+ *                            bound is larger than the implicit GEMM's);
+ *   MDNN_CONV_AUTO           mdnn_conv2d_fwd_choose(shape, io_type, ws_bytes).
+ * mdnn_conv2d_fwd_choose: the library's per-layer choice, a fixed table of
+ * shapes timed on MI355X restricted to the algorithms that keep the implicit
+ * GEMM's accuracy (Winograd is never chosen automatically) and to what the
+ * given workspace holds; shapes not in the table run the implicit GEMM.
+ * mdnn_conv2d_fwd_algo_workspace: bytes of 256-byte aligned workspace an
+ * algorithm needs (0 for the implicit GEMM or a bad shape).  Errors as the
+ * algorithm's own entry point; MDNN_ERR_WORKSPACE when the workspace is too
+ * small; MDNN_ERR_DTYPE for an unknown algorithm. */
+typedef enum {
+  MDNN_CONV_AUTO = 0,
+  MDNN_CONV_IMPLICIT_GEMM = 1,
+  MDNN_CONV_IM2COL_GEMM = 2,
+  MDNN_CONV_WINOGRAD = 3
+} mdnn_conv_algo_t;
+mdnn_conv_algo_t mdnn_conv2d_fwd_choose(const mdnn_conv_shape_t* shape, mdnn_dtype_t io_type, size_t ws_bytes);
+size_t mdnn_conv2d_fwd_algo_workspace(const mdnn_conv_shape_t* shape, mdnn_dtype_t io_type,
+                                      mdnn_conv_algo_t algo);
+mdnn_status_t mdnn_conv2d_fwd_algo(const mdnn_conv_shape_t* shape, const void* x, const void* w,
+                                   mdnn_dtype_t io_type, const float* bias, mdnn_act_t act, void* y,
+                                   mdnn_dtype_t y_type, mdnn_conv_algo_t algo, void* workspace,
+                                   size_t ws_bytes, mdnn_stream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Bias + activation epilogue as stand-alone kernels (section 2.1: a layer's
  * activation and its derivative in backpropagation).

@@ -34,6 +34,7 @@ NN, NT, TN = 0, 1, 2
 ACT_NONE, ACT_RELU = 0, 1
 LAYER_FC, LAYER_CONV, LAYER_MAXPOOL2 = 0, 1, 2
 LOSS_XENT, LOSS_MSE = 0, 1
+CONV_AUTO, CONV_IMPLICIT_GEMM, CONV_IM2COL_GEMM, CONV_WINOGRAD = 0, 1, 2, 3
 
 _STATUS_NAMES = {0: "SUCCESS", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_LAYOUT", 4: "ERR_DTYPE",
                  5: "ERR_MISALIGNED", 6: "ERR_WORKSPACE", 7: "ERR_LAUNCH", 8: "ERR_STATE"}
@@ -77,6 +78,7 @@ _SIGS = {
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
     "mdnn_conv2d_bwd_filter_noalloc": [_vp, _vp, _vp, _i, _vp, _vp, _vp],
     "mdnn_conv2d_fwd_winograd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp, C.c_size_t, _vp],
+    "mdnn_conv2d_fwd_algo": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _i, _vp, C.c_size_t, _vp],
     "mdnn_bias_act_fwd": [_i64, _i64, _vp, _vp, _i, _vp, _i, _vp],
     "mdnn_bias_act_bwd": [_i64, _i64, _vp, _vp, _i, _vp, _vp, _i, _vp, C.c_size_t, _vp],
     "mdnn_maxpool2_fwd": [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _i, _vp],
@@ -108,6 +110,10 @@ _lib.mdnn_conv2d_bwd_filter_noalloc_max_workspace.argtypes = []
 _lib.mdnn_conv2d_bwd_filter_noalloc_max_workspace.restype = C.c_size_t
 _lib.mdnn_conv2d_fwd_winograd_workspace.argtypes = [_vp, _i]
 _lib.mdnn_conv2d_fwd_winograd_workspace.restype = C.c_size_t
+_lib.mdnn_conv2d_fwd_algo_workspace.argtypes = [_vp, _i, _i]
+_lib.mdnn_conv2d_fwd_algo_workspace.restype = C.c_size_t
+_lib.mdnn_conv2d_fwd_choose.argtypes = [_vp, _i, C.c_size_t]
+_lib.mdnn_conv2d_fwd_choose.restype = _i
 _lib.mdnn_gemm_workspace.argtypes = [_i, _i64, _i64, _i64]
 _lib.mdnn_gemm_workspace.restype = C.c_size_t
 _lib.mdnn_gemm_split3_workspace.argtypes = [_i64, _i64, _i64]
@@ -174,7 +180,8 @@ def exported_symbols():
     return sorted(list(_SIGS) + ["mdnn_conv2d_bwd_filter_workspace", "mdnn_bias_act_bwd_workspace",
                                  "mdnn_conv2d_bwd_filter_noalloc_max_workspace",
                                  "mdnn_gemm_split3_workspace", "mdnn_gemm_workspace",
-                                 "mdnn_conv2d_fwd_winograd_workspace",
+                                 "mdnn_conv2d_fwd_winograd_workspace", "mdnn_conv2d_fwd_algo_workspace",
+                                 "mdnn_conv2d_fwd_choose",
                                  "mdnn_last_error",
                                  "mdnn_version", "mdnn_net_activation", "mdnn_net_output_grad", "mdnn_net_destroy",
                                  "mdnn_graph_destroy", "mdnn_set_gemm_tile"])
@@ -220,6 +227,20 @@ def mdnn_conv2d_fwd_winograd(shape: ConvShape, x, w, io_type, bias, act, y, y_ty
                              stream=None):
     return _call("mdnn_conv2d_fwd_winograd", _p(shape), _p(x), _p(w), io_type, _p(bias), act, _p(y), y_type,
                  _p(workspace), ws_bytes, _s(stream))
+
+
+def mdnn_conv2d_fwd_algo(shape: ConvShape, x, w, io_type, bias, act, y, y_type, algo, workspace, ws_bytes,
+                         stream=None):
+    return _call("mdnn_conv2d_fwd_algo", _p(shape), _p(x), _p(w), io_type, _p(bias), act, _p(y), y_type, algo,
+                 _p(workspace), ws_bytes, _s(stream))
+
+
+def mdnn_conv2d_fwd_algo_workspace(shape: ConvShape, io_type, algo) -> int:
+    return _lib.mdnn_conv2d_fwd_algo_workspace(_p(shape), io_type, algo)
+
+
+def mdnn_conv2d_fwd_choose(shape: ConvShape, io_type, ws_bytes) -> int:
+    return _lib.mdnn_conv2d_fwd_choose(_p(shape), io_type, ws_bytes)
 
 
 def mdnn_conv2d_fwd_winograd_workspace(shape: ConvShape, io_type) -> int:

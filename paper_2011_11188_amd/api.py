@@ -15,10 +15,10 @@ from . import (ACT_NONE, BF16, F16, F32, LAYER_CONV, LAYER_FC, LAYER_MAXPOOL2, L
                mdnn_gemm_split3_workspace, mdnn_net_activation, mdnn_net_output_grad, mdnn_net_bind, mdnn_net_create, mdnn_net_destroy, mdnn_net_sizes, mdnn_net_sync_lowp,
                mdnn_split_f16, mdnn_train_step, mdnn_train_step_async, mdnn_train_graph_create,
                mdnn_graph_launch, mdnn_graph_destroy, mdnn_conv2d_fwd_winograd,
-               mdnn_conv2d_fwd_winograd_workspace)
+               mdnn_conv2d_fwd_winograd_workspace, mdnn_conv2d_fwd_algo, mdnn_conv2d_fwd_algo_workspace)
 
 __all__ = ["torch_dtype", "gemm", "split_f16", "gemm_split3", "conv_shape", "conv2d_fwd",
-           "conv2d_fwd_winograd", "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net", "StepGraph"]
+           "conv2d_fwd_winograd", "conv2d_fwd_algo", "conv2d_bwd_data", "conv2d_bwd_filter", "make_scaler", "read_scaler", "Net", "StepGraph"]
 
 
 def torch_dtype(code: int):
@@ -102,6 +102,24 @@ def conv2d_fwd(x, w, pad: int, bias=None, act: int = ACT_NONE, out_dtype=None, s
     ho, wo = sh.h + 2 * pad - r + 1, sh.w + 2 * pad - s + 1
     y = torch.empty((sh.n, ho, wo, k), dtype=out_dtype or x.dtype, device=x.device)
     mdnn_conv2d_fwd(sh, x, w, dtype_of(x), bias, act, y, dtype_of(y), stream)
+    return y
+
+
+def conv2d_fwd_algo(x, w, pad: int, algo: int, bias=None, act: int = ACT_NONE, out_dtype=None, workspace=None,
+                    stream=None):
+    """conv2d_fwd through a chosen algorithm (CONV_AUTO: the library's
+    per-layer choice for the given workspace; a workspace of the algorithm's
+    size is allocated when none is given)."""
+    import torch
+    k, r, s, c = w.shape
+    sh = conv_shape(x.shape, k, r, s, pad)
+    ho, wo = sh.h + 2 * pad - r + 1, sh.w + 2 * pad - s + 1
+    y = torch.empty((sh.n, ho, wo, k), dtype=out_dtype or x.dtype, device=x.device)
+    io = dtype_of(x)
+    if workspace is None:
+        need = mdnn_conv2d_fwd_algo_workspace(sh, io, algo)
+        workspace = torch.empty((max(need, 256),), dtype=torch.uint8, device=x.device)
+    mdnn_conv2d_fwd_algo(sh, x, w, io, bias, act, y, dtype_of(y), algo, workspace, workspace.numel(), stream)
     return y
 
 

@@ -158,6 +158,31 @@ def test_gemm_workspace_plan(m):
     assert e.value.status == m.ERR_MISALIGNED
 
 
+def test_conv_algorithm_choice_and_errors(m):
+    """The per-layer choice never picks Winograd, picks im2col + GEMM only
+    with room for its workspace, and the algorithm entry point validates
+    before it runs anything."""
+    cs = m.ConvShape(128, 32, 32, 64, 64, 3, 3, 1)
+    need = m.mdnn_conv2d_fwd_algo_workspace(cs, m.F16, m.CONV_IM2COL_GEMM)
+    assert need == 128 * 32 * 32 * 576 * 2
+    assert m.mdnn_conv2d_fwd_algo_workspace(cs, m.F16, m.CONV_IMPLICIT_GEMM) == 0
+    assert m.mdnn_conv2d_fwd_algo_workspace(cs, m.F16, m.CONV_WINOGRAD) == m.mdnn_conv2d_fwd_winograd_workspace(cs, m.F16)
+    for shape in [cs, m.ConvShape(256, 14, 14, 32, 64, 5, 5, 2), m.ConvShape(3, 9, 7, 16, 24, 3, 3, 1)]:
+        assert m.mdnn_conv2d_fwd_choose(shape, m.F16, 0) == m.CONV_IMPLICIT_GEMM
+        assert m.mdnn_conv2d_fwd_choose(shape, m.F16, 1 << 40) in (m.CONV_IMPLICIT_GEMM, m.CONV_IM2COL_GEMM)
+    with pytest.raises(m.MdnnError) as e:                    # unknown algorithm
+        m.mdnn_conv2d_fwd_algo(cs, FAKE, FAKE, m.F16, None, 0, FAKE, m.F16, 9, None, 0, stream=0)
+    assert e.value.status == m.ERR_DTYPE
+    with pytest.raises(m.MdnnError) as e:                    # im2col workspace too small
+        m.mdnn_conv2d_fwd_algo(cs, FAKE, FAKE, m.F16, None, 0, FAKE, m.F16, m.CONV_IM2COL_GEMM, FAKE, need - 256,
+                               stream=0)
+    assert e.value.status == m.ERR_WORKSPACE
+    with pytest.raises(m.MdnnError) as e:                    # winograd needs a 3x3 filter
+        m.mdnn_conv2d_fwd_algo(m.ConvShape(2, 8, 8, 16, 16, 5, 5, 2), FAKE, FAKE, m.F16, None, 0, FAKE, m.F16,
+                               m.CONV_WINOGRAD, FAKE, 1 << 30, stream=0)
+    assert e.value.status == m.ERR_SHAPE
+
+
 def test_noalloc_bwd_filter_rejects_shapes_beyond_its_array(m):
     """The filter gradient without a caller workspace takes at most the fixed
     48 MiB per GPU; a larger need fails before anything runs (the pointers
