@@ -252,6 +252,8 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
             return "gemm_lds_kernel (64x256 direct-to-LDS pipeline)"
         if n > 128 and m > 128 and cd(m, 256) * cd(n, 256) >= 256:
             return "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"
+        if cd(m, 128) * cd(n, 128) < 128 and cd(m, 64) * cd(n, 64) >= 128:
+            return "gemm_lds_kernel (64x64 direct-to-LDS pipeline)"
         if cd(m, 128) * cd(n, 128) <= 256:
             return "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 4 stages)"
         return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
@@ -501,11 +503,8 @@ def _cpu_baseline(cfg):
     import numpy as np
     import workloads as W
     from oracle import train
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    # the host cores this process may run on (numpy's BLAS pool is sized to them)
+    threads = len(os.sched_getaffinity(0))
     orc = train.from_config(cfg, W.init_params(cfg))
     x, t = W.batch_inputs(cfg, 0)
     t0 = time.perf_counter()
@@ -514,8 +513,37 @@ def _cpu_baseline(cfg):
     del np
     return {"value": round(cfg.batch / dt, 2), "unit": "samples/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"one full SGD step (batch {cfg.batch}) of {cfg.name} in fp64 numpy, "
-                      f"{dt:.1f} s wall"}
+            "sample": f"one full SGD step (batch {cfg.batch}) of {cfg.name} in fp64 numpy "
+                      f"(its products through numpy's BLAS), {dt:.1f} s wall"}
+
+
+def _copy_calibration(mdnn):
+    """Calibration for HBM-traffic counters: a plain fp32 copy of known size
+    (256 MiB read + 256 MiB written per launch), three launches."""
+    import torch
+    ncopy = 64 << 20
+    csrc = torch.empty(ncopy, dtype=torch.float32, device="cuda").normal_()
+    cdst = torch.empty_like(csrc)
+    for _ in range(3):
+        mdnn.mdnn_cast(ncopy, csrc, mdnn.F32, cdst, mdnn.F32)
+    _sync()
+    del csrc, cdst
+
+
+def _workloads_bench(mdnn):
+    """The LeNet bf16 and fp32 MLP training steps, eager and as recorded graphs."""
+    import workloads as W
+    wl = {}
+    for c in (W.lenet_bf16(), W.mlp784_fp32()):
+        n2, xs2, ts2 = _train_setup(mdnn, c)
+        m2 = _time_steps(n2, xs2, ts2, 50, 5)
+        g2 = _time_graph_steps(n2, xs2, ts2, 200, 5)
+        wl[c.name] = {"ms_per_step": round(m2, 4), "samples_per_s": round(c.batch / (m2 * 1e-3), 1),
+                      "tflops": round(c.flops_per_step() / (m2 * 1e-3) / 1e12, 2),
+                      "graph_ms_per_step": round(g2, 4),
+                      "graph_samples_per_s": round(c.batch / (g2 * 1e-3), 1)}
+        n2.close()
+    return wl
 
 
 def main():
@@ -525,6 +553,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--quick", action="store_true", help="headline only (no sub-benchmarks)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--only", choices=["gemm", "conv", "split3", "workloads", "async"],
+                    help="profiling runs: the counter calibration copy and one sub-benchmark, printed as JSON "
+                         "(no headline line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: the step runs on one GPU (no collectives are implemented); use --gpus 1",
@@ -538,6 +569,13 @@ def main():
         print("bench.py: no GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+
+    if args.only:
+        _copy_calibration(mdnn)
+        subs = {"gemm": _gemm_sweep, "conv": _conv_bench, "split3": _split3_sweep, "workloads": _workloads_bench,
+                "async": _async_bench}
+        print(json.dumps({args.only: subs[args.only](mdnn), "clocks": _clocks()}), flush=True)
+        return
 
     clocks_before = _clocks()
     cfg = W.wide_mlp_fp16()
@@ -555,16 +593,21 @@ def main():
     graph_applied = check.stop(args.steps)
     print(f"[bench] {cfg.name} as a recorded graph: {graph_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # dominant kernel: the kernel instantiation (layout, output type, tile)
-    # whose launches in the step take the most time
+    # every kernel instantiation (layout, output type, tile) of the step's
+    # GEMMs, its launches replayed as the step issues them; the dominant
+    # kernel is the one whose launches take the most time per step
     gemms = _step_gemms(cfg)
     groups = {}
     for g in gemms:
         groups.setdefault((g[0], g[4], _kernel_choice(g[0], g[1], g[2], g[3])), []).append(g)
-    best = None
+    best, step_groups = None, {}
     for key, grp in groups.items():
         mpl, fpl = _replay_group(mdnn, net, cfg, grp, reps=max(5, args.steps // 2))
         total = mpl * len(grp)
+        tf = fpl / (mpl * 1e-3) / 1e12
+        step_groups[f"{key[0]} f16 -> {key[1]}, {key[2]}"] = {
+            "launches_per_step": len(grp), "avg_launch_ms": round(mpl, 4), "flop_per_launch": fpl,
+            "tflops": round(tf, 1), "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4), "ms_per_step": round(total, 4)}
         if best is None or total > best[0]:
             best = (total, key, mpl, fpl, len(grp))
     _, key, mpl, fpl, nl = best
@@ -576,15 +619,7 @@ def main():
     print(f"[bench] dominant kernel {roofline['kernel']}: {mpl:.4f} ms/launch, "
           f"{achieved:.1f} TFLOP/s", file=sys.stderr, flush=True)
 
-    # calibration for HBM-traffic counters: a plain fp32 copy of known size
-    # (256 MiB read + 256 MiB written per launch)
-    ncopy = 64 << 20
-    csrc = torch.empty(ncopy, dtype=torch.float32, device="cuda").normal_()
-    cdst = torch.empty_like(csrc)
-    for _ in range(3):
-        mdnn.mdnn_cast(ncopy, csrc, mdnn.F32, cdst, mdnn.F32)
-    _sync()
-    del csrc, cdst
+    _copy_calibration(mdnn)
     traffic = _traffic_record(roofline["kernel"])
     if traffic is not None:
         roofline["traffic"] = traffic
@@ -604,6 +639,7 @@ def main():
                    "step_mfma_frac": round(step_tf / PEAK_F16_TFLOPS, 4),
                    "flop_per_step": cfg.flops_per_step()},
         "roofline": roofline,
+        "step_gemm_kernels": step_groups,
     }
     if not args.quick:
         line["gemm_sweep"] = _gemm_sweep(mdnn)
@@ -612,17 +648,7 @@ def main():
         print("[bench] conv done", file=sys.stderr, flush=True)
         line["gemm_fp32_split3"] = _split3_sweep(mdnn)
         print("[bench] fp32 split3 sweep done", file=sys.stderr, flush=True)
-        wl = {}
-        for c in (W.lenet_bf16(), W.mlp784_fp32()):
-            n2, xs2, ts2 = _train_setup(mdnn, c)
-            m2 = _time_steps(n2, xs2, ts2, 50, 5)
-            g2 = _time_graph_steps(n2, xs2, ts2, 200, 5)
-            wl[c.name] = {"ms_per_step": round(m2, 4), "samples_per_s": round(c.batch / (m2 * 1e-3), 1),
-                          "tflops": round(c.flops_per_step() / (m2 * 1e-3) / 1e12, 2),
-                          "graph_ms_per_step": round(g2, 4),
-                          "graph_samples_per_s": round(c.batch / (g2 * 1e-3), 1)}
-            n2.close()
-        line["workloads"] = wl
+        line["workloads"] = _workloads_bench(mdnn)
         print("[bench] workloads done", file=sys.stderr, flush=True)
         line["async_sgd"] = _async_bench(mdnn)
         print("[bench] async sgd done", file=sys.stderr, flush=True)

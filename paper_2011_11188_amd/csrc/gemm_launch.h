@@ -212,6 +212,12 @@ typedef lds::Tile<64, 256, 2, 4, 2> TileNarrowM;
 // 128 x 128 with four LDS stages (128 KB): one workgroup per CU, so the
 // register budget is that of two waves per SIMD
 typedef lds::Tile<128, 128, 2, 4, 2> Tile128Deep;
+// Grids of fewer than 128 tiles of 128 x 128 (e.g. 1024 x 1024): 64 x 64
+// tiles with four waves of 32 x 32 put four times as many workgroups on the
+// chip (1024^3: 11.2 -> 7.2 us; splitting each tile's K among more waves of
+// one workgroup measured no faster, the time being the load latency, the
+// epilogue and the launch rather than the K loop).
+typedef lds::Tile<64, 64, 2, 2, 4> Tile64;
 
 template <class T, class OutT, bool A_KC, bool B_KC>
 inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
@@ -224,6 +230,9 @@ inline mdnn_status_t run_gemm_lds(const LdsOperand& a, const LdsOperand& b, int6
   else if (o == TILE_LDS_PIPE ||
            (o != TILE_LDS_PIPE128 && N > 128 && M > 128 && ceil_div(M, 256) * ceil_div(N, 256) * splits >= 256))
     launch_gemm_lds<T, OutT, lds::Tile256, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
+  else if (o == TILE_AUTO && ceil_div(M, 128) * ceil_div(N, 128) * splits < 128 &&
+           ceil_div(M, 64) * ceil_div(N, 64) * splits >= 128)
+    launch_gemm_lds<T, OutT, Tile64, A_KC, B_KC>(a, b, M, N, K, ep, splits, stream);
   else if (ceil_div(M, 128) * ceil_div(N, 128) * splits <= 256)
     // at most one workgroup per CU: the LDS a second one would use holds two
     // more stages instead, so three tiles are in flight behind the MFMAs

@@ -104,6 +104,32 @@ def test_gemm_pipelined_kernel_ragged(mdnn, dt, layout, tile):
         mdnn.mdnn_set_gemm_tile(0)
 
 
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_gemm_pipelined_64x64_tiles(mdnn, dt, layout):
+    """Grids of fewer than 128 tiles of 128 x 128 but at least 128 of 64 x 64
+    (chosen automatically): ragged shapes, fp32 output, and the bias + ReLU
+    and ReLU-mask epilogues stored in the storage type."""
+    for i, (m, n, k) in enumerate([(1000, 1032, 448), (760, 1096, 192), (1024, 1024, 1024)]):
+        sa, sb = _shapes(layout, m, n, k)
+        a = W.normal(sa, 11, 10 * i + 1, dt, 1 / np.sqrt(k))
+        b = W.normal(sb, 11, 10 * i + 2, dt, 1 / np.sqrt(k))
+        got = _run(mdnn, layout, dev(a, dt), dev(b, dt), "f32", m, n, k)
+        a64, b64 = decode(a, dt), decode(b, dt)
+        want = ops.gemm(layout, a64, b64)
+        assert norm_max_err(got, want) <= TOL, (layout, dt, (m, n, k))
+        bias = W.normal((n,), 11, 10 * i + 3, "f32", 0.5)
+        got = _run(mdnn, layout, dev(a, dt), dev(b, dt), dt, m, n, k, bias=dev(bias, "f32"), act=1)
+        exact = ops.bias_act(want, bias.astype(np.float64), "relu")
+        err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)) + np.abs(bias), k + 1)
+        assert lowp_close(got, exact, dt, err)
+        y_in = W.normal((m, n), 11, 10 * i + 4, dt)
+        got = _run(mdnn, layout, dev(a, dt), dev(b, dt), dt, m, n, k, mask=dev(y_in, dt))
+        exact = np.where(decode(y_in, dt) > 0, want, 0.0)
+        err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)), k)
+        assert lowp_close(got, exact, dt, err)
+
+
 @pytest.mark.parametrize("tile", [1, 2, 4, 5])
 @pytest.mark.parametrize("out_dt", ["f32", "f16"])
 def test_gemm_every_epilogue_term_interior_and_edge_tiles(mdnn, tile, out_dt):

@@ -60,6 +60,7 @@ def test_spills_report_only_vector_register_spills():
     (("TN", 4096, 1, 4096), "skinny cols kernel"),
     (("NT", 4096, 4096, 1), "skinny depth kernel"),
     (("NN", 100, 136, 100), "gemm_mfma_kernel 64x64"),
+    (("NT", 1024, 1024, 1024), "gemm_lds_kernel (64x64 direct-to-LDS pipeline)"),
 ])
 def test_kernel_choice_for_the_step_shapes(shape, kernel):
     assert bench._kernel_choice(*shape) == kernel
