@@ -184,7 +184,8 @@ static size_t filter_ws_split_bytes(const ConvGeom& g) {
   const SplitPlan p = filter_plan(g), q = conv_pipe_filter_plan(g);
   size_t splits = p.splits > 1 ? (size_t)p.splits : 0;
   if (q.splits > 1 && (size_t)q.splits > splits) splits = (size_t)q.splits;
-  const int64_t sb = conv_small_filter_blocks(g);
+  // the vector-ALU kernels' block count (at least the matrix-core kernel's)
+  const int64_t sb = conv_small_filter_blocks(g, MDNN_F32);
   if (sb > 0 && (size_t)sb > splits) splits = (size_t)sb;
   return (splits * mn + 255) & ~(size_t)255;
 }
@@ -271,7 +272,7 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
     return db ? fill_zero(db, (size_t)g.k * 4, st) : MDNN_SUCCESS;
   }
   bool done = false;
-  if (pipe_allowed() && conv_small_filter_blocks(g) > 0) {
+  if (pipe_allowed() && conv_small_filter_blocks(g, io_type) > 0) {
     MDNN_TRY(conv_small_filter(g, x, dy, dw, workspace, io_type, st));
     done = true;
   }

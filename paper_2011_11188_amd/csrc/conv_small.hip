@@ -316,6 +316,164 @@ conv_small_filter_px_kernel(const typename T::storage* __restrict__ x, const typ
   }
 }
 
+// ---------------------------------------------------------------------------
+// 16-bit data with K = r*s*c_in <= 32: the whole reduction of a forward
+// output is one 32-deep MFMA step, and the filter gradient is a product of
+// depth n*ho*wo with a 32 x 32 (or smaller) result; both run on the matrix
+// cores.  Fragments are gathered straight from global memory (x is small
+// and stays in the caches): lane l owns row l % 16 of a 16 x 32 operand
+// fragment and the eight consecutive reduction indices 8 (l / 16) .. + 7,
+// zero past the reduction, in the padding or past the last pixel.
+// ---------------------------------------------------------------------------
+
+// Eight consecutive im2col entries (pixel m, columns kk0 .. kk0 + 7) of a
+// stride-1 convolution, as packed 16-bit bits.
+template <class T>
+__device__ __forceinline__ uint4 im2col8(const typename T::storage* __restrict__ x, const ConvGeom& g, int m,
+                                         bool m_ok, int kk0, int K) {
+  uint16_t v[8];
+  const int hw = g.ho * g.wo;
+  const int n = m / hw, rem = m - n * hw, i = rem / g.wo, j = rem - i * g.wo;
+  int tap = kk0 / g.c, ch = kk0 - tap * g.c;
+  int tr = tap / g.s, ts = tap - tr * g.s;
+  const typename T::storage* xn = x + (int64_t)n * g.h * g.w * g.c;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int y = i + tr - g.pad, xx = j + ts - g.pad;
+    const bool ok = m_ok && kk0 + e < K && (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
+    const uint16_t val = xn[ok ? ((int64_t)y * g.w + xx) * g.c + ch : 0];
+    v[e] = ok ? val : (uint16_t)0;
+    if (++ch == g.c) {
+      ch = 0;
+      if (++ts == g.s) {
+        ts = 0;
+        ++tr;
+      }
+    }
+  }
+  return pack8(v);
+}
+
+// y[m][n] = epi(sum_kk im2col[m][kk] w[n][kk]): one wave per 16 output
+// pixels, all output channels (up to 64, 16 per MFMA).
+constexpr int MF_NB = 4;
+template <class T, class OutT>
+__global__ void __launch_bounds__(256)
+conv_small_fwd_mfma_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ w,
+                           ConvGeom g, int64_t M, Epilogue ep) {
+  const int lane = threadIdx.x & 63;
+  const int K = g.r * g.s * g.c, N = g.k, nb_n = (N + 15) / 16;
+  const int64_t pb = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t m = pb * 16 + (lane & 15);
+  const int kk0 = 8 * (lane >> 4);
+  if (pb * 16 >= M) return;
+  const uint4 a = im2col8<T>(x, g, (int)(m < M ? m : 0), m < M, kk0, K);
+  const int64_t mrow = pb * 16 + (lane & 15);
+  const int64_t nrow = 4 * (lane >> 4);
+#pragma unroll
+  for (int nb = 0; nb < MF_NB; ++nb) {
+    if (nb < nb_n) {
+      const int n = nb * 16 + (lane & 15);
+      uint16_t v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = n < N && kk0 + e < K;
+        const uint16_t val = w[ok ? (int64_t)n * K + kk0 + e : 0];
+        v[e] = ok ? val : (uint16_t)0;
+      }
+      const float4_t acc = Mfma<T>::run(pack8(v), a, (float4_t){0.f, 0.f, 0.f, 0.f});
+      epilogue_store4<T, OutT>(ep, M, N, mrow, nb * 16 + nrow, acc);
+    }
+  }
+}
+
+// partial[b][k][kk] = sum over block b's pixels of dy[p][k] * im2col[p][kk]
+// (c_out <= 32, K <= 32): each wave takes every fourth 32-pixel step of the
+// block's range, the four waves' sums are added in wave order in LDS.
+constexpr int MF_FILTER_STEPS = 8;  // 32-pixel steps per wave
+constexpr int64_t MF_FILTER_PIXELS = 4 * MF_FILTER_STEPS * 32;
+template <class T>
+__global__ void __launch_bounds__(256)
+conv_small_filter_mfma_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ dy,
+                              ConvGeom g, int64_t P, float* __restrict__ partial) {
+  __shared__ float red[3][4][64][4];  // waves 1..3: [wave][fragment][lane][4]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int K = g.r * g.s * g.c, N = g.k;
+  float4_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = (float4_t){0.f, 0.f, 0.f, 0.f};
+  const int pk0 = 8 * (lane >> 4);  // this lane's 8 pixels within a 32-pixel step
+  for (int st = 0; st < MF_FILTER_STEPS; ++st) {
+    const int64_t p0 = (int64_t)blockIdx.x * MF_FILTER_PIXELS + (int64_t)(st * 4 + wave) * 32 + pk0;
+    if (p0 - pk0 >= P) break;
+    // A = dy^T: rows k, reduction over pixels
+    uint4 af[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int k = mb * 16 + (lane & 15);
+      uint16_t v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = k < N && p0 + e < P;
+        const uint16_t val = dy[ok ? (p0 + e) * N + k : 0];
+        v[e] = ok ? val : (uint16_t)0;
+      }
+      af[mb] = pack8(v);
+    }
+    // B^T = im2col^T: rows kk, reduction over pixels
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int kk = tb * 16 + (lane & 15);
+      uint16_t v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t p = p0 + e;
+        bool ok = kk < K && p < P;
+        int64_t off = 0;
+        if (ok) {
+          const int pi = (int)p, hw = g.ho * g.wo;
+          const int n = pi / hw, rem = pi - n * hw, i = rem / g.wo, j = rem - i * g.wo;
+          const int tap = kk / g.c, ch = kk - tap * g.c, tr = tap / g.s, ts = tap - tr * g.s;
+          const int y = i + tr - g.pad, xx = j + ts - g.pad;
+          ok = (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
+          off = (((int64_t)n * g.h + y) * g.w + xx) * g.c + ch;
+        }
+        const uint16_t val = x[ok ? off : 0];
+        v[e] = ok ? val : (uint16_t)0;
+      }
+      const uint4 bf = pack8(v);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) acc[mb][tb] = Mfma<T>::run(bf, af[mb], acc[mb][tb]);
+    }
+  }
+  // acc[mb][tb][e] = D[k = mb*16 + lane%16][kk = tb*16 + 4*(lane/16) + e]
+  if (wave > 0) {
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb)
+        *(float4_t*)red[wave - 1][mb * 2 + tb][lane] = acc[mb][tb];
+  }
+  __syncthreads();
+  if (wave > 0) return;
+  const int MN = N * K;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      float4_t s = acc[mb][tb];
+      for (int wv = 0; wv < 3; ++wv) s += *(const float4_t*)red[wv][mb * 2 + tb][lane];
+      const int k = mb * 16 + (lane & 15), kk = tb * 16 + 4 * (lane >> 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (k < N && kk + e < K) partial[(int64_t)blockIdx.x * MN + (int64_t)k * K + kk + e] = s[e];
+    }
+}
+
+bool mfma_small(const ConvGeom& g, mdnn_dtype_t io) { return io != MDNN_F32 && g.r * g.s * g.c <= 32; }
+
 constexpr int64_t FILTER_PIXELS = 128;  // pixels per block of the filter gradient (enough blocks to hide the staging latency)
 constexpr size_t LDS_LIMIT = 65536;      // dynamic LDS bytes per block
 
@@ -356,11 +514,30 @@ static void small_fwd_launch(const ConvGeom& g, const void* x, const void* w, co
                        st, (const S*)x, (const S*)w, g, M, ep);
 }
 
+template <class T, class OutT>
+static void small_fwd_mfma_launch(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, int64_t M,
+                                  hipStream_t st) {
+  typedef typename T::storage S;
+  hipLaunchKernelGGL((conv_small_fwd_mfma_kernel<T, OutT>), dim3((unsigned)ceil_div(M, 64)), dim3(256), 0, st,
+                     (const S*)x, (const S*)w, g, M, ep);
+}
+
 mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
                              mdnn_dtype_t out, hipStream_t st) {
   const int64_t M = (int64_t)g.n * g.ho * g.wo;
   if (M == 0) return MDNN_SUCCESS;
   if (ceil_div(M, TP) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: too many output pixels");
+  if (mfma_small(g, io) && g.k <= 16 * MF_NB) {
+    // one 32-deep matrix-core step per 16 pixels x 16 channels
+    if (io == MDNN_F16) {
+      if (out == MDNN_F32) small_fwd_mfma_launch<F16, F32>(g, x, w, ep, M, st);
+      else small_fwd_mfma_launch<F16, F16>(g, x, w, ep, M, st);
+    } else {
+      if (out == MDNN_F32) small_fwd_mfma_launch<BF16, F32>(g, x, w, ep, M, st);
+      else small_fwd_mfma_launch<BF16, BF16>(g, x, w, ep, M, st);
+    }
+    return check_launch("conv_small_fwd_mfma_kernel");
+  }
   // one pixel per thread when c_out fits its registers
   const bool px = fwd_px_ok(g);
   if (io == MDNN_F16) {
@@ -375,10 +552,14 @@ mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, co
   return check_launch("conv_small_fwd_kernel");
 }
 
-int64_t conv_small_filter_blocks(const ConvGeom& g) {
+// the matrix-core filter gradient: 16-bit data, K <= 32, c_out <= 32
+static bool filter_mfma_ok(const ConvGeom& g, mdnn_dtype_t io) { return mfma_small(g, io) && g.k <= 32; }
+
+int64_t conv_small_filter_blocks(const ConvGeom& g, mdnn_dtype_t io) {
   const int K = g.r * g.s * g.c;
   if (K > 64 || g.k > 256 || (int64_t)g.k * K > 1024 || filter_lds(g) > LDS_LIMIT || !pixels_fit(g)) return 0;
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
+  if (filter_mfma_ok(g, io)) return ceil_div(P, MF_FILTER_PIXELS);
   return ceil_div(P, filter_px_ok(g) ? (int64_t)PX : FILTER_PIXELS);
 }
 
@@ -398,10 +579,20 @@ static void small_filter_launch(const ConvGeom& g, const void* x, const void* dy
 
 mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
                                 mdnn_dtype_t io, hipStream_t st) {
-  const int64_t blocks = conv_small_filter_blocks(g);
+  const int64_t blocks = conv_small_filter_blocks(g, io);
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
   if (blocks <= 0 || blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: filter gradient shape");
   float* part = (float*)ws;
+  if (filter_mfma_ok(g, io)) {
+    if (io == MDNN_F16)
+      hipLaunchKernelGGL(conv_small_filter_mfma_kernel<F16>, dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const uint16_t*)x, (const uint16_t*)dy, g, P, part);
+    else
+      hipLaunchKernelGGL(conv_small_filter_mfma_kernel<BF16>, dim3((unsigned)blocks), dim3(256), 0, st,
+                         (const uint16_t*)x, (const uint16_t*)dy, g, P, part);
+    MDNN_TRY(check_launch("conv_small_filter_mfma_kernel"));
+    return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st);
+  }
   if (io == MDNN_F16) small_filter_launch<F16>(g, x, dy, P, blocks, part, st);
   else if (io == MDNN_BF16) small_filter_launch<BF16>(g, x, dy, P, blocks, part, st);
   else small_filter_launch<F32>(g, x, dy, P, blocks, part, st);
