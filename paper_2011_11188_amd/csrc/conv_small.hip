@@ -354,44 +354,104 @@ __device__ __forceinline__ uint4 im2col8(const typename T::storage* __restrict__
   return pack8(v);
 }
 
-// y[m][n] = epi(sum_kk im2col[m][kk] w[n][kk]): one wave per 16 output
-// pixels, all output channels (up to 64, 16 per MFMA).
+// y[m][n] = epi(sum_kk im2col[m][kk] w[n][kk]): a wave loads the filter's
+// fragments once (all output channels, up to 64, 16 per MFMA), then handles
+// MF_Q blocks of 16 output pixels with every block's gathers in flight
+// together before any of its products.
 constexpr int MF_NB = 4;
+constexpr int MF_Q = 4;
 template <class T, class OutT>
 __global__ void __launch_bounds__(256)
 conv_small_fwd_mfma_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ w,
                            ConvGeom g, int64_t M, Epilogue ep) {
   const int lane = threadIdx.x & 63;
   const int K = g.r * g.s * g.c, N = g.k, nb_n = (N + 15) / 16;
-  const int64_t pb = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int64_t m = pb * 16 + (lane & 15);
+  const int64_t pb0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * MF_Q;
+  if (pb0 * 16 >= M) return;
   const int kk0 = 8 * (lane >> 4);
-  if (pb * 16 >= M) return;
-  const uint4 a = im2col8<T>(x, g, (int)(m < M ? m : 0), m < M, kk0, K);
-  const int64_t mrow = pb * 16 + (lane & 15);
-  const int64_t nrow = 4 * (lane >> 4);
+  uint4 wf[MF_NB];
 #pragma unroll
   for (int nb = 0; nb < MF_NB; ++nb) {
-    if (nb < nb_n) {
-      const int n = nb * 16 + (lane & 15);
-      uint16_t v[8];
+    const int n = nb * 16 + (lane & 15);
+    uint16_t v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool ok = n < N && kk0 + e < K;
-        const uint16_t val = w[ok ? (int64_t)n * K + kk0 + e : 0];
-        v[e] = ok ? val : (uint16_t)0;
+    for (int e = 0; e < 8; ++e) {
+      const bool ok = nb < nb_n && n < N && kk0 + e < K;
+      const uint16_t val = w[ok ? (int64_t)n * K + kk0 + e : 0];
+      v[e] = ok ? val : (uint16_t)0;
+    }
+    wf[nb] = pack8(v);
+  }
+  uint4 a[MF_Q];
+#pragma unroll
+  for (int q = 0; q < MF_Q; ++q) {
+    const int64_t m = (pb0 + q) * 16 + (lane & 15);
+    a[q] = im2col8<T>(x, g, (int)(m < M ? m : 0), m < M, kk0, K);
+  }
+  const int64_t nrow = 4 * (lane >> 4);
+#pragma unroll
+  for (int q = 0; q < MF_Q; ++q) {
+    const int64_t mrow = (pb0 + q) * 16 + (lane & 15);
+#pragma unroll
+    for (int nb = 0; nb < MF_NB; ++nb) {
+      if (nb < nb_n) {
+        const float4_t acc = Mfma<T>::run(wf[nb], a[q], (float4_t){0.f, 0.f, 0.f, 0.f});
+        epilogue_store4<T, OutT>(ep, M, N, mrow, nb * 16 + nrow, acc);
       }
-      const float4_t acc = Mfma<T>::run(pack8(v), a, (float4_t){0.f, 0.f, 0.f, 0.f});
-      epilogue_store4<T, OutT>(ep, M, N, mrow, nb * 16 + nrow, acc);
     }
   }
 }
 
 // partial[b][k][kk] = sum over block b's pixels of dy[p][k] * im2col[p][kk]
-// (c_out <= 32, K <= 32): each wave takes every fourth 32-pixel step of the
-// block's range, the four waves' sums are added in wave order in LDS.
-constexpr int MF_FILTER_STEPS = 8;  // 32-pixel steps per wave
-constexpr int64_t MF_FILTER_PIXELS = 4 * MF_FILTER_STEPS * 32;
+// (c_out <= 32, K <= 32): each wave takes every fourth pair of 32-pixel steps
+// of the block's range (both steps' fragments gathered before their
+// products), and the four waves' sums are added in wave order in LDS.
+constexpr int MF_FILTER_PAIRS = 2;  // pairs of 32-pixel steps per wave
+constexpr int64_t MF_FILTER_PIXELS = 4 * MF_FILTER_PAIRS * 64;
+
+// A = dy^T (rows k) and B^T = im2col^T (rows kk) fragments of the 32-pixel
+// step whose lane pixels start at p0.
+template <class T>
+__device__ __forceinline__ void filter_frags(const typename T::storage* __restrict__ x,
+                                             const typename T::storage* __restrict__ dy, const ConvGeom& g,
+                                             int64_t P, int64_t p0, int lane, int K, uint4 (&af)[2], uint4 (&bf)[2]) {
+  const int N = g.k;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int k = mb * 16 + (lane & 15);
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const bool ok = k < N && p0 + e < P;
+      const uint16_t val = dy[ok ? (p0 + e) * N + k : 0];
+      v[e] = ok ? val : (uint16_t)0;
+    }
+    af[mb] = pack8(v);
+  }
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    const int kk = tb * 16 + (lane & 15);
+    const int tap = kk / g.c, ch = kk - tap * g.c, tr = tap / g.s, ts = tap - tr * g.s;
+    uint16_t v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t p = p0 + e;
+      bool ok = kk < K && p < P;
+      int64_t off = 0;
+      if (ok) {
+        const int pi = (int)p, hw = g.ho * g.wo;
+        const int n = pi / hw, rem = pi - n * hw, i = rem / g.wo, j = rem - i * g.wo;
+        const int y = i + tr - g.pad, xx = j + ts - g.pad;
+        ok = (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
+        off = (((int64_t)n * g.h + y) * g.w + xx) * g.c + ch;
+      }
+      const uint16_t val = x[ok ? off : 0];
+      v[e] = ok ? val : (uint16_t)0;
+    }
+    bf[tb] = pack8(v);
+  }
+}
+
 template <class T>
 __global__ void __launch_bounds__(256)
 conv_small_filter_mfma_kernel(const typename T::storage* __restrict__ x, const typename T::storage* __restrict__ dy,
@@ -405,48 +465,18 @@ conv_small_filter_mfma_kernel(const typename T::storage* __restrict__ x, const t
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = (float4_t){0.f, 0.f, 0.f, 0.f};
   const int pk0 = 8 * (lane >> 4);  // this lane's 8 pixels within a 32-pixel step
-  for (int st = 0; st < MF_FILTER_STEPS; ++st) {
-    const int64_t p0 = (int64_t)blockIdx.x * MF_FILTER_PIXELS + (int64_t)(st * 4 + wave) * 32 + pk0;
-    if (p0 - pk0 >= P) break;
-    // A = dy^T: rows k, reduction over pixels
-    uint4 af[2];
+  for (int pr = 0; pr < MF_FILTER_PAIRS; ++pr) {
+    const int64_t s0 = (int64_t)blockIdx.x * MF_FILTER_PIXELS + (int64_t)(pr * 4 + wave) * 64;
+    if (s0 >= P) break;
+    uint4 af[2][2], bf[2][2];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      const int k = mb * 16 + (lane & 15);
-      uint16_t v[8];
+    for (int h = 0; h < 2; ++h) filter_frags<T>(x, dy, g, P, s0 + h * 32 + pk0, lane, K, af[h], bf[h]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool ok = k < N && p0 + e < P;
-        const uint16_t val = dy[ok ? (p0 + e) * N + k : 0];
-        v[e] = ok ? val : (uint16_t)0;
-      }
-      af[mb] = pack8(v);
-    }
-    // B^T = im2col^T: rows kk, reduction over pixels
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const int kk = tb * 16 + (lane & 15);
-      uint16_t v[8];
+      for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int64_t p = p0 + e;
-        bool ok = kk < K && p < P;
-        int64_t off = 0;
-        if (ok) {
-          const int pi = (int)p, hw = g.ho * g.wo;
-          const int n = pi / hw, rem = pi - n * hw, i = rem / g.wo, j = rem - i * g.wo;
-          const int tap = kk / g.c, ch = kk - tap * g.c, tr = tap / g.s, ts = tap - tr * g.s;
-          const int y = i + tr - g.pad, xx = j + ts - g.pad;
-          ok = (unsigned)y < (unsigned)g.h && (unsigned)xx < (unsigned)g.w;
-          off = (((int64_t)n * g.h + y) * g.w + xx) * g.c + ch;
-        }
-        const uint16_t val = x[ok ? off : 0];
-        v[e] = ok ? val : (uint16_t)0;
-      }
-      const uint4 bf = pack8(v);
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) acc[mb][tb] = Mfma<T>::run(bf, af[mb], acc[mb][tb]);
-    }
+        for (int mb = 0; mb < 2; ++mb) acc[mb][tb] = Mfma<T>::run(bf[h][tb], af[h][mb], acc[mb][tb]);
   }
   // acc[mb][tb][e] = D[k = mb*16 + lane%16][kk = tb*16 + 4*(lane/16) + e]
   if (wave > 0) {
@@ -518,7 +548,7 @@ template <class T, class OutT>
 static void small_fwd_mfma_launch(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, int64_t M,
                                   hipStream_t st) {
   typedef typename T::storage S;
-  hipLaunchKernelGGL((conv_small_fwd_mfma_kernel<T, OutT>), dim3((unsigned)ceil_div(M, 64)), dim3(256), 0, st,
+  hipLaunchKernelGGL((conv_small_fwd_mfma_kernel<T, OutT>), dim3((unsigned)ceil_div(M, 64 * MF_Q)), dim3(256), 0, st,
                      (const S*)x, (const S*)w, g, M, ep);
 }
 
