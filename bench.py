@@ -300,16 +300,27 @@ def _replay_group(mdnn, net, cfg, group, reps):
     # ahead of the GPU, so each pair brackets that kernel's execution alone,
     # as a kernel trace reports it, not the gaps between kernels)
     import torch
+    # the step's split-K workspace and, for the weight gradients, its loss
+    # scaler's overflow flag: the replay takes the kernel paths the step takes
+    ws_bytes = max([mdnn.mdnn_gemm_workspace(lp, c[1], c[2], c[3]) for c in calls] + [256])
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
 
     def launch(c):
-        mdnn.mdnn_gemm_mixed(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
-                             None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14])
+        mdnn.mdnn_gemm_mixed_ws(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
+                                None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14], ws, ws_bytes,
+                                nonfinite=flag if c[0] == 2 and c[10] == 0 else None)
     for _ in range(3):
         for c in calls:
             launch(c)
     torch.cuda.synchronize()
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
              for _ in range(reps * len(calls))]
+    # a bounded spin ahead of the timed launches keeps the GPU busy while the
+    # host queues them all, so short kernels are not timed waiting for their
+    # own submission
+    if hasattr(torch.cuda, "_sleep"):
+        torch.cuda._sleep(4_000_000)
     k = 0
     for _ in range(reps):
         for c in calls:

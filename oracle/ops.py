@@ -59,6 +59,21 @@ def split_f16(x: np.ndarray, scale: float) -> Tuple[np.ndarray, np.ndarray]:
     return hi, lo
 
 
+def split_scale(x: np.ndarray) -> float:
+    """The leading scale s1 of Eq. (1) when the caller leaves it to the
+    method.  The section fixes only the well-scaled case; the reading taken
+    here: the power of two that puts max|X| / s1 in [2^14, 2^15), so the
+    leading fp16 term keeps its 11 bits and stays a factor two below fp16's
+    largest finite value; 1 when max|X| is 0 or not finite; never below
+    2^-126 (the smallest normal fp32 power of two)."""
+    x = np.asarray(x, dtype=np.float64)
+    mx = float(np.max(np.abs(x))) if x.size else 0.0
+    if mx == 0.0 or not np.isfinite(mx):
+        return 1.0
+    e = int(np.floor(np.log2(mx))) - 14
+    return float(2.0 ** max(e, -126))
+
+
 def gemm_split3(layout: str, a: np.ndarray, b: np.ndarray, a_scale: float, b_scale: float,
                 alpha: float = 1.0, beta: float = 0.0, c: Optional[np.ndarray] = None) -> np.ndarray:
     """alpha * (a1 b1 A1B1 + a1 b2 A1B2 + a2 b1 A2B1) + beta * C, exactly, for

@@ -16,6 +16,8 @@
 //   the ResNet-style layers (including the reduction): 38.9 -> 32.7,
 //   40.2 -> 26.1, 33.6 -> 26.5 us.
 #include "conv_pipe.h"
+
+#include <numeric>
 #include "gemm_launch.h"
 
 namespace mdnn {
@@ -153,6 +155,11 @@ SplitPlan conv_pipe_filter_plan(const ConvGeom& g) {
   if (s > steps / 4) s = steps / 4;
   while (s > 1 && (size_t)s * M * N * 4 > FILTER_WS_MAX) --s;
   if (s < 1) s = 1;
+  // with few tiles, tiles x splits a multiple of 8 lets the kernel keep the
+  // tiles of one split on one XCD (its slice of x and dy then comes through
+  // that L2 once)
+  const int64_t q = 8 / std::gcd(tiles, (int64_t)8);
+  if (tiles <= SPLIT_XCD_MAX_TILES && s >= q) s -= s % q;
   const int64_t kps = ceil_div(steps, s) * lds::BK;
   p.splits = (int)ceil_div(K, kps);
   p.k_per_split = kps;

@@ -749,13 +749,13 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / TL::WN, wn = wave % TL::WN;
 
-  int tm, tn;
-  tile_coords(ceil_div(M, TL::BM), ceil_div(N, TL::BN), tm, tn);
+  int tm, tn, split;
+  split_tile_coords(ceil_div(M, TL::BM), ceil_div(N, TL::BN), tm, tn, split);
   const int64_t m0 = (int64_t)tm * TL::BM, n0 = (int64_t)tn * TL::BN;
 
   int64_t kbeg = 0, kend = K;
   if (ep.partial) {
-    kbeg = (int64_t)blockIdx.y * ep.k_per_split;
+    kbeg = (int64_t)split * ep.k_per_split;
     kend = kbeg + ep.k_per_split < K ? kbeg + ep.k_per_split : K;
   }
   const int nk = (int)((kend - kbeg) / BK);
@@ -809,7 +809,7 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
   const int64_t mb = m0 + wm * TL::WTM + (lane & 15);
   const int64_t nb = n0 + wn * TL::WTN + 4 * (lane >> 4);
   if (ep.partial) {
-    float* P = ep.partial + (int64_t)blockIdx.y * M * N;
+    float* P = ep.partial + (int64_t)split * M * N;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll

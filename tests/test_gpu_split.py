@@ -77,15 +77,6 @@ def test_gemm_split3_against_oracle(mdnn, layout):
         assert np.max(np.abs(got - exact)) * 64 < err16
 
 
-def _auto_scale(x):
-    """The header's rule for a scale chosen on the device: 2^(floor(log2
-    max|x|) - 14), 1 for a zero or non-finite maximum, at least 2^-126."""
-    mx = float(np.max(np.abs(x.astype(np.float64)))) if x.size else 0.0
-    if mx == 0.0 or not np.isfinite(mx):
-        return 1.0
-    return 2.0 ** max(int(np.floor(np.log2(mx))) - 14, -126)
-
-
 @pytest.mark.parametrize("case", ["large", "small", "subnormal", "zeros", "inf", "nan", "ragged"])
 def test_split_scale_chosen_on_device(mdnn, case):
     """scale 0: the library picks the power of two from max|x| on the device
@@ -103,7 +94,7 @@ def test_split_scale_chosen_on_device(mdnn, case):
         x[5, 7] = np.inf
     if case == "nan":
         x[rows - 1, cols - 1] = np.nan
-    want = _auto_scale(x)
+    want = ops.split_scale(x)
     assert {"large": 2.0 ** 7, "small": 2.0 ** -41, "zeros": 1.0, "inf": 1.0, "nan": 1.0,
             "subnormal": 2.0 ** -126}.get(case, want) == want
     hi, lo, s = mdnn.split_f16(dev(x, "f32"), 0.0)
@@ -125,7 +116,7 @@ def test_gemm_split3_alpha_beta_scales_and_aliasing(mdnn, auto):
     b = _fp32((k, n), 40, 2, -30, -26)                  # |b| ~ 2^-30: below fp16's normals
     c = _fp32((m, n), 40, 3)
     A, B = dev(a, "f32"), dev(b, "f32")
-    sa, sb = _auto_scale(a), _auto_scale(b)
+    sa, sb = ops.split_scale(a), ops.split_scale(b)
     assert sa == 2.0 ** 7 and sb == 2.0 ** -41
     D = dev(c, "f32")
     if auto:

@@ -69,10 +69,41 @@ def test_power_of_two_scale_and_sign(k):
     assert np.array_equal(hn, -h0) and np.array_equal(ln, -l0)
 
 
+@pytest.mark.parametrize("mx, want", [
+    (1.0, 2.0 ** -14),                 # 1 / 2^-14 = 2^14: the bottom of [2^14, 2^15)
+    (1.9990234375, 2.0 ** -14),        # just below 2: still exponent 0
+    (2.0, 2.0 ** -13),
+    (65504.0, 2.0),                    # fp16's largest finite value -> 32752
+    (65536.0, 4.0),
+    (-3.0, 2.0 ** -13),                # the magnitude decides
+    (1.5 * 2.0 ** -130, 2.0 ** -126),  # the floor: an fp32 subnormal maximum
+    (2.0 ** -112, 2.0 ** -126),        # exponent -126 exactly
+    (2.0 ** -111, 2.0 ** -125),
+    (0.0, 1.0), (np.inf, 1.0), (-np.inf, 1.0), (np.nan, 1.0),
+])
+def test_split_scale_rule(mx, want):
+    """The scale chosen for Eq. (1) when the caller leaves it open, on
+    hand-picked maxima (the other entries are smaller)."""
+    x = np.array([0.25 * abs(mx) if np.isfinite(mx) else 0.0, mx, 0.0])
+    assert ops.split_scale(x) == want
+
+
+def test_split_scale_puts_the_maximum_in_range():
+    """Property of the chosen scale on random data of any magnitude: the
+    largest |X| / s lies in [2^14, 2^15), a power of two, exact."""
+    g = np.random.default_rng(11)
+    for lo_e, hi_e in ((-100, -90), (-20, -5), (-1, 1), (10, 20), (100, 120)):
+        x = _fp32(g, 500, lo_e, hi_e)
+        s = ops.split_scale(x)
+        assert np.frexp(s)[0] == 0.5
+        r = np.max(np.abs(x)) / s
+        assert 2.0 ** 14 <= r < 2.0 ** 15
+
+
 def test_scale_brings_large_values_into_fp16_range():
     g = np.random.default_rng(8)
     x = _fp32(g, 1000, 20, 30)                     # far beyond fp16's range
-    s = 2.0 ** (int(np.floor(np.log2(np.max(np.abs(x))))) - 14)
+    s = ops.split_scale(x)
     hi, lo = ops.split_f16(x, s)
     assert np.max(np.abs(hi)) < F16_MAX
     rec = s * (hi + ops.SPLIT_SHIFT * lo)
