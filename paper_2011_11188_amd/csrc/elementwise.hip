@@ -301,13 +301,21 @@ softmax_xent_kernel(int64_t B, int64_t C, const float* __restrict__ z, int64_t l
 // Thread t sums the losses of rows t, t + 1024, ... in order; the block then
 // adds the 1024 partial sums in a fixed tree order.
 constexpr int SMALL_C = 32;
+constexpr size_t XENT_DB_LDS = 48 * 1024;  // the stored dz rows kept for the bias gradient
 
+// db (nullable, B <= LOSS_THREADS): also the column sums of the stored dz
+// (the classifier's bias gradient), kept as float in dynamic LDS [B][C], in
+// row order within 32 row segments and then segment order; nonfinite
+// (nullable) is set when one of them is Inf or NaN.
 template <class OutT>
 __global__ void __launch_bounds__(LOSS_THREADS)
 softmax_xent_rows_kernel(int64_t B, int64_t C, const float* __restrict__ z, int64_t ldl,
                          const int32_t* __restrict__ labels, const float* __restrict__ scale_p,
-                         float* __restrict__ loss_out, typename OutT::storage* __restrict__ dz, int64_t ldd) {
+                         float* __restrict__ loss_out, typename OutT::storage* __restrict__ dz, int64_t ldd,
+                         float* __restrict__ db, int32_t* __restrict__ nonfinite) {
   __shared__ float red[LOSS_THREADS];
+  __shared__ float seg_sum[SMALL_C][33];
+  extern __shared__ float dzs[];
   const float S = scale_p ? *scale_p : 1.0f;
   const float inv_b = 1.0f / (float)B;
   float acc = 0.0f;
@@ -332,7 +340,9 @@ softmax_xent_rows_kernel(int64_t B, int64_t C, const float* __restrict__ z, int6
       if (j < C) {
         float g = S * (expf(v[j] - lse) - (j == lab ? 1.0f : 0.0f)) * inv_b;
         if (!ok) g = NAN;
-        dz[r * ldd + j] = from_f<OutT>(g);
+        const typename OutT::storage q = from_f<OutT>(g);
+        dz[r * ldd + j] = q;
+        if (db) dzs[r * C + j] = to_f<OutT>(q);
       }
     }
     acc += ok ? (lse - zr[lab]) : NAN;
@@ -344,6 +354,35 @@ softmax_xent_rows_kernel(int64_t B, int64_t C, const float* __restrict__ z, int6
     __syncthreads();
   }
   if (threadIdx.x == 0) *loss_out = red[0] * inv_b;
+  if (!db) return;
+  // column j, segment t of ceil(B / 32) rows: thread 32 j + t
+  const int j = threadIdx.x >> 5, t = threadIdx.x & 31;
+  const int64_t seg = (B + 31) / 32;
+  if (j < C) {
+    float cs = 0.0f;
+    const int64_t r1 = (t + 1) * seg < B ? (t + 1) * seg : B;
+    // eight reads in flight, added in row order
+    for (int64_t r = t * seg; r < r1; r += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = dzs[(r + u < r1 ? r + u : r) * C + j];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (r + u < r1) cs += v[u];
+    }
+    seg_sum[j][t] = cs;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < C) {
+    float v[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) v[u] = seg_sum[threadIdx.x][u];
+    float tot = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 32; ++u) tot += v[u];
+    db[threadIdx.x] = tot;
+    if (nonfinite && !isfinite(tot)) atomicOr(nonfinite, 1);
+  }
 }
 
 template <class OutT>
@@ -722,6 +761,33 @@ extern "C" mdnn_status_t mdnn_maxpool2_bwd(int64_t n, int64_t h, int64_t w, int6
   return check_launch("maxpool2_bwd_kernel");
 }
 
+namespace mdnn {
+namespace {
+mdnn_status_t launch_xent_rows(int64_t B, int64_t C, const float* logits, int64_t ldl, const int32_t* labels,
+                               const float* loss_scale, float* loss_out, void* dlogits, int64_t ldd,
+                               mdnn_dtype_t t, float* db, int32_t* nonfinite, hipStream_t st) {
+  const size_t lds = db ? (size_t)B * C * sizeof(float) : 0;
+  switch (t) {
+    case MDNN_F32: hipLaunchKernelGGL(softmax_xent_rows_kernel<F32>, dim3(1), dim3(LOSS_THREADS), lds, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd, db, nonfinite); break;
+    case MDNN_F16: hipLaunchKernelGGL(softmax_xent_rows_kernel<F16>, dim3(1), dim3(LOSS_THREADS), lds, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd, db, nonfinite); break;
+    default: hipLaunchKernelGGL(softmax_xent_rows_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), lds, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd, db, nonfinite); break;
+  }
+  return check_launch("softmax_xent_rows_kernel");
+}
+}  // namespace
+
+bool softmax_xent_db_ok(int64_t B, int64_t C) {
+  return B >= 1 && B <= LOSS_THREADS && C >= 1 && C <= SMALL_C && (size_t)B * C * sizeof(float) <= XENT_DB_LDS;
+}
+
+mdnn_status_t softmax_xent_db(int64_t B, int64_t C, const float* logits, int64_t ldl, const int32_t* labels,
+                              const float* loss_scale, float* loss_out, void* dlogits, int64_t ldd, mdnn_dtype_t t,
+                              float* db, int32_t* nonfinite, hipStream_t st) {
+  if (!softmax_xent_db_ok(B, C)) return fail(MDNN_ERR_SHAPE, "softmax_xent_db: shape outside the fused kernel");
+  return launch_xent_rows(B, C, logits, ldl, labels, loss_scale, loss_out, dlogits, ldd, t, db, nonfinite, st);
+}
+}  // namespace mdnn
+
 extern "C" mdnn_status_t mdnn_softmax_xent(int64_t B, int64_t C, const float* logits, int64_t ldl,
                                            const int32_t* labels, const float* loss_scale,
                                            float* loss_out, void* dlogits, int64_t ldd,
@@ -735,14 +801,8 @@ extern "C" mdnn_status_t mdnn_softmax_xent(int64_t B, int64_t C, const float* lo
     return fail(MDNN_ERR_MISALIGNED, "softmax_xent: misaligned buffer");
   clear_error();
   hipStream_t st = as_stream(stream);
-  if (C <= SMALL_C) {
-    switch (dlogits_type) {
-      case MDNN_F32: hipLaunchKernelGGL(softmax_xent_rows_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd); break;
-      case MDNN_F16: hipLaunchKernelGGL(softmax_xent_rows_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
-      default: hipLaunchKernelGGL(softmax_xent_rows_kernel<BF16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;
-    }
-    return check_launch("softmax_xent_rows_kernel");
-  }
+  if (C <= SMALL_C) return launch_xent_rows(B, C, logits, ldl, labels, loss_scale, loss_out, dlogits, ldd,
+                                            dlogits_type, nullptr, nullptr, st);
   switch (dlogits_type) {
     case MDNN_F32: hipLaunchKernelGGL(softmax_xent_kernel<F32>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (float*)dlogits, ldd); break;
     case MDNN_F16: hipLaunchKernelGGL(softmax_xent_kernel<F16>, dim3(1), dim3(LOSS_THREADS), 0, st, B, C, logits, ldl, labels, loss_scale, loss_out, (uint16_t*)dlogits, ldd); break;

@@ -274,8 +274,23 @@ colsum_single_kernel(const typename T::storage* __restrict__ x, const typename T
   const int cx = threadIdx.x & 31, ry = threadIdx.x >> 5;
   const int64_t col = (int64_t)blockIdx.x * 32 + cx;
   float s = 0.0f;
-  if (col < cols)
-    for (int64_t r = ry; r < rows; r += 8) s += masked_val<T>(x, y, r * cols + col);
+  if (col < cols) {
+    int64_t r = ry;
+    // eight of this thread's rows in flight, added in row order (a load per
+    // dependent add had left the kernel waiting on memory once per row)
+    for (; r + 56 < rows; r += 64) {
+      float v[8], keep[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t i = (r + 8 * u) * cols + col;
+        v[u] = to_f<T>(x[i]);
+        keep[u] = y ? to_f<T>(y[i]) : 1.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += keep[u] > 0.0f ? v[u] : 0.0f;
+    }
+    for (; r < rows; r += 8) s += masked_val<T>(x, y, r * cols + col);
+  }
   part[ry][cx] = s;
   __syncthreads();
   if (ry == 0 && col < cols) {
@@ -450,11 +465,58 @@ reduce_splits_epilogue_kernel(const float* __restrict__ part, int splits, int64_
   epilogue_store4<MaskT, OutT>(ep, M, N, m, n, tot);
 }
 
+// At most 8 splits: one thread per output quad adds the splits in split
+// order, four in flight at a time.  The grouped kernel above gives each of
+// its groups one split in that case and then adds the groups in order, so
+// the sums are the same; this one keeps every thread busy instead of one in
+// sixteen (a 256 x 3136 output over 3 splits: 11.6 -> 4.2 us, 256 x 1024
+// over 7: 6.1 -> 3.9 us).  With 16 splits its four rounds of loads were
+// slower than the grouped kernel's one (1024 x 10: 6.8 against 5.0 us).
+constexpr int REDUCE_SEQ_MAX_SPLITS = 8;
+template <class MaskT, class OutT>
+__global__ void __launch_bounds__(256)
+reduce_splits_seq_kernel(const float* __restrict__ part, int splits, int64_t M, int64_t N, Epilogue ep) {
+  const int64_t groups = ceil_div(N, 4);
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= M * groups) return;
+  const int64_t m = q / groups, n = (q - m * groups) * 4;
+  const int64_t MN = M * N;
+  const bool vec = (N & 3) == 0;  // rows of 16-byte aligned quads (the workspace is 16-byte aligned)
+  const float* p = part + m * N + n;
+  float4_t acc = {0.f, 0.f, 0.f, 0.f};
+  auto load = [&](int sp) -> float4_t {
+    const float* ps = p + (int64_t)sp * MN;
+    if (vec) {
+      const float4 t = *(const float4*)ps;
+      return (float4_t){t.x, t.y, t.z, t.w};
+    }
+    float4_t v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = n + e < N ? ps[e] : 0.0f;
+    return v;
+  };
+  int s = 0;
+  for (; s + 4 <= splits; s += 4) {
+    float4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = load(s + u);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc += v[u];
+  }
+  for (; s < splits; ++s) acc += load(s);
+  epilogue_store4<MaskT, OutT>(ep, M, N, m, n, acc);
+}
+
 template <class MaskT, class OutT>
 static mdnn_status_t reduce_epilogue(const void* ws, int splits, int64_t M, int64_t N, const Epilogue& ep,
                                      hipStream_t st) {
   const int64_t quads = M * ceil_div(N, 4);
   if (ceil_div(quads, 16) > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the reduction");
+  if (splits <= REDUCE_SEQ_MAX_SPLITS) {
+    hipLaunchKernelGGL((reduce_splits_seq_kernel<MaskT, OutT>), dim3((unsigned)ceil_div(quads, 256)), dim3(256), 0,
+                       st, (const float*)ws, splits, M, N, ep);
+    return check_launch("reduce_splits_seq_kernel");
+  }
   hipLaunchKernelGGL((reduce_splits_epilogue_kernel<MaskT, OutT>), dim3((unsigned)ceil_div(quads, 16)), dim3(256),
                      0, st, (const float*)ws, splits, M, N, ep);
   return check_launch("reduce_splits_epilogue_kernel");

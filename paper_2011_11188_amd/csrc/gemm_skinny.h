@@ -8,8 +8,8 @@
 namespace mdnn {
 
 // Whether D = op(A) op(B) may run on the skinny kernels: K <= 4 (any
-// layout), N <= 4 with A K-contiguous (NN / NT, B staged in 64 KB of LDS),
-// or TN with N <= 16.  Never while a tile override is set (those force the
+// layout), N <= 4 with A K-contiguous (NN / NT, B staged in 64 KB of LDS;
+// N <= 16 when M <= 2048), or TN with N <= 16.  Never while a tile override is set (those force the
 // MFMA kernels).  skinny_takes: whether it does, given the workspace.
 bool skinny_applies(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K);
 bool skinny_takes(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, const void* ws, size_t ws_bytes);

@@ -5,9 +5,9 @@
 // the large operand, so these kernels read it once with wide loads on the
 // vector ALUs, accumulate in fp32 and reduce in a fixed order (deterministic).
 //
-//   rows  (A K-contiguous, N <= 4): B is staged in LDS as [N][K]; one wave
-//         (or four, when rows are few) per output row, 8 consecutive k per
-//         lane, butterfly sum per column.
+//   rows  (A K-contiguous, N <= 4, or N <= 16 on at most 2048 rows): B is
+//         staged in LDS as [N][K]; one wave (or four, when rows are few) per
+//         output row, 8 consecutive k per lane, butterfly sum per column.
 //   cols  (TN, N <= 16): a lane owns MB consecutive m, the block's four waves
 //         take every fourth k of the block's K range and are combined in wave
 //         order; with a workspace K is split across blocks into fp32 partials
@@ -29,7 +29,9 @@ template <> constexpr mdnn_dtype_t code_of<F16>() { return MDNN_F16; }
 template <> constexpr mdnn_dtype_t code_of<BF16>() { return MDNN_BF16; }
 
 constexpr int NMAX = 16;          // widest "skinny" N
+constexpr int KMAX_DEPTH = 4;     // deepest product of the depth kernel
 constexpr size_t ROWS_LDS = 65536;
+constexpr int64_t ROWS_WIDE_MAX_M = 2048;  // 4 < N <= 16: few rows only
 
 template <class T>
 __device__ __forceinline__ float ldf(const typename T::storage* p) { return to_f<T>(*p); }
@@ -95,12 +97,44 @@ __device__ __forceinline__ void rows_chunk(const float (&a)[8], const float* Bs,
 template <class T, class OutT, bool B_NK, int WPR>
 __global__ void __launch_bounds__(256)
 skinny_rows_kernel(const typename T::storage* __restrict__ A, int64_t lda, const typename T::storage* __restrict__ B,
-                   int64_t ldb, int64_t M, int N, int K, int Kp, bool vec, Epilogue ep) {
+                   int64_t ldb, int64_t M, int N, int K, int Kp, bool vec, bool vec_b, Epilogue ep) {
   extern __shared__ float Bs[];  // [N][Kp], zero beyond K
   __shared__ float part[4][NMAX];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (vec_b) {
+    // B's K x N (NN, ldb = N) or N x K (NT, ldb = K) elements are one
+    // 16-byte aligned run: eight per load, all of a thread's loads in flight
+    // (Kp = K here, a multiple of 8)
+    constexpr int VB = 16 / sizeof(typename T::storage);
+    const int nv = N * K / VB;
+    for (int base = 0; base < nv; base += 4 * 256) {
+      float v[4][VB];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = base + u * 256 + tid;
+        const int ic = i < nv ? i : 0;
+        if constexpr (VB == 8) {
+          load8<T>(B + (int64_t)ic * 8, v[u]);
+        } else {
+          const float4 q = *(const float4*)(B + (int64_t)ic * 4);
+          v[u][0] = q.x, v[u][1] = q.y, v[u][2] = q.z, v[u][3] = q.w;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = base + u * 256 + tid;
+        if (i < nv)
+#pragma unroll
+          for (int e = 0; e < VB; ++e) {
+            const int f = i * VB + e;  // flat index into B's run
+            const int k = B_NK ? f % K : f / N, n = B_NK ? f / K : f % N;
+            Bs[n * Kp + k] = v[u][e];
+          }
+      }
+    }
+  }
   // eight loads per thread in flight, then their stores
-  for (int base = 0; base < N * Kp; base += 8 * 256) {
+  for (int base = 0; base < N * Kp && !vec_b; base += 8 * 256) {
     float v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -469,7 +503,7 @@ template <class T, class OutT>
 mdnn_status_t launch_skinny(mdnn_layout_t layout, const void* A, int64_t lda, const void* B, int64_t ldb, int64_t M,
                             int64_t N, int64_t K, const Epilogue& ep, void* ws, size_t ws_bytes, hipStream_t st) {
   typedef typename T::storage S;
-  if (K <= 4) {
+  if (K <= KMAX_DEPTH) {
     const int64_t bx = ceil_div(ceil_div(N, 8), 256);
     if (bx > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "gemm: problem too large for the launch grid");
     // about 2048 blocks in all, each over several rows
@@ -498,13 +532,15 @@ mdnn_status_t launch_skinny(mdnn_layout_t layout, const void* A, int64_t lda, co
   const int kp = (int)ceil_div(K, 8) * 8;
   const size_t lds = (size_t)N * kp * sizeof(float);
   const bool vec = K % 8 == 0 && lda % 8 == 0 && aligned(A, 16);
+  // B one contiguous run: NN with ldb = N, NT with ldb = K
+  const bool vec_b = K % 8 == 0 && aligned(B, 16) && ldb == (layout == MDNN_NT ? K : N);
   // fewer than 2048 rows: four waves per row (each a quarter of the chunks)
   const bool share = M < 2048 && K >= 1024;
   int64_t blocks = share ? M : ceil_div(M, 4);
   if (blocks > 1024) blocks = 1024;
 #define MDNN_ROWS(NK, WPR)                                                                                          \
   hipLaunchKernelGGL((skinny_rows_kernel<T, OutT, NK, WPR>), dim3((unsigned)blocks), dim3(256), lds, st, (const S*)A, \
-                     lda, (const S*)B, ldb, M, (int)N, (int)K, kp, vec, ep)
+                     lda, (const S*)B, ldb, M, (int)N, (int)K, kp, vec, vec_b, ep)
   if (layout == MDNN_NT) {
     if (share) MDNN_ROWS(true, 4); else MDNN_ROWS(true, 1);
   } else {
@@ -517,26 +553,29 @@ mdnn_status_t launch_skinny(mdnn_layout_t layout, const void* A, int64_t lda, co
 }  // namespace
 
 // Measured against the MFMA kernels (with their workspace split): the depth
-// kernel wins for K <= 4 (K = 10 is a tie), the rows kernel for N <= 4 (with
-// N = 10 its per-block staging of B costs more than it saves), the cols
-// kernel for N <= 16 when it can split K over a workspace or the grid is
-// already wide.
+// kernel wins for K <= 4 (K = 10 is a tie; a K <= 16 instantiation took
+// 12.5 us against 11.8 for 256 x 1024 x 10), the rows kernel for N <= 4 and,
+// with B staged by 16-byte loads, for N <= 16 on few rows (256 x 10 x 1024:
+// 13.2 us in one launch against 9.8 + 4.4 for the split MFMA product and its
+// reduction), the cols kernel for N <= 16 when it can split K over a
+// workspace or the grid is already wide.
 bool skinny_applies(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K) {
   if (gemm_tile_override() != 0 || M <= 0 || N <= 0 || K <= 0) return false;
-  if (K <= 4) return true;
+  if (K <= KMAX_DEPTH) return true;
   if (layout == MDNN_TN) return N <= NMAX;
-  return N <= 4 && K <= 0x7fffffff - 8 && (size_t)N * ceil_div(K, 8) * 8 * sizeof(float) <= ROWS_LDS;
+  return N <= NMAX && K <= 0x7fffffff - 8 && (size_t)N * ceil_div(K, 8) * 8 * sizeof(float) <= ROWS_LDS &&
+         (N <= 4 || M <= ROWS_WIDE_MAX_M);
 }
 
 size_t skinny_ws_bytes(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K) {
-  if (!skinny_applies(layout, M, N, K) || K <= 4 || layout != MDNN_TN) return 0;
+  if (!skinny_applies(layout, M, N, K) || K <= KMAX_DEPTH || layout != MDNN_TN) return 0;
   const SplitPlan p = cols_plan(M, K, cols_mb(N));
   return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
 }
 
 bool skinny_takes(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K, const void* ws, size_t ws_bytes) {
   if (!skinny_applies(layout, M, N, K)) return false;
-  if (layout != MDNN_TN || K <= 4) return true;
+  if (layout != MDNN_TN || K <= KMAX_DEPTH) return true;
   // the cols kernel alone runs ceil(M / (64 MB)) workgroups: without its K
   // split it only pays off on a wide grid
   const int mb = cols_mb(N);

@@ -60,6 +60,15 @@ mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t 
 // stores).  Deterministic, but not bitwise the same as column_sums where
 // the chunks differ.
 int64_t column_sums_chunks(int64_t rows, int64_t cols, mdnn_dtype_t t);
+
+// mdnn_softmax_xent (C <= 32) that also writes db[C], the column sums of the
+// stored dlogits (the classifier layer's bias gradient), in one launch;
+// nonfinite (nullable) is set when a sum is Inf or NaN.  Shapes:
+// softmax_xent_db_ok (B <= 1024 and B * C floats within the kernel's LDS).
+bool softmax_xent_db_ok(int64_t B, int64_t C);
+mdnn_status_t softmax_xent_db(int64_t B, int64_t C, const float* logits, int64_t ldl, const int32_t* labels,
+                              const float* loss_scale, float* loss_out, void* dlogits, int64_t ldd, mdnn_dtype_t t,
+                              float* db, int32_t* nonfinite, hipStream_t st);
 mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, int64_t cols, float* partial,
                                   hipStream_t stream);
 constexpr int kMaxColsumBatch = 32;

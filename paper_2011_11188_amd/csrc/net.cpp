@@ -311,16 +311,24 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
   char* gnxt = ws + net->g1_off;
   const LayerPlan& last = net->layers.back();
   const float* out = (const float*)act_ptr(net->layers.size());
+  // FC weight gradients (and bias gradients) checked for the loss scaler as they are stored
+  int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
+  // a classifier head's bias gradient comes out of the loss kernel itself
+  const bool head_db = net->cfg.loss == MDNN_LOSS_XENT && last.L.kind == MDNN_LAYER_FC &&
+                       softmax_xent_db_ok(B, last.out_feat) && (nonfinite || !net->scaler || async);
   if (net->cfg.loss == MDNN_LOSS_XENT) {
-    MDNN_TRY(mdnn_softmax_xent(B, last.out_feat, out, last.out_feat, (const int32_t*)target, scale,
-                               loss_out, gcur, last.out_feat, lp, stream));
+    if (head_db)
+      MDNN_TRY(softmax_xent_db(B, last.out_feat, out, last.out_feat, (const int32_t*)target, scale, loss_out, gcur,
+                               last.out_feat, lp, net->grads + last.b_off, nonfinite, as_stream(stream)));
+    else
+      MDNN_TRY(mdnn_softmax_xent(B, last.out_feat, out, last.out_feat, (const int32_t*)target, scale,
+                                 loss_out, gcur, last.out_feat, lp, stream));
   } else {
     MDNN_TRY(mdnn_mse_loss(B, last.out_feat, out, (const float*)target, scale, loss_out, gcur, lp,
                            stream));
   }
 
-  // backward (FC weight gradients checked for the loss scaler as they are stored)
-  int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
+  // backward
   // loss-scaled FC bias gradients: partial column sums per layer now, all
   // layers finished (and checked) in one launch after the loop
   ColsumBatch bias_sums{};
@@ -332,11 +340,10 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     const void* mask = p.input_relu ? (const void*)a_in : nullptr;
     if (p.L.kind == MDNN_LAYER_FC) {
       const int64_t in = p.L.c_in, o = p.L.c_out;
-      // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
-      MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
-                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
-                             nonfinite));
-      if (nonfinite) {
+      // bias gradient first, while dZ (just written) is still in the caches
+      if (head_db && ii + 1 == net->layers.size()) {
+        // done by the loss kernel
+      } else if (nonfinite) {
         float* part = (float*)(ws + p.cs_off);
         MDNN_TRY(column_sums_partial(gcur, lp, B, o, part, as_stream(stream)));
         if (bias_sums.n == kMaxColsumBatch) {
@@ -352,6 +359,10 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
         MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, ws + net->fws_off,
                                    net->fws_bytes, stream));
       }
+      // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
+      MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
+                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
+                             nonfinite));
       if (ii > 0) {
         // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
         MDNN_TRY(gemm_mixed_ws(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0, gnxt, in, lp,
