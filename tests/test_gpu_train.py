@@ -244,3 +244,71 @@ def test_wide_mlp_first_layer_gradients_from_stored_values(mdnn, size):
     act1 = stored(net.activation_ptr(1), batch * cfg.layers[0].c_out).reshape(batch, -1)
     assert np.all(dz[0][act1 <= 0] == 0)
     assert mdnn.read_scaler(net.scaler)["good_steps"] == 1
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("case", ["lenet_bf16", "mlp784_fp32", "mlp_f16_scaled", "mlp_bf16_b1000"])
+def test_classifier_head_from_stored_values(mdnn, case):
+    """The classifier head of one step (cross-entropy over <= 32 classes: the
+    loss kernel also sums the bias gradient from the dZ it stores), checked on
+    the GPU's own stored logits, labels and layer input: dZ = S (softmax -
+    onehot) / B rounded once to the storage type, the loss the batch mean of
+    logsumexp - z[label], db = column sums of the stored dZ and dW = X^T dZ
+    (bar gamma_B * sum |terms|, plus one storage step wherever fp32 softmax
+    arithmetic may round dZ either way).  Cases: LeNet bf16 (batch 256), the
+    fp32 MLP, an fp16 MLP with dynamic loss scaling (the bias sums carry the
+    overflow test), and 1000 rows (most of the kernel's 1024 threads, ragged
+    row segments)."""
+    import dataclasses
+    import torch
+    from oracle.rounding import round_to
+    from tests.helpers import accum_bound
+    cfg = {"lenet_bf16": W.lenet_bf16(), "mlp784_fp32": W.mlp784_fp32(),
+           "mlp_f16_scaled": dataclasses.replace(W.mlp784_fp32(), dtype="f16", loss_scaling=True,
+                                                 init_scale=2.0 ** 10),
+           "mlp_bf16_b1000": dataclasses.replace(W.mlp784_fp32(), dtype="bf16", batch=1000)}[case]
+    net = _gpu_net(mdnn, cfg)
+    x, t = W.batch_inputs(cfg, 0)
+    loss = float(net.step(dev(x, "f32"), _target(cfg, t)).item())
+    torch.cuda.synchronize()
+    B, L = cfg.batch, len(cfg.layers)
+    C, K = cfg.layers[-1].c_out, cfg.layers[-1].c_in
+    es = 4 if cfg.dtype == "f32" else 2
+    st = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[cfg.dtype]
+
+    def stored(ptr, n, typ=st, size=es):
+        off = ptr - net.ws.data_ptr()
+        return net.ws[off:off + size * n].clone().view(typ).float().cpu().numpy().astype(np.float64)
+
+    a = stored(net.activation_ptr(L - 1), B * K).reshape(B, K)
+    z = stored(net.activation_ptr(L), B * C, torch.float32, 4).reshape(B, C)
+    scale = cfg.init_scale if cfg.loss_scaling else 1.0
+    zmax = z.max(axis=1, keepdims=True)
+    lse = zmax[:, 0] + np.log(np.exp(z - zmax).sum(axis=1))
+    p = np.exp(z - lse[:, None])
+    onehot = np.zeros_like(p)
+    onehot[np.arange(B), t] = 1.0
+    want = scale * (p - onehot) / B
+    # fp32 softmax arithmetic (exp, log, a product and a difference) before
+    # the one rounding: a few fp32 ulps of the terms
+    tol = 16 * 2.0 ** -24 * (np.abs(scale * p / B) + np.abs(want)) + 1e-38
+    lo = round_to(want - tol, cfg.dtype) if cfg.dtype != "f32" else want - tol
+    hi = round_to(want + tol, cfg.dtype) if cfg.dtype != "f32" else want + tol
+    if L == 2:
+        # the head's dZ buffer is not reused by a later layer: check it and use it
+        d = stored(net.output_grad_ptr(0), B * C).reshape(B, C)
+        assert np.all((d >= lo) & (d <= hi)), "dZ"
+        slack = np.zeros_like(d)
+    else:
+        d = round_to(want, cfg.dtype)
+        slack = hi - lo
+    assert abs(loss - float(np.mean(lse - z[np.arange(B), t]))) <= 1e-5 * abs(loss)
+    g = net.grads.cpu().numpy().astype(np.float64)
+    wo, bo = cfg.param_offsets()[-1]
+    db = g[bo:bo + C]
+    dw = g[wo:wo + K * C].reshape(K, C)
+    assert np.all(np.abs(db - d.sum(axis=0)) <= accum_bound(np.abs(d).sum(axis=0), B + 1) + slack.sum(axis=0)), "db"
+    assert np.all(np.abs(dw - a.T @ d) <= accum_bound(np.abs(a).T @ np.abs(d), B + 1) + np.abs(a).T @ slack), "dW"
+    assert np.any(db != 0)
+    if cfg.loss_scaling:
+        assert mdnn.read_scaler(net.scaler)["good_steps"] == 1
