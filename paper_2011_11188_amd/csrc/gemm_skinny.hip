@@ -310,6 +310,51 @@ skinny_depth_kernel(mdnn_layout_t layout, const typename T::storage* __restrict_
 #pragma unroll
     for (int k = 0; k < KT; ++k)
       b[e][k] = ldz<T>(B, layout == MDNN_NT ? (n + e) * ldb + k : (int64_t)k * ldb + n + e, k < K && n + e < N);
+  // a ReLU mask with nothing else after the product (back-propagation into a
+  // hidden layer): four of this thread's rows with their mask runs loaded
+  // before any is stored, the mask applied before the epilogue (alpha * 0 is
+  // still 0).  A row at a time, each mask load waited for behind the previous
+  // row's stores, had left the 4096 x 4096 outer product at 3 TB/s.
+  if (full && ep.mask && ep.beta == 0.0f && !ep.bias && ep.act == MDNN_ACT_NONE && (ep.ldm & 7) == 0 &&
+      ((uintptr_t)ep.mask & 15) == 0) {
+    constexpr int RB = 4;
+    Epilogue e2 = ep;
+    e2.mask = nullptr;
+    const typename T::storage* mk = (const typename T::storage*)ep.mask;
+    for (int64_t m0 = blockIdx.y; m0 < M; m0 += RB * (int64_t)gridDim.y) {
+      float a[RB][KT], mv[RB][8];
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const int64_t m = m0 + r * (int64_t)gridDim.y, mm = m < M ? m : m0;
+#pragma unroll
+        for (int k = 0; k < KT; ++k)
+          a[r][k] = ldz<T>(A, layout == MDNN_TN ? (int64_t)k * lda + mm : mm * lda + k, k < K);
+        load8<T>(mk + mm * ep.ldm + n, mv[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const int64_t m = m0 + r * (int64_t)gridDim.y;
+        if (m >= M) break;
+        float4_t lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < KT; ++k) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            lo[e] = fmaf(a[r][k], b[e][k], lo[e]);
+            hi[e] = fmaf(a[r][k], b[4 + e][k], hi[e]);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (!(mv[r][e] > 0.0f)) lo[e] = 0.0f;
+          if (!(mv[r][4 + e] > 0.0f)) hi[e] = 0.0f;
+        }
+        epilogue_store4<T, OutT, true>(e2, M, N, m, n, lo);
+        epilogue_store4<T, OutT, true>(e2, M, N, m, n + 4, hi);
+      }
+    }
+    return;
+  }
   for (int64_t m = blockIdx.y; m < M; m += gridDim.y) {
     float a[KT];
 #pragma unroll

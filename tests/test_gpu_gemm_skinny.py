@@ -17,8 +17,8 @@ import pytest
 
 import workloads as W
 from oracle import ops
-from oracle.rounding import decode
-from tests.helpers import DT, accum_bound, dev, empty, host64, lowp_close, norm_max_err
+from oracle.rounding import decode, round_to
+from tests.helpers import DT, accum_bound, dev, empty, host64, lowp_close, norm_max_err, ulp
 
 pytestmark = pytest.mark.gpu
 
@@ -131,3 +131,47 @@ def test_skinny_strided_operands(mdnn):
     want = ops.gemm("TN", decode(at, "bf16")[:, 1:m + 1], decode(bt, "bf16")[:, :n])
     assert norm_max_err(got, want) <= TOL
     del torch
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("mnk", [(1001, 4096, 1), (4096, 4100, 3), (37, 64, 2)], ids=["ragged_m", "ragged_n", "small"])
+def test_skinny_depth_relu_mask_rows_in_flight(mdnn, dt, layout, mnk):
+    """The outer-product kernel (K <= 4) with only a ReLU mask after the
+    product and contiguous 8-aligned rows: four rows' mask runs loaded ahead
+    of their stores (rows beyond M, and columns past the last whole run of
+    eight, on the row-at-a-time path).  Masked entries are 0 even where the
+    incoming gradient is Inf."""
+    m, n, k = mnk
+    sa, sb = _shapes(layout, m, n, k)
+    a = W.normal(sa, 43, 1, dt, 1.0)
+    b = W.normal(sb, 43, 2, dt)
+    y_in = W.normal((m, n), 43, 3, dt)
+    a64, b64 = decode(a, dt), decode(b, dt)
+    # an Inf in A: its products are masked to 0 wherever y_in <= 0
+    ai = np.array(a, copy=True)
+    inf = 0x7F80 if dt == "bf16" else np.inf  # bf16 is stored as bit patterns
+    if layout == "TN":
+        ai[0, 5] = inf
+    else:
+        ai[5, 0] = inf
+    a64i = decode(ai, dt)
+    got = _run(mdnn, layout, dev(ai, dt), dev(b, dt), dt, m, n, k, mask=dev(y_in, dt))
+    # the same product with a padded output row (the row-at-a-time path): the same bits
+    slow = _run(mdnn, layout, dev(ai, dt), dev(b, dt), dt, m, n, k, mask=dev(y_in, dt), ld_pad=3)
+    same = (got == slow) | (np.isnan(got) & np.isnan(slow))
+    assert np.all(same), [(i, got.flat[i], slow.flat[i]) for i in np.flatnonzero(~same)[:5]]
+    keep = decode(y_in, dt) > 0
+    with np.errstate(invalid="ignore"):
+        prod = ops.gemm(layout, a64i, b64)
+    exact = np.where(keep, prod, 0.0)
+    assert np.all(got[~keep] == 0)
+    fin = np.isfinite(exact)
+    err = accum_bound(ops.gemm(layout, np.abs(a64), np.abs(b64)), k)
+    if dt == "f32":
+        assert np.all(np.abs(got[fin] - exact[fin]) <= err[fin] + 1e-30)
+    else:
+        ok = np.abs(got[fin] - round_to(exact[fin], dt)) <= ulp(np.abs(exact[fin]), dt) + err[fin]
+        bad = np.flatnonzero(~ok)[:5]
+        assert lowp_close(got[fin], exact[fin], dt, err[fin]), [(got[fin][i], exact[fin][i]) for i in bad]
+    assert np.all(~np.isfinite(got[~fin])) and np.all(np.sign(got[~fin]) == np.sign(exact[~fin]))
