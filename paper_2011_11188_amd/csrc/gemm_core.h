@@ -343,10 +343,11 @@ __device__ __forceinline__ bool full_tile_epilogue(const Epilogue& ep, bool insi
 // FULL: the caller guarantees m < M, n + 4 <= N and 4-element vector access
 // to every operand the epilogue touches (vec4, vec4_c when beta != 0, vec4_m
 // with a mask, a 16-byte aligned bias), so no per-lane bound is tested and
-// the code is straight-line.
+// the code is straight-line.  mv (FULL only, nullable): the four mask values,
+// loaded by the caller.
 template <class MaskT, class OutT, bool FULL = false>
 __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, int64_t N, int64_t m,
-                                                int64_t n, float4_t acc) {
+                                                int64_t n, float4_t acc, const float* mv_in = nullptr) {
   if (!FULL && m >= M) return;
   float v[4] = {acc[0], acc[1], acc[2], acc[3]};
   const bool in4 = FULL || n + 4 <= N;
@@ -385,7 +386,11 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
   }
   if (ep.mask) {
     const typename MaskT::storage* mk = (const typename MaskT::storage*)ep.mask + m * ep.ldm + n;
-    if (FULL || (ep.vec4_m && in4)) {
+    if (FULL && mv_in) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (!(mv_in[e] > 0.0f)) v[e] = 0.0f;
+    } else if (FULL || (ep.vec4_m && in4)) {
       float mv[4];
       load4<MaskT>(mk, mv);
 #pragma unroll

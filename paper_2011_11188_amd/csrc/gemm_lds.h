@@ -829,6 +829,29 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
   }
   // interior tiles with 4-aligned rows everywhere take the straight-line store
   if (full_tile_epilogue(ep, m0 + TL::BM <= M && n0 + TL::BN <= N, N)) {
+    if (ep.mask) {
+      // every mask quad of this wave in flight before the first store: one
+      // round trip instead of one per fragment, each of which had waited for
+      // its load behind the previous fragment's stores (4096^3 backward data
+      // with the ReLU mask: 113.2 against 104.0 us without it)
+      typedef typename T::storage S;
+      static_assert(sizeof(S) == 2, "16-bit operands and mask");
+      uint2 mq[FM][FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          mq[i][j] = *(const uint2*)((const S*)ep.mask + (mb + i * 16) * ep.ldm + nb + j * 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const float mv[4] = {to_f<T>((S)(mq[i][j].x & 0xffffu)), to_f<T>((S)(mq[i][j].x >> 16)),
+                               to_f<T>((S)(mq[i][j].y & 0xffffu)), to_f<T>((S)(mq[i][j].y >> 16))};
+          epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], mv);
+        }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
