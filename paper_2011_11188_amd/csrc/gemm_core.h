@@ -343,11 +343,12 @@ __device__ __forceinline__ bool full_tile_epilogue(const Epilogue& ep, bool insi
 // FULL: the caller guarantees m < M, n + 4 <= N and 4-element vector access
 // to every operand the epilogue touches (vec4, vec4_c when beta != 0, vec4_m
 // with a mask, a 16-byte aligned bias), so no per-lane bound is tested and
-// the code is straight-line.  mv (FULL only, nullable): the four mask values,
-// loaded by the caller.
+// the code is straight-line.  mv_in / bias_in (FULL only, nullable): the four
+// mask values / bias values, loaded by the caller.
 template <class MaskT, class OutT, bool FULL = false>
 __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, int64_t N, int64_t m,
-                                                int64_t n, float4_t acc, const float* mv_in = nullptr) {
+                                                int64_t n, float4_t acc, const float* mv_in = nullptr,
+                                                const float* bias_in = nullptr) {
   if (!FULL && m >= M) return;
   float v[4] = {acc[0], acc[1], acc[2], acc[3]};
   const bool in4 = FULL || n + 4 <= N;
@@ -371,7 +372,10 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
     }
   }
   if (ep.bias) {
-    if (FULL || (in4 && ((uintptr_t)(ep.bias + n) & 15) == 0)) {
+    if (FULL && bias_in) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += bias_in[e];
+    } else if (FULL || (in4 && ((uintptr_t)(ep.bias + n) & 15) == 0)) {
       const float4 b = *(const float4*)(ep.bias + n);
       v[0] += b.x, v[1] += b.y, v[2] += b.z, v[3] += b.w;
     } else {

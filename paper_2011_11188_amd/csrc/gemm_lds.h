@@ -829,6 +829,15 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
   }
   // interior tiles with 4-aligned rows everywhere take the straight-line store
   if (full_tile_epilogue(ep, m0 + TL::BM <= M && n0 + TL::BN <= N, N)) {
+    // the bias quads of this wave's columns, loaded once before any store
+    float bq[FN][4];
+    if (ep.bias) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const float4 b = *(const float4*)(ep.bias + nb + j * 16);
+        bq[j][0] = b.x, bq[j][1] = b.y, bq[j][2] = b.z, bq[j][3] = b.w;
+      }
+    }
     if (ep.mask) {
       // every mask quad of this wave in flight before the first store: one
       // round trip instead of one per fragment, each of which had waited for
@@ -848,14 +857,17 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
         for (int j = 0; j < FN; ++j) {
           const float mv[4] = {to_f<T>((S)(mq[i][j].x & 0xffffu)), to_f<T>((S)(mq[i][j].x >> 16)),
                                to_f<T>((S)(mq[i][j].y & 0xffffu)), to_f<T>((S)(mq[i][j].y >> 16))};
-          epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], mv);
+          epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], mv,
+                                         ep.bias ? bq[j] : nullptr);
         }
       return;
     }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j) epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j]);
+      for (int j = 0; j < FN; ++j)
+        epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], nullptr,
+                                       ep.bias ? bq[j] : nullptr);
     return;
   }
 #pragma unroll
