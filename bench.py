@@ -296,9 +296,11 @@ def _replay_group(mdnn, net, cfg, group, reps):
             calls.append((1, M, N, K, g0, K, wptr, K, g1, N, lp, None, 0,
                           a_in, N))
     flops = sum(2.0 * c[1] * c[2] * c[3] for c in calls) / len(calls)
-    # one event pair around each replayed launch (the launches are queued
-    # ahead of the GPU, so each pair brackets that kernel's execution alone,
-    # as a kernel trace reports it, not the gaps between kernels)
+    # one event pair around the timed replay: reps x the group's launches back
+    # to back, queued behind a bounded spin kernel so that the GPU never waits
+    # for the host; the mean launch duration is the elapsed time over the
+    # launches (an event pair around every launch added about 5 us to each,
+    # against the kernel trace's durations of the same launches)
     import torch
     # the step's split-K workspace and, for the weight gradients, its loss
     # scaler's overflow flag: the replay takes the kernel paths the step takes
@@ -314,22 +316,16 @@ def _replay_group(mdnn, net, cfg, group, reps):
         for c in calls:
             launch(c)
     torch.cuda.synchronize()
-    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(reps * len(calls))]
-    # a bounded spin ahead of the timed launches keeps the GPU busy while the
-    # host queues them all, so short kernels are not timed waiting for their
-    # own submission
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     if hasattr(torch.cuda, "_sleep"):
         torch.cuda._sleep(4_000_000)
-    k = 0
+    e0.record()
     for _ in range(reps):
         for c in calls:
-            pairs[k][0].record()
             launch(c)
-            pairs[k][1].record()
-            k += 1
+    e1.record()
     torch.cuda.synchronize()
-    return sum(e0.elapsed_time(e1) for e0, e1 in pairs) / len(pairs), flops
+    return e0.elapsed_time(e1) / (reps * len(calls)), flops
 
 
 def _gemm_sweep(mdnn, reps_scale=1.0):
