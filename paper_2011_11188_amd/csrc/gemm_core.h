@@ -432,6 +432,53 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
   }
 }
 
+// The interior epilogue of a wave's FM x FN fragments (16-bit operands; the
+// caller has checked full_tile_epilogue): the loads the stores depend on are
+// issued before the first store -- the bias quads of the wave's columns once
+// (rather than once per fragment) and every ReLU-mask quad of the wave (one
+// round trip instead of one per fragment, each of which had waited for its
+// load behind the previous fragment's stores).  In the 4096-wide MLP step:
+// 3 us per forward product (bias), the mask of a 4096^3 backward data
+// product 9.2 -> 6.4 us (its 32 MB read at the end of the tile).
+template <class T, class OutT, int FM, int FN>
+__device__ __forceinline__ void epilogue_interior(const Epilogue& ep, int64_t M, int64_t N, int64_t mb, int64_t nb,
+                                                  const float4_t (&acc)[FM][FN]) {
+  typedef typename T::storage S;
+  static_assert(sizeof(S) == 2, "16-bit operands and mask");
+  float bq[FN][4];
+  if (ep.bias) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const float4 b = *(const float4*)(ep.bias + nb + j * 16);
+      bq[j][0] = b.x, bq[j][1] = b.y, bq[j][2] = b.z, bq[j][3] = b.w;
+    }
+  }
+  if (ep.mask) {
+    uint2 mq[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        mq[i][j] = *(const uint2*)((const S*)ep.mask + (mb + i * 16) * ep.ldm + nb + j * 16);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const float mv[4] = {to_f<T>((S)(mq[i][j].x & 0xffffu)), to_f<T>((S)(mq[i][j].x >> 16)),
+                             to_f<T>((S)(mq[i][j].y & 0xffffu)), to_f<T>((S)(mq[i][j].y >> 16))};
+        epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], mv,
+                                       ep.bias ? bq[j] : nullptr);
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], nullptr,
+                                     ep.bias ? bq[j] : nullptr);
+}
+
 // ---------------------------------------------------------------------------
 // the kernel
 // ---------------------------------------------------------------------------
@@ -672,11 +719,7 @@ gemm_mfma_kernel(SrcA srcA, SrcB srcB, int64_t M, int64_t N, int64_t K, Epilogue
     return;
   }
   if (full_tile_epilogue(ep, m0 + BM <= M && n0 + BN <= N, N)) {
-#pragma unroll
-    for (int i = 0; i < TS::FM; ++i)
-#pragma unroll
-      for (int j = 0; j < TS::FN; ++j)
-        epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j]);
+    epilogue_interior<T, OutT, TS::FM, TS::FN>(ep, M, N, mb, nb, acc);
     return;
   }
 #pragma unroll

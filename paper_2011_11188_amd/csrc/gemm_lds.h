@@ -829,48 +829,7 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
   }
   // interior tiles with 4-aligned rows everywhere take the straight-line store
   if (full_tile_epilogue(ep, m0 + TL::BM <= M && n0 + TL::BN <= N, N)) {
-    // the bias quads of this wave's columns, loaded once before any store
-    // (rather than once per fragment, each load waited for behind the previous
-    // fragment's stores: the forward products of a 4096-wide MLP step, 3 us
-    // per 4096^3 launch)
-    float bq[FN][4];
-    if (ep.bias) {
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const float4 b = *(const float4*)(ep.bias + nb + j * 16);
-        bq[j][0] = b.x, bq[j][1] = b.y, bq[j][2] = b.z, bq[j][3] = b.w;
-      }
-    }
-    if (ep.mask) {
-      // every mask quad of this wave in flight before the first store: one
-      // round trip instead of one per fragment (the mask of a 4096^3 backward
-      // data product cost 9.2 us with a round trip per fragment, 6.4 us so:
-      // its 32 MB read at the end of the tile)
-      typedef typename T::storage S;
-      static_assert(sizeof(S) == 2, "16-bit operands and mask");
-      uint2 mq[FM][FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          mq[i][j] = *(const uint2*)((const S*)ep.mask + (mb + i * 16) * ep.ldm + nb + j * 16);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const float mv[4] = {to_f<T>((S)(mq[i][j].x & 0xffffu)), to_f<T>((S)(mq[i][j].x >> 16)),
-                               to_f<T>((S)(mq[i][j].y & 0xffffu)), to_f<T>((S)(mq[i][j].y >> 16))};
-          epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], mv,
-                                         ep.bias ? bq[j] : nullptr);
-        }
-      return;
-    }
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        epilogue_store4<T, OutT, true>(ep, M, N, mb + i * 16, nb + j * 16, acc[i][j], nullptr,
-                                       ep.bias ? bq[j] : nullptr);
+    epilogue_interior<T, OutT, FM, FN>(ep, M, N, mb, nb, acc);
     return;
   }
 #pragma unroll
