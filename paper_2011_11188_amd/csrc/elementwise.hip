@@ -44,17 +44,39 @@ mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t st) {
 // ---------------------------------------------------------------------------
 // cast
 // ---------------------------------------------------------------------------
+// Four consecutive elements in one vector access (p aligned to four elements).
+template <class T>
+__device__ __forceinline__ void load_quad(const typename T::storage* p, float (&v)[4]) {
+  if constexpr (sizeof(typename T::storage) == 4) {
+    const float4 q = *(const float4*)p;
+    v[0] = q.x, v[1] = q.y, v[2] = q.z, v[3] = q.w;
+  } else {
+    const uint2 q = *(const uint2*)p;
+    v[0] = to_f<T>((uint16_t)(q.x & 0xffffu)), v[1] = to_f<T>((uint16_t)(q.x >> 16));
+    v[2] = to_f<T>((uint16_t)(q.y & 0xffffu)), v[3] = to_f<T>((uint16_t)(q.y >> 16));
+  }
+}
+template <class T>
+__device__ __forceinline__ void store_quad(typename T::storage* p, const float (&v)[4]) {
+  if constexpr (sizeof(typename T::storage) == 4) {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    uint2 q;
+    q.x = (uint32_t)from_f<T>(v[0]) | ((uint32_t)from_f<T>(v[1]) << 16);
+    q.y = (uint32_t)from_f<T>(v[2]) | ((uint32_t)from_f<T>(v[3]) << 16);
+    *(uint2*)p = q;
+  }
+}
+
 template <class Src, class Dst, bool VEC>
 __global__ void cast_kernel(const typename Src::storage* __restrict__ src,
                             typename Dst::storage* __restrict__ dst, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  if (VEC) {  // 4 elements per thread, n % 4 == 0, 16/8-byte aligned
+  if (VEC) {  // 4 elements per thread in one vector load and store, n % 4 == 0, 4-element aligned
     for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n; i += stride * 4) {
       float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = to_f<Src>(src[i + e]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dst[i + e] = from_f<Dst>(v[e]);
+      load_quad<Src>(src + i, v);
+      store_quad<Dst>(dst + i, v);
     }
   } else {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
