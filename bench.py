@@ -255,7 +255,7 @@ def _kernel_choice(layout: str, m: int, n: int, k: int) -> str:
         if cd(m, 128) * cd(n, 128) < 128 and cd(m, 64) * cd(n, 64) >= 128:
             return "gemm_lds_kernel (64x64 direct-to-LDS pipeline)"
         if cd(m, 128) * cd(n, 128) <= 256:
-            return "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 4 stages)"
+            return "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 3 stages)"
         return "gemm_lds_kernel (128x128 direct-to-LDS pipeline)"
     if m <= 64 or n <= 64:
         return "gemm_mfma_kernel 64x64"
@@ -467,8 +467,8 @@ def _async_bench(mdnn, steps=40):
 def _traffic_key(kernel_desc: str) -> str:
     """'NN f16 -> f16 256x256' style key of a step kernel description."""
     tile = "256x256" if "256x256" in kernel_desc else "128x128"
-    if "4 stages" in kernel_desc:
-        tile += " (4 stages)"
+    if "3 stages" in kernel_desc:
+        tile += " (3 stages)"
     parts = kernel_desc.split(", ")
     return f"{parts[1]} {tile}"
 

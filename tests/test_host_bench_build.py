@@ -55,7 +55,7 @@ def test_spills_report_only_vector_register_spills():
 @pytest.mark.parametrize("shape,kernel", [
     (("NN", 4096, 4096, 4096), "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"),
     (("NN", 4096, 4096, 1024), "gemm_lds_kernel (256x256 direct-to-LDS pipeline)"),
-    (("TN", 1024, 4096, 4096), "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 4 stages)"),
+    (("TN", 1024, 4096, 4096), "gemm_lds_kernel (128x128 direct-to-LDS pipeline with 3 stages)"),
     (("NN", 4096, 1, 4096), "skinny rows kernel"),
     (("TN", 4096, 1, 4096), "skinny cols kernel"),
     (("NT", 4096, 4096, 1), "skinny depth kernel"),
