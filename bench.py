@@ -23,7 +23,11 @@ Also on the same JSON line:
   workloads     samples/s of the LeNet-style bf16 step and the fp32 MLP step;
   async_sgd     the same two nets trained asynchronously (section 3.1) by
                 several workers on separate streams sharing one parameter
-                vector, samples/s over all workers.
+                vector, samples/s over all workers;
+  sustained_clock  the shader clock rocm-smi reports while the headline step,
+                and the NN 8192^3 fp16 GEMM on the sweep's operands and on
+                all-zero operands, run back to back for a few seconds: the
+                rate the matrix cores keep at the clock the power limit allows.
 Every timed region follows sustained untimed load (about a second of the
 same work, or 3 runs of at least 50 ms with the median kept for the
 sub-benchmarks): the GPU's clocks settle under sustained load, which is the
@@ -350,6 +354,83 @@ def _gemm_sweep(mdnn, reps_scale=1.0):
     return res
 
 
+CLOCK_MAX_MHZ = 2400   # the shader clock PEAK_F16_TFLOPS assumes
+
+
+def _sampled_clock(fn, seconds=3.0):
+    """Run fn back to back for about `seconds` (after _warm) while a thread
+    samples rocm-smi's shader clock; returns (ms per call, median sclk MHz or
+    None, samples)."""
+    import statistics
+    import threading
+    import torch
+    _warm(fn)
+    samples, stop = [], threading.Event()
+
+    def sample():
+        while not stop.is_set():
+            c = _clocks()
+            if c and c.get("sclk_mhz"):
+                samples.append(c["sclk_mhz"])
+            stop.wait(0.2)
+    th = threading.Thread(target=sample, daemon=True)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    th.start()
+    a.record()
+    n, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            fn()
+        n += 8
+        _sync()
+    b.record()
+    _sync()
+    stop.set()
+    th.join()
+    return a.elapsed_time(b) / n, (statistics.median(samples) if samples else None), len(samples)
+
+
+def _sustained_clock(mdnn, net=None, xs=None, ts=None, cfg=None):
+    """The shader clock under sustained load.  MI355X's matrix-core peak
+    assumes 2.4 GHz; with N(0,1) fp16 operands the GEMMs draw enough power
+    that the clock settles well below it, while the same product on all-zero
+    operands (far less switching) holds 2.4 GHz.  frac_at_sclk is the GEMM's
+    rate over the peak scaled to the sampled clock."""
+    import torch
+    import workloads as W
+    res = {}
+    if net is not None:
+        it = iter(range(1 << 62))
+
+        def step():
+            i = next(it)
+            net.step(xs[i % len(xs)], ts[i % len(ts)])
+        ms, mhz, ns = _sampled_clock(step)
+        tf = cfg.flops_per_step() / (ms * 1e-3) / 1e12
+        res["wide_mlp_step"] = {"ms": round(ms, 4), "tflops": round(tf, 1), "sclk_mhz": mhz, "sclk_samples": ns,
+                                "frac_at_sclk": round(tf / (PEAK_F16_TFLOPS * mhz / CLOCK_MAX_MHZ), 4)
+                                if mhz else None}
+    size = 8192
+    a, b = W.gemm_operands("NN", size, size, size)
+    A, B = torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()
+    D = torch.empty((size, size), dtype=torch.float32, device="cuda")
+
+    def run():
+        mdnn.mdnn_gemm_mixed(0, size, size, size, 1.0, A, A.stride(0), B, B.stride(0), 1,
+                             0.0, None, 0, D, size, 0)
+    for name in ("NN_8192", "NN_8192_zero_operands"):
+        if name.endswith("zero_operands"):
+            A.zero_()
+            B.zero_()
+        ms, mhz, ns = _sampled_clock(run)
+        tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
+        res[name] = {"ms": round(ms, 4), "tflops": round(tf, 1), "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4),
+                     "sclk_mhz": mhz, "sclk_samples": ns,
+                     "frac_at_sclk": round(tf / (PEAK_F16_TFLOPS * mhz / CLOCK_MAX_MHZ), 4) if mhz else None}
+    del A, B, D
+    return res
+
+
 def _split3_sweep(mdnn):
     """fp32 GEMMs through three fp16 MFMA products (section 3.2, Eq. (1)),
     next to the native fp32 (VALU) kernel; inputs fp32 N(0,1)/sqrt(K)."""
@@ -560,7 +641,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--quick", action="store_true", help="headline only (no sub-benchmarks)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
-    ap.add_argument("--only", choices=["gemm", "conv", "split3", "workloads", "async"],
+    ap.add_argument("--only", choices=["gemm", "conv", "split3", "workloads", "async", "clock"],
                     help="profiling runs: the counter calibration copy and one sub-benchmark, printed as JSON "
                          "(no headline line)")
     args = ap.parse_args()
@@ -580,7 +661,7 @@ def main():
     if args.only:
         _copy_calibration(mdnn)
         subs = {"gemm": _gemm_sweep, "conv": _conv_bench, "split3": _split3_sweep, "workloads": _workloads_bench,
-                "async": _async_bench}
+                "async": _async_bench, "clock": _sustained_clock}
         print(json.dumps({args.only: subs[args.only](mdnn), "clocks": _clocks()}), flush=True)
         return
 
@@ -659,6 +740,9 @@ def main():
         print("[bench] workloads done", file=sys.stderr, flush=True)
         line["async_sgd"] = _async_bench(mdnn)
         print("[bench] async sgd done", file=sys.stderr, flush=True)
+        if not _under_profiler():
+            line["sustained_clock"] = _sustained_clock(mdnn, net, xs, ts, cfg)
+            print("[bench] sustained clock done", file=sys.stderr, flush=True)
     line["clocks"] = {"before": clocks_before, "after": _clocks()}
     if not args.no_cpu:
         line["cpu_baseline"] = _cpu_baseline(cfg)
