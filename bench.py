@@ -332,6 +332,30 @@ def _replay_group(mdnn, net, cfg, group, reps):
     return e0.elapsed_time(e1) / (reps * len(calls)), flops
 
 
+GRAPH_CALLS = 32
+
+
+def _graph_measure(fn, reps_scale=1.0):
+    """Per-call time (ms) of GRAPH_CALLS calls of fn recorded into one HIP
+    graph and replayed: the launches reach the GPU back to back, without the
+    host's per-call cost (which exceeds the kernel itself for a 1024^3
+    product)."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()   # first call outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    _sync()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(GRAPH_CALLS):
+            fn()
+    ms = _measure(g.replay, min_ms=50.0 * reps_scale) / GRAPH_CALLS
+    del g
+    return ms
+
+
 def _gemm_sweep(mdnn, reps_scale=1.0):
     import torch
     import workloads as W
@@ -348,8 +372,11 @@ def _gemm_sweep(mdnn, reps_scale=1.0):
                                      0.0, None, 0, D, size, 0)
             ms = _measure(run, min_ms=50.0 * reps_scale)
             tf = 2.0 * size ** 3 / (ms * 1e-3) / 1e12
+            gms = _graph_measure(run, reps_scale)
+            gtf = 2.0 * size ** 3 / (gms * 1e-3) / 1e12
             res[f"{layout}_{size}"] = {"ms": round(ms, 4), "tflops": round(tf, 1),
-                                       "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4)}
+                                       "mfma_frac": round(tf / PEAK_F16_TFLOPS, 4),
+                                       "graph_ms": round(gms, 4), "graph_tflops": round(gtf, 1)}
             del A, B, D
     return res
 
