@@ -178,8 +178,8 @@ struct LdsOperand {
 };
 
 // Whether the pipelined kernel can run this problem (see gemm_lds.h): the
-// 256 x 256 tile when it gives at least one tile per CU, else the 128 x 128
-// tile (8 waves of 64 x 32) when that gives at least 32 tiles.
+// 256 x 256 tile when it gives at least one tile per CU, else 128 x 128 or
+// 64 x 64 tiles (run_gemm_lds) when 128 x 128 tiles number at least 32.
 inline bool lds_pipe_eligible(const LdsOperand& a, const LdsOperand& b, int64_t M, int64_t N,
                               int64_t K, int64_t k_per_split, int splits) {
   const int o = gemm_tile_override();
