@@ -113,11 +113,12 @@ mdnn_status_t mdnn_gemm_mixed(mdnn_layout_t layout, int64_t M, int64_t N, int64_
  * exactly mdnn_gemm_mixed.  mdnn_gemm_workspace returns 0 when no split is
  * planned (and for negative sizes).  The workspace is scratch, overwritten;
  * calls that share one must be ordered on one stream.
- * nonfinite (nullable, device int32, d_type MDNN_F32 only, else
- * MDNN_ERR_DTYPE): the dynamic loss scaler's overflow test done where the
- * gradients are produced -- every kernel path sets *nonfinite = 1 (atomic
- * OR) if any value it stores into D is Inf or NaN, and never clears it; for
- * mdnn_sgd_update's scaler this is scaler->reserved. */
+ * nonfinite (nullable, device int32): the dynamic loss scaler's overflow
+ * test done where the gradients are produced -- every kernel path sets
+ * *nonfinite = 1 (atomic OR) if any value it stores into D is Inf or NaN
+ * (16-bit D: the stored value, so a finite result that rounds to Inf counts),
+ * and never clears it; for mdnn_sgd_update's scaler this is
+ * scaler->reserved. */
 size_t mdnn_gemm_workspace(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K);
 mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t K,
                                  float alpha, const void* A, int64_t lda, const void* B,
@@ -397,6 +398,36 @@ mdnn_status_t mdnn_sgd_update(int64_t n, float* w32, const float* g32, float* v3
 mdnn_status_t mdnn_sgd_update_async(int64_t n, float* w32, const float* g32, float* v32, float lr,
                                     float momentum, mdnn_scaler_t* scaler, mdnn_stream_t stream);
 
+/* Weight-gradient product with the SGD update applied where it is produced
+ * (section 3.1's update of the fp32 master weights, section 3.2's mixed
+ * precision): G = A^T B in the TN layout of mdnn_gemm_mixed (A [K][M] with
+ * lda >= M, B [K][N] with ldb >= N, ab_type F16 or BF16, fp32 accumulation)
+ * is not stored; element (m, n) of G updates w32[m*ldw + n], v32[m*ldw + n]
+ * and w_lp[m*ldw + n] exactly as mdnn_sgd_update does with g = G[m][n]
+ * (bit for bit: g / scale with a scaler, v = momentum*v + g, w -= lr*v, or
+ * w -= lr*g when momentum is 0, w_lp = RNE(w) in ab_type).  scaler
+ * (nullable) is only read: when scaler->reserved is set nothing is updated.
+ * G itself is not tested for Inf / NaN, so a loss-scaled caller must have
+ * set reserved for every non-finite operand value before the call (with
+ * finite fp16 operands the fp32 product is finite for any K below 2^96; the
+ * train step tests the stored activations and output gradients; bf16
+ * operands carry no such bound).  The scaler's state is not advanced (the
+ * update of the remaining parameters does that).
+ * Shapes: M and N positive multiples of 256, K a positive multiple of 64,
+ * M * N at least 32 tiles of 128 x 128; A, B 16-byte aligned with lda, ldb
+ * multiples of 8; w32 (and v32) 16-byte aligned, w_lp 8-byte aligned
+ * (nullable: no working copy), ldw >= N a multiple of 4; v32 required when
+ * momentum != 0.  The product takes the pipelined kernel of mdnn_gemm_mixed
+ * (same tiles, no K split), every tile interior.
+ * Errors: MDNN_ERR_DTYPE (F32 or unknown ab_type), MDNN_ERR_NULL,
+ * MDNN_ERR_SHAPE (sizes, or operands the pipelined kernel does not take),
+ * MDNN_ERR_LAYOUT (a leading dimension too small), MDNN_ERR_MISALIGNED,
+ * MDNN_ERR_LAUNCH. */
+mdnn_status_t mdnn_gemm_tn_update(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                                  const void* B, int64_t ldb, mdnn_dtype_t ab_type, float* w32,
+                                  float* v32, void* w_lp, int64_t ldw, float lr, float momentum,
+                                  const mdnn_scaler_t* scaler, mdnn_stream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Precision conversion (section 3.2: fp32 data stored as fp16 or bf16).
  * dst[i] = convert(src[i]) for i < n, round to nearest even.
@@ -434,6 +465,15 @@ typedef struct {
   float momentum;       /* 0: plain SGD (momentum buffer may be NULL)          */
   int32_t loss_scaling; /* nonzero: dynamic loss scaling via the bound scaler  */
   int32_t n_classes;    /* cross-entropy classes (= last layer's outputs)      */
+  int32_t fuse_update;  /* nonzero: FC layers after the first whose weight
+                           gradient fits mdnn_gemm_tn_update (in and out
+                           multiples of 256, batch a multiple of 64, 16-bit
+                           storage; fp16 when the loss is scaled; buffers
+                           aligned as that call needs) and is not split
+                           over K in the unfused step are updated inside
+                           that product, after the whole backward pass: the
+                           same results bit for bit, without storing and
+                           re-reading their fp32 weight gradients          */
 } mdnn_train_cfg_t;
 
 typedef struct mdnn_net mdnn_net_t;
@@ -465,7 +505,8 @@ mdnn_status_t mdnn_net_sync_lowp(mdnn_net_t* net, mdnn_stream_t stream);
  * as in mdnn_sgd_update; the step tests the gradients where it produces
  * them (GEMM epilogues, the bias column sums) plus one pass over the ranges
  * no such producer covers, instead of a second pass over all gradients.
- * grads holds this step's scaled gradients afterwards. */
+ * grads holds this step's scaled gradients afterwards, except the weight
+ * gradients of layers fused by cfg.fuse_update (never stored). */
 mdnn_status_t mdnn_train_step(mdnn_net_t* net, const float* x, const void* target,
                               float* loss_out, mdnn_stream_t stream);
 /* Asynchronous step (section 3.1): for several nets bound to the same
@@ -487,7 +528,9 @@ const void* mdnn_net_activation(const mdnn_net_t* net, int32_t i);
  * loss gradient (last layer, L - 1) goes to buffer 0 and each layer's input
  * gradient to the other buffer, so the gradient with respect to the output
  * of layer i is in buffer (L - 1 - i) % 2; after a step the buffers hold
- * those of layers 0 and 1 (the last two written). */
+ * those of layers 0 and 1 (the last two written).  With cfg.fuse_update the
+ * gradient of a fused layer's output is in a workspace buffer of its own
+ * instead (the rule holds for the other layers). */
 const void* mdnn_net_output_grad(const mdnn_net_t* net, int32_t which);
 void mdnn_net_destroy(mdnn_net_t* net);
 

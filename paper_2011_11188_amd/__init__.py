@@ -63,7 +63,8 @@ class LayerDesc(C.Structure):
 
 class TrainCfg(C.Structure):
     _fields_ = [("dtype", C.c_int32), ("loss", C.c_int32), ("lr", C.c_float),
-                ("momentum", C.c_float), ("loss_scaling", C.c_int32), ("n_classes", C.c_int32)]
+                ("momentum", C.c_float), ("loss_scaling", C.c_int32), ("n_classes", C.c_int32),
+                ("fuse_update", C.c_int32)]
 
 
 _vp, _i64, _f, _i = C.c_void_p, C.c_int64, C.c_float, C.c_int
@@ -73,6 +74,7 @@ _SIGS = {
                         _i64, _i, _vp, _i, _vp, _i64, _vp],
     "mdnn_gemm_mixed_ws": [_i, _i64, _i64, _i64, _f, _vp, _i64, _vp, _i64, _i, _f, _vp, _i64, _vp,
                            _i64, _i, _vp, _i, _vp, _i64, _vp, C.c_size_t, _vp, _vp],
+    "mdnn_gemm_tn_update": [_i64, _i64, _i64, _vp, _i64, _vp, _i64, _i, _vp, _vp, _vp, _i64, _f, _f, _vp, _vp],
     "mdnn_conv2d_fwd": [_vp, _vp, _vp, _i, _vp, _i, _vp, _i, _vp],
     "mdnn_conv2d_bwd_data": [_vp, _vp, _vp, _i, _vp, _vp, _i, _vp],
     "mdnn_conv2d_bwd_filter": [_vp, _vp, _vp, _i, _vp, _vp, _vp, C.c_size_t, _vp],
@@ -217,6 +219,12 @@ def mdnn_gemm_mixed_ws(layout, M, N, K, alpha, A, lda, B, ldb, ab_type, beta, Cm
     return _call("mdnn_gemm_mixed_ws", layout, M, N, K, alpha, _p(A), lda, _p(B), ldb, ab_type, beta,
                  _p(Cm), ldc, _p(D), ldd, d_type, _p(bias), act, _p(mask_src), ldm, _p(workspace), ws_bytes,
                  _p(nonfinite), _s(stream))
+
+
+def mdnn_gemm_tn_update(M, N, K, A, lda, B, ldb, ab_type, w32, v32, w_lp, ldw, lr, momentum, scaler=None,
+                        stream=None):
+    return _call("mdnn_gemm_tn_update", M, N, K, _p(A), lda, _p(B), ldb, ab_type, _p(w32), _p(v32), _p(w_lp),
+                 ldw, lr, momentum, _p(scaler), _s(stream))
 
 
 def mdnn_gemm_workspace(ab_type, M, N, K) -> int:

@@ -181,13 +181,15 @@ class Net:
 
     def __init__(self, layers, batch: int, dtype: int, loss: int, lr: float,
                  momentum: float = 0.0, loss_scaling: bool = False, init_scale: float = 1.0,
-                 n_classes: int = 10, device="cuda", shared_master=None):
+                 n_classes: int = 10, device="cuda", shared_master=None, fuse_update: bool = False):
         """shared_master: another Net's `master` tensor to bind instead of a
-        private one (asynchronous workers; step with step_async only)."""
+        private one (asynchronous workers; step with step_async only).
+        fuse_update: the train config's fuse_update (eligible FC layers
+        updated inside their weight-gradient products)."""
         import torch
         descs = [LayerDesc(l.kind, l.act, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.pad) for l in layers]
         self.cfg = TrainCfg(dtype, loss, lr, momentum, 1 if loss_scaling else 0,
-                            n_classes if loss == LOSS_XENT else 0)
+                            n_classes if loss == LOSS_XENT else 0, 1 if fuse_update else 0)
         self.handle = mdnn_net_create(descs, batch, self.cfg)
         self.batch = batch
         self.dtype = dtype

@@ -463,6 +463,79 @@ __global__ void finite_check_ranges_kernel(const float* __restrict__ g, CheckRan
   if (bad && threadIdx.x == 0) atomicOr(&sc->reserved, 1);
 }
 
+// sgd_kernel over a few ranges of the flat parameter vector: block row y
+// covers range y (the same arithmetic per element)
+template <class LpT, bool MOM, bool SCALE>
+__global__ void sgd_ranges_kernel(CheckRanges r, float* __restrict__ w, const float* __restrict__ g,
+                                  float* __restrict__ v, typename LpT::storage* __restrict__ wlp, float lr,
+                                  float mu, const mdnn_scaler_t* __restrict__ sc, bool vec) {
+  float S = 1.0f;
+  if (SCALE) {
+    if (sc->reserved) return;  // overflow: skip the whole update
+    S = sc->scale;
+  }
+  const int64_t off = r.off[blockIdx.y], n = r.len[blockIdx.y];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t done = 0;
+  if (vec && off % 4 == 0) {
+    // four elements per thread with 16-byte accesses (the buffers are
+    // 16-byte aligned at element 0), the same arithmetic per element
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+    const int64_t n4 = n / 4;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n4; q += stride) {
+      const int64_t k = off + 4 * q;
+      const f4v gi = __builtin_nontemporal_load((const f4v*)(g + k));
+      const f4v wi = __builtin_nontemporal_load((const f4v*)(w + k));
+      float ga[4] = {gi[0], gi[1], gi[2], gi[3]}, wa[4] = {wi[0], wi[1], wi[2], wi[3]};
+      if (SCALE) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ga[e] = ga[e] / S;
+      }
+      if (MOM) {
+        const f4v vi = __builtin_nontemporal_load((const f4v*)(v + k));
+        float va[4] = {vi[0], vi[1], vi[2], vi[3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          va[e] = fmaf(mu, va[e], ga[e]);
+          wa[e] = fmaf(-lr, va[e], wa[e]);
+        }
+        __builtin_nontemporal_store((f4v){va[0], va[1], va[2], va[3]}, (f4v*)(v + k));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wa[e] = fmaf(-lr, ga[e], wa[e]);
+      }
+      __builtin_nontemporal_store((f4v){wa[0], wa[1], wa[2], wa[3]}, (f4v*)(w + k));
+      if (wlp) {
+        if constexpr (sizeof(typename LpT::storage) == 4) {
+          __builtin_nontemporal_store((f4v){wa[0], wa[1], wa[2], wa[3]}, (f4v*)(wlp + k));
+        } else {
+          u2v u;
+          u[0] = (uint32_t)from_f<LpT>(wa[0]) | ((uint32_t)from_f<LpT>(wa[1]) << 16);
+          u[1] = (uint32_t)from_f<LpT>(wa[2]) | ((uint32_t)from_f<LpT>(wa[3]) << 16);
+          __builtin_nontemporal_store(u, (u2v*)(wlp + k));
+        }
+      }
+    }
+    done = n4 * 4;
+  }
+  for (int64_t i = done + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t k = off + i;
+    float gi = g[k];
+    if (SCALE) gi = gi / S;
+    float wi = w[k];
+    if (MOM) {
+      const float vi = fmaf(mu, v[k], gi);
+      v[k] = vi;
+      wi = fmaf(-lr, vi, wi);
+    } else {
+      wi = fmaf(-lr, gi, wi);
+    }
+    w[k] = wi;
+    if (wlp) wlp[k] = from_f<LpT>(wi);
+  }
+}
+
 template <class LpT, bool MOM, bool SCALE>
 __global__ void sgd_kernel(int64_t n, float* __restrict__ w, const float* __restrict__ g,
                            float* __restrict__ v, typename LpT::storage* __restrict__ wlp, float lr,
@@ -917,6 +990,49 @@ mdnn_status_t mdnn::finite_check_ranges(const float* g, const CheckRanges& r, md
   if (gx > 256) gx = 256;
   hipLaunchKernelGGL(finite_check_ranges_kernel, dim3(gx, (unsigned)r.n), dim3(256), 0, st, g, r, scaler);
   return check_launch("finite_check_ranges_kernel");
+}
+
+template <class LpT>
+static void sgd_ranges_launch(const CheckRanges& r, unsigned gx, float* w, const float* g, float* v, void* wlp,
+                              float lr, float mu, const mdnn_scaler_t* sc, hipStream_t st) {
+  typedef typename LpT::storage L;
+  const dim3 grid(gx, (unsigned)r.n);
+  const bool vec = aligned(w, 16) && aligned(g, 16) && (!v || aligned(v, 16)) && (!wlp || aligned(wlp, 4 * sizeof(L)));
+  if (v && sc)
+    hipLaunchKernelGGL((sgd_ranges_kernel<LpT, true, true>), grid, dim3(256), 0, st, r, w, g, v, (L*)wlp, lr, mu, sc,
+                       vec);
+  else if (v)
+    hipLaunchKernelGGL((sgd_ranges_kernel<LpT, true, false>), grid, dim3(256), 0, st, r, w, g, v, (L*)wlp, lr, mu,
+                       sc, vec);
+  else if (sc)
+    hipLaunchKernelGGL((sgd_ranges_kernel<LpT, false, true>), grid, dim3(256), 0, st, r, w, g, v, (L*)wlp, lr, mu,
+                       sc, vec);
+  else
+    hipLaunchKernelGGL((sgd_ranges_kernel<LpT, false, false>), grid, dim3(256), 0, st, r, w, g, v, (L*)wlp, lr, mu,
+                       sc, vec);
+}
+
+mdnn_status_t mdnn::sgd_update_ranges_prechecked(const CheckRanges& r, float* w32, const float* g32, float* v32,
+                                                 void* w_lp, mdnn_dtype_t lp_type, float lr, float momentum,
+                                                 mdnn_scaler_t* scaler, hipStream_t st) {
+  if (r.n < 0 || r.n > kMaxCheckRanges) return fail(MDNN_ERR_SHAPE, "sgd_update: too many ranges");
+  int64_t longest = 0;
+  for (int i = 0; i < r.n; ++i) longest = r.len[i] > longest ? r.len[i] : longest;
+  if (longest > 0) {
+    const unsigned gx = stream_grid(ceil_div(longest, (int64_t)4));
+    float* v = momentum != 0.0f ? v32 : nullptr;
+    switch (lp_type) {
+      case MDNN_F32: sgd_ranges_launch<F32>(r, gx, w32, g32, v, w_lp, lr, momentum, scaler, st); break;
+      case MDNN_F16: sgd_ranges_launch<F16>(r, gx, w32, g32, v, w_lp, lr, momentum, scaler, st); break;
+      default: sgd_ranges_launch<BF16>(r, gx, w32, g32, v, w_lp, lr, momentum, scaler, st); break;
+    }
+    MDNN_TRY(check_launch("sgd_ranges_kernel"));
+  }
+  if (scaler) {
+    hipLaunchKernelGGL(scaler_finalize_kernel, dim3(1), dim3(64), 0, st, scaler);
+    MDNN_TRY(check_launch("scaler_finalize_kernel"));
+  }
+  return MDNN_SUCCESS;
 }
 
 static mdnn_status_t sgd_update_impl(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,

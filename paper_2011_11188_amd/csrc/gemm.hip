@@ -718,7 +718,6 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
     return fail(MDNN_ERR_MISALIGNED, "gemm: a base pointer is not aligned to its element size");
   if (ab_type == MDNN_F32 && d_type != MDNN_F32)
     return fail(MDNN_ERR_DTYPE, "gemm: fp32 operands need an fp32 output");
-  if (nonfinite && d_type != MDNN_F32) return fail(MDNN_ERR_DTYPE, "gemm: the finite check needs an fp32 output");
 
   Epilogue ep{};
   ep.alpha = alpha;
@@ -754,6 +753,56 @@ mdnn_status_t mdnn::gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, in
   if (d_type == MDNN_F32)
     return gemm_dispatch16<BF16, F32>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
   return gemm_dispatch16<BF16, BF16>(layout, M, N, K, A, lda, va, B, ldb, vb, ep, ws, ws_bytes, st);
+}
+
+int mdnn::gemm_lp_splits(int64_t M, int64_t N, int64_t K) { return lp_split_plan(M, N, K, 128).splits; }
+
+bool mdnn::gemm_tn_update_ok(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                              const void* B, int64_t ldb, const float* w32, const float* v32, const void* w_lp,
+                              int64_t ldw) {
+  if (ab_type != MDNN_F16 && ab_type != MDNN_BF16) return false;
+  // every tile of every pipelined configuration is interior, no K split
+  if (M <= 0 || N <= 0 || K <= 0 || M % 256 != 0 || N % 256 != 0) return false;
+  if (lda < M || ldb < N || ldw < N || ldw % 4 != 0) return false;
+  if (!w32 || !aligned(w32, 16) || (v32 && !aligned(v32, 16)) || (w_lp && !aligned(w_lp, 8))) return false;
+  const LdsOperand la{A, lda, M, false}, lb{B, ldb, N, false};
+  return lds_pipe_eligible(la, lb, M, N, K, K, 1);
+}
+
+extern "C" mdnn_status_t mdnn_gemm_tn_update(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                                             const void* B, int64_t ldb, mdnn_dtype_t ab_type, float* w32,
+                                             float* v32, void* w_lp, int64_t ldw, float lr, float momentum,
+                                             const mdnn_scaler_t* scaler, mdnn_stream_t stream) {
+  if (!dtype_ok(ab_type)) return fail(MDNN_ERR_DTYPE, "gemm_tn_update: unknown dtype");
+  if (ab_type == MDNN_F32) return fail(MDNN_ERR_DTYPE, "gemm_tn_update: 16-bit operands only");
+  if (!A || !B || !w32) return fail(MDNN_ERR_NULL, "gemm_tn_update: A, B and w32 are required");
+  if (momentum != 0.0f && !v32) return fail(MDNN_ERR_NULL, "gemm_tn_update: v32 is required with momentum");
+  if (M <= 0 || N <= 0 || K <= 0 || M % 256 != 0 || N % 256 != 0 || K % lds::BK != 0)
+    return fail(MDNN_ERR_SHAPE, "gemm_tn_update: M and N must be positive multiples of 256, K of %d", lds::BK);
+  if (lda < M || ldb < N || ldw < N) return fail(MDNN_ERR_LAYOUT, "gemm_tn_update: a leading dimension is too small");
+  if (!aligned(A, 16) || !aligned(B, 16) || lda % 8 != 0 || ldb % 8 != 0 || !aligned(w32, 16) ||
+      (v32 && !aligned(v32, 16)) || (w_lp && !aligned(w_lp, 8)) || ldw % 4 != 0 || (scaler && !aligned(scaler, 4)))
+    return fail(MDNN_ERR_MISALIGNED,
+                "gemm_tn_update: A, B, w32, v32 need 16-byte alignment (w_lp 8), lda / ldb multiples of 8, ldw of 4");
+  if (!gemm_tn_update_ok(ab_type, M, N, K, A, lda, B, ldb, w32, momentum != 0.0f ? v32 : nullptr, w_lp, ldw))
+    return fail(MDNN_ERR_SHAPE, "gemm_tn_update: the operands do not fit the pipelined kernel");
+  Epilogue ep{};
+  ep.alpha = 1.0f;
+  ep.D = w32;  // never stored: every tile is interior and takes the update
+  ep.ldd = ldw;
+  ep.vec4 = 1;
+  ep.k_per_split = K;
+  ep.upd_w = w32;
+  ep.upd_v = momentum != 0.0f ? v32 : nullptr;
+  ep.upd_lp = w_lp;
+  ep.upd_lr = lr;
+  ep.upd_mu = momentum;
+  ep.upd_sc = scaler;
+  const LdsOperand la{A, lda, M, false}, lb{B, ldb, N, false};
+  clear_error();
+  hipStream_t st = as_stream(stream);
+  if (ab_type == MDNN_F16) return run_gemm_lds<F16, F32, false, false>(la, lb, M, N, K, ep, 1, st);
+  return run_gemm_lds<BF16, F32, false, false>(la, lb, M, N, K, ep, 1, st);
 }
 
 extern "C" int mdnn_set_gemm_tile(int code) {

@@ -303,8 +303,17 @@ struct Epilogue {
   float* partial;      // split-K: fp32 [splits][M][N]; null otherwise
   int64_t k_per_split; // multiple of GEMM_BK
   int64_t bstride_d;   // batched products (grid z): elements of D between batch entries
-  int32_t* nonfinite;  // fp32 D only: set to 1 (atomic OR) when a stored value is not finite; or null
+  int32_t* nonfinite;  // set to 1 (atomic OR) when a stored value is Inf or NaN (16-bit D: as stored); or null
   const float* alpha_dev;  // device scalar multiplied into alpha (scales chosen on the device), or null
+  // SGD update in place of storing D (the pipelined kernel's TN products
+  // with an fp32 gradient, interior tiles only; see update_epilogue in
+  // gemm_lds.h): element (m, n) of the product is the gradient of
+  // upd_w[m * ldd + n]; null otherwise
+  float* upd_w;
+  float* upd_v;        // momentum, same indexing, or null (plain SGD)
+  void* upd_lp;        // working copy in the operands' 16-bit type, same indexing, or null
+  float upd_lr, upd_mu;
+  const mdnn_scaler_t* upd_sc;  // loss scaler (skip when reserved, divide by scale), or null
 };
 
 // Batched products: grid z selects one matrix of a batch of plain matrices
@@ -406,6 +415,7 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
         if (n + e < N && !(to_f<MaskT>(mk[e]) > 0.0f)) v[e] = 0.0f;
     }
   }
+  typename OutT::storage* d = (typename OutT::storage*)ep.D + m * ep.ldd + n;
   if constexpr (sizeof(typename OutT::storage) == 4) {
     // the loss scaler's overflow test, on the values as stored
     if (ep.nonfinite) {
@@ -414,21 +424,36 @@ __device__ __forceinline__ void epilogue_store4(const Epilogue& ep, int64_t M, i
       for (int e = 0; e < 4; ++e) bad |= (FULL || n + e < N) && !isfinite(v[e]);
       if (bad) atomicOr(ep.nonfinite, 1);
     }
-  }
-  typename OutT::storage* d = (typename OutT::storage*)ep.D + m * ep.ldd + n;
-  if (full) {
-    if constexpr (sizeof(typename OutT::storage) == 4) {
+    if (full) {
       *(float4*)d = make_float4(v[0], v[1], v[2], v[3]);
     } else {
-      uint2 u;
-      u.x = (uint32_t)from_f<OutT>(v[0]) | ((uint32_t)from_f<OutT>(v[1]) << 16);
-      u.y = (uint32_t)from_f<OutT>(v[2]) | ((uint32_t)from_f<OutT>(v[3]) << 16);
-      *(uint2*)d = u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N) d[e] = v[e];
     }
   } else {
+    uint16_t h[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (n + e < N) d[e] = from_f<OutT>(v[e]);
+    for (int e = 0; e < 4; ++e) h[e] = from_f<OutT>(v[e]);
+    // 16-bit stores: the test is on the stored bits (an all-ones exponent),
+    // which also catches finite values that round to Inf
+    if (ep.nonfinite) {
+      constexpr uint16_t EXP = OutT::id == MDNN_F16 ? 0x7c00u : 0x7f80u;
+      bool bad = false;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bad |= (FULL || n + e < N) && (h[e] & EXP) == EXP;
+      if (bad) atomicOr(ep.nonfinite, 1);
+    }
+    if (full) {
+      uint2 u;
+      u.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+      u.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+      *(uint2*)d = u;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n + e < N) d[e] = h[e];
+    }
   }
 }
 

@@ -51,6 +51,8 @@
 // stored.
 #pragma once
 
+#include <type_traits>
+
 #include "gemm_core.h"
 
 namespace mdnn {
@@ -719,6 +721,107 @@ __device__ __forceinline__ void pipeline_round(int t, int nk, const Stages<NS>& 
   }
 }
 
+// The SGD update of a square tile's weights in place of storing its weight
+// gradient (mdnn_gemm_tn_update), with g = alpha * acc per element exactly
+// the arithmetic of the SGD kernels (g / scale with a scaler, v = fma(mu, v,
+// g) and w = fma(-lr, v, w), or w = fma(-lr, g, w), then the working copy
+// rounded from w), so the result is bitwise that of storing the gradient
+// and updating from it; a set scaler->reserved (an earlier producer of the
+// step saw Inf or NaN) skips it.  The accumulators go through LDS (the A
+// stage of the pipeline, A_BYTES = 32 rows x BN fp32) 32 rows at a time, so
+// that each wave then reads, updates and writes whole 16-byte-per-lane runs
+// of those rows: the weight, momentum and working-copy traffic (18 bytes per
+// element) is contiguous, where the accumulator layout would split it into
+// 64-byte pieces.  LDS slot s of row r holds float4 s ^ (r & 15) (the 16
+// lanes writing one column block hit different banks).
+struct UpdateArgs {
+  float S, alpha;
+  bool mom;
+};
+template <class T, class TL, int P, int FM, int FN>
+__device__ __forceinline__ void update_pass(const Epilogue& ep, float4* st, int64_t m0, int64_t n0, int wm, int wn,
+                                            int lane, int tid, const float4_t (&acc)[FM][FN], const UpdateArgs& u) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+  constexpr int BN = TL::BN, S4 = BN / 4;          // float4 slots per row
+  constexpr int ROWS = TL::A_BYTES / (BN * 4);     // rows per pass
+  constexpr int PER = ROWS * S4 / TL::NT;           // float4 per thread per pass
+  static_assert(ROWS == 32 && ROWS * S4 == PER * TL::NT && TL::WTM % ROWS == 0, "update staging shape");
+  if constexpr (P * ROWS < TL::BM) {
+    // the waves whose rows fall in this pass (wave row WMP) stage their two
+    // fragment rows I0, I0 + 1
+    constexpr int WMP = P * ROWS / TL::WTM, I0 = (P * ROWS - WMP * TL::WTM) / 16;
+    if (wm == WMP) {
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int r = ii * 16 + (lane & 15);
+          const int s = (wn * TL::WTN + j * 16) / 4 + (lane >> 4);
+          st[r * S4 + (s ^ (r & 15))] =
+              make_float4(acc[I0 + ii][j][0], acc[I0 + ii][j][1], acc[I0 + ii][j][2], acc[I0 + ii][j][3]);
+        }
+    }
+    __syncthreads();
+    float4 gq[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * TL::NT, r = idx / S4, s = idx % S4;
+      gq[k] = st[r * S4 + (s ^ (r & 15))];
+    }
+    __syncthreads();  // the next pass may overwrite the stage
+    f4v wq[PER], vq[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * TL::NT, r = idx / S4, s = idx % S4;
+      const int64_t e = (m0 + P * ROWS + r) * ep.ldd + n0 + 4 * s;
+      wq[k] = *(const f4v*)(ep.upd_w + e);
+      if (u.mom) vq[k] = *(const f4v*)(ep.upd_v + e);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = tid + k * TL::NT, r = idx / S4, s = idx % S4;
+      const int64_t e = (m0 + P * ROWS + r) * ep.ldd + n0 + 4 * s;
+      const float ga[4] = {gq[k].x, gq[k].y, gq[k].z, gq[k].w};
+      float w[4] = {wq[k][0], wq[k][1], wq[k][2], wq[k][3]};
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (u.mom) v[0] = vq[k][0], v[1] = vq[k][1], v[2] = vq[k][2], v[3] = vq[k][3];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        float g = ga[c] * u.alpha;
+        if (ep.upd_sc) g = g / u.S;
+        if (u.mom) {
+          v[c] = fmaf(ep.upd_mu, v[c], g);
+          w[c] = fmaf(-ep.upd_lr, v[c], w[c]);
+        } else {
+          w[c] = fmaf(-ep.upd_lr, g, w[c]);
+        }
+      }
+      *(f4v*)(ep.upd_w + e) = (f4v){w[0], w[1], w[2], w[3]};
+      if (u.mom) *(f4v*)(ep.upd_v + e) = (f4v){v[0], v[1], v[2], v[3]};
+      if (ep.upd_lp) {
+        u2v q;
+        q[0] = (uint32_t)from_f<T>(w[0]) | ((uint32_t)from_f<T>(w[1]) << 16);
+        q[1] = (uint32_t)from_f<T>(w[2]) | ((uint32_t)from_f<T>(w[3]) << 16);
+        *(u2v*)((typename T::storage*)ep.upd_lp + e) = q;
+      }
+    }
+    update_pass<T, TL, P + 1>(ep, st, m0, n0, wm, wn, lane, tid, acc, u);
+  }
+}
+
+template <class T, class TL, int FM, int FN>
+__device__ __forceinline__ void update_epilogue(const Epilogue& ep, char* lds, int64_t m0, int64_t n0, int wm, int wn,
+                                                int lane, int tid, const float4_t (&acc)[FM][FN]) {
+  if (ep.upd_sc && ep.upd_sc->reserved) return;     // uniform: read by every thread alike
+  UpdateArgs u;
+  u.S = ep.upd_sc ? ep.upd_sc->scale : 1.0f;
+  u.alpha = ep.alpha_dev ? ep.alpha * *ep.alpha_dev : ep.alpha;
+  u.mom = ep.upd_v != nullptr;
+  __syncthreads();  // the mainloop's last fragment reads are done
+  update_pass<T, TL, 0>(ep, (float4*)lds, m0, n0, wm, wn, lane, tid, acc, u);
+}
+
 // D = epilogue(op(A) op(B)), or fp32 split partials when ep.partial is set
 // (grid.y = split index, each split ep.k_per_split deep).  NS LDS stages
 // (2..4) of A_BYTES + B_BYTES each.
@@ -828,6 +931,16 @@ gemm_lds_kernel(typename LA::Args aa, typename LB::Args ba, int64_t M, int64_t N
     return;
   }
   // interior tiles with 4-aligned rows everywhere take the straight-line store
+  // the fused SGD update (plain TN products with an fp32 gradient; every
+  // tile interior, which the host has checked)
+  constexpr bool UPD = std::is_same<OutT, F32>::value && std::is_same<LA, MatLoader<false, TL::BM, TL::LA>>::value &&
+                       std::is_same<LB, MatLoader<false, TL::BN, TL::LB>>::value && TL::BM == TL::BN;
+  if constexpr (UPD) {
+    if (ep.upd_w) {
+      update_epilogue<T, TL>(ep, lds_a0, m0, n0, wm, wn, lane, tid, acc);
+      return;
+    }
+  }
   if (full_tile_epilogue(ep, m0 + TL::BM <= M && n0 + TL::BN <= N, N)) {
     epilogue_interior<T, OutT, FM, FN>(ep, M, N, mb, nb, acc);
     return;

@@ -92,6 +92,15 @@ mdnn_status_t gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int64_t 
                             size_t ws_bytes, mdnn_stream_t stream, int32_t* nonfinite = nullptr,
                             const float* alpha_dev = nullptr);
 
+// K splits of a 16-bit product given a large enough workspace (1: none).
+int gemm_lp_splits(int64_t M, int64_t N, int64_t K);
+// Whether mdnn_gemm_tn_update takes this problem (16-bit operands, M and N
+// multiples of 256, the pipelined kernel's operand alignment, 16-byte
+// aligned w32 / v32, 8-byte aligned w_lp, ldw a multiple of 4).
+bool gemm_tn_update_ok(mdnn_dtype_t ab_type, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                       const void* B, int64_t ldb, const float* w32, const float* v32, const void* w_lp,
+                       int64_t ldw);
+
 // Loss-scaled updates whose gradients were checked where they were produced:
 // gemm_mixed_ws with `nonfinite` = &scaler->reserved covers every fp32 value
 // it stores (all of its kernel paths store through the same epilogue); the
@@ -107,5 +116,10 @@ mdnn_status_t finite_check_ranges(const float* g, const CheckRanges& r, mdnn_sca
 mdnn_status_t sgd_update_prechecked(int64_t n, float* w32, const float* g32, float* v32, void* w_lp,
                                     mdnn_dtype_t lp_type, float lr, float momentum, mdnn_scaler_t* scaler,
                                     mdnn_stream_t stream);
+// The same update over the listed ranges of the flat vectors only (one
+// launch), then the scaler's state update.
+mdnn_status_t sgd_update_ranges_prechecked(const CheckRanges& r, float* w32, const float* g32, float* v32,
+                                           void* w_lp, mdnn_dtype_t lp_type, float lr, float momentum,
+                                           mdnn_scaler_t* scaler, hipStream_t st);
 
 }  // namespace mdnn

@@ -11,6 +11,9 @@
 //   act[i+1]        stored output of layer i (fp32 for the last layer)
 //   argmax[i]       window index of each max-pool output
 //   grad0, grad1    ping-pong buffers for activation gradients (low precision)
+//   dz[i]           with fuse_update: the output gradient of each FC layer
+//                   whose update runs in its weight-gradient product (it is
+//                   read after the whole backward pass)
 //   reduce_ws       split-K partials of the convolution backward-filter and
 //                   of fp32 fully connected GEMMs, partial column sums of the
 //                   bias gradients (the users run one after another)
@@ -30,6 +33,10 @@ struct LayerPlan {
   size_t cs_off = 0;                  // FC: bias-gradient partial column sums
   bool input_relu = false;            // input produced by a ReLU (directly or through pooling)
   bool last = false;
+  // fuse_update: this FC layer's weights are updated inside its weight-gradient
+  // product (mdnn_gemm_tn_update); its output gradient lives at dz_off
+  bool fuse_cand = false, fused = false;
+  size_t dz_off = 0;
 };
 
 struct mdnn_net {
@@ -57,6 +64,10 @@ struct mdnn_net {
   // full check.
   bool prechecked = false;
   CheckRanges unchecked{};
+  // fuse_update: whether any layer is fused (decided at bind time, from the
+  // bound pointers) and the parameter ranges the SGD pass still updates
+  bool fuse = false;
+  CheckRanges rest{};
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -194,6 +205,20 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
     if (p.in_feat > max_feat) max_feat = p.in_feat;
     if (p.out_feat > max_feat) max_feat = p.out_feat;
   }
+  // fuse_update candidates: FC layers after the first (the first layer's
+  // input is not tested for Inf / NaN on the way in) whose weight gradient
+  // takes mdnn_gemm_tn_update's shapes; fp16 storage when the loss is scaled
+  // (finite fp16 operands give a finite fp32 product, so testing the
+  // operands where they are stored tests the gradient)
+  if (cfg->fuse_update && net->lp != MDNN_F32 && (!cfg->loss_scaling || net->lp == MDNN_F16)) {
+    for (size_t i = 1; i < net->layers.size(); ++i) {
+      LayerPlan& p = net->layers[i];
+      if (p.L.kind != MDNN_LAYER_FC || p.L.c_in % 256 != 0 || p.L.c_out % 256 != 0 || batch % 64 != 0) continue;
+      p.fuse_cand = true;
+      p.dz_off = w;
+      w = align256(w + (size_t)batch * p.L.c_out * lps);
+    }
+  }
   net->g0_off = w;
   w = align256(w + (size_t)batch * max_feat * lps);
   net->g1_off = w;
@@ -234,6 +259,50 @@ extern "C" mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* 
   net->lowp = net->lp == MDNN_F32 ? nullptr : lowp_w;
   net->ws = (char*)workspace;
   net->scaler = net->cfg.loss_scaling ? scaler : nullptr;
+  // fused layers: the candidates whose bound buffers fit the fused product
+  // (a loss-scaled step needs the producer-side tests: prechecked)
+  net->fuse = false;
+  net->rest = CheckRanges{};
+  const bool can_fuse = !net->scaler || net->prechecked;
+  for (size_t i = 0; i < net->layers.size(); ++i) {
+    LayerPlan& p = net->layers[i];
+    p.fused = false;
+    if (!p.fuse_cand || !can_fuse || i == 0) continue;
+    // dW[in, out] = X^T dZ with X = the stored output of layer i - 1; only
+    // where the unfused product would not split K (the fused one never does:
+    // the same summation order keeps the step's results bit for bit)
+    if (gemm_lp_splits(p.L.c_in, p.L.c_out, net->batch) > 1) continue;
+    const char* x = net->ws + net->layers[i - 1].out_off;
+    const char* wlp = (const char*)net->lowp + p.w_off * dtype_size(net->lp);
+    p.fused = gemm_tn_update_ok(net->lp, p.L.c_in, p.L.c_out, net->batch, x, p.L.c_in, net->ws + p.dz_off,
+                                p.L.c_out, net->master + p.w_off, net->mom ? net->mom + p.w_off : nullptr, wlp,
+                                p.L.c_out);
+    net->fuse |= p.fused;
+  }
+  if (net->fuse) {
+    CheckRanges& r = net->rest;
+    auto add = [&](int64_t o, int64_t len) {
+      if (len == 0) return true;
+      if (r.n > 0 && r.off[r.n - 1] + r.len[r.n - 1] == o) {
+        r.len[r.n - 1] += len;
+        return true;
+      }
+      if (r.n == kMaxCheckRanges) return false;
+      r.off[r.n] = o;
+      r.len[r.n] = len;
+      ++r.n;
+      return true;
+    };
+    bool ok = true;
+    for (const auto& p : net->layers) {
+      if (!p.fused) ok &= add(p.w_off, p.nw);
+      ok &= add(p.b_off, p.nb);
+    }
+    if (!ok) {  // too fragmented: no fusion
+      net->fuse = false;
+      for (auto& p : net->layers) p.fused = false;
+    }
+  }
   net->bound = true;
   clear_error();
   return MDNN_SUCCESS;
@@ -281,6 +350,13 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     return i == 0 ? ws + net->in_off : ws + net->layers[i - 1].out_off;
   };
   auto wptr = [&](const LayerPlan& p) { return (const char*)wlp + p.w_off * lps; };
+  // FC weight gradients (and bias gradients) checked for the loss scaler as they are stored
+  int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
+  // fused updates (fuse_update): the activations and output gradients the
+  // fused products read are tested where they are stored, and those
+  // products run after every test of the step
+  const bool fused = net->fuse && !async;
+  int32_t* stored_flag = fused ? nonfinite : nullptr;
 
   // a1: input batch to the storage type (and, asynchronously, this worker's
   // snapshot of the shared weights)
@@ -296,7 +372,7 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     if (p.L.kind == MDNN_LAYER_FC) {
       MDNN_TRY(gemm_mixed_ws(MDNN_NN, B, p.L.c_out, p.L.c_in, 1.0f, act_ptr(i), p.L.c_in, wptr(p), p.L.c_out,
                              lp, 0.0f, nullptr, 0, act_ptr(i + 1), p.L.c_out, out_t, bias, act, nullptr, 0,
-                             ws + net->fws_off, net->fws_bytes, stream));
+                             ws + net->fws_off, net->fws_bytes, stream, stored_flag));
     } else if (p.L.kind == MDNN_LAYER_CONV) {
       mdnn_conv_shape_t cs = conv_shape(p.L, B);
       MDNN_TRY(mdnn_conv2d_fwd(&cs, act_ptr(i), wptr(p), lp, bias, act, act_ptr(i + 1), out_t, stream));
@@ -306,13 +382,17 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     }
   }
 
-  // loss and its gradient (scaled by the loss scale), into grad0
-  char* gcur = ws + net->g0_off;
-  char* gnxt = ws + net->g1_off;
+  // loss and its gradient (scaled by the loss scale), into grad0.  The
+  // gradient with respect to the output of layer i goes to buffer
+  // (L - 1 - i) % 2, or to its own buffer when layer i is fused.
+  const size_t L = net->layers.size();
+  auto dz_of = [&](size_t i) -> char* {
+    if (fused && net->layers[i].fused) return ws + net->layers[i].dz_off;
+    return ws + ((L - 1 - i) % 2 == 0 ? net->g0_off : net->g1_off);
+  };
+  char* gcur = dz_of(L - 1);
   const LayerPlan& last = net->layers.back();
   const float* out = (const float*)act_ptr(net->layers.size());
-  // FC weight gradients (and bias gradients) checked for the loss scaler as they are stored
-  int32_t* nonfinite = (!async && net->scaler && net->prechecked) ? &net->scaler->reserved : nullptr;
   // a classifier head's bias gradient comes out of the loss kernel itself
   const bool head_db = net->cfg.loss == MDNN_LOSS_XENT && last.L.kind == MDNN_LAYER_FC &&
                        softmax_xent_db_ok(B, last.out_feat) && (nonfinite || !net->scaler || async);
@@ -335,6 +415,8 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
   for (size_t ii = net->layers.size(); ii-- > 0;) {
     const LayerPlan& p = net->layers[ii];
     const char* a_in = act_ptr(ii);
+    gcur = dz_of(ii);
+    char* gnxt = ii > 0 ? dz_of(ii - 1) : nullptr;
     float* gw = net->grads + p.w_off;
     float* gb = net->grads + p.b_off;
     const void* mask = p.input_relu ? (const void*)a_in : nullptr;
@@ -359,14 +441,17 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
         MDNN_TRY(mdnn_bias_act_bwd(B, o, gcur, nullptr, MDNN_ACT_NONE, nullptr, gb, lp, ws + net->fws_off,
                                    net->fws_bytes, stream));
       }
-      // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out])
-      MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
-                             nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
-                             nonfinite));
+      // dW[in, out] = X^T dZ  (TN: A = X stored [B, in], B = dZ stored [B, out]); a fused
+      // layer's product runs after the backward pass, updating the weights
+      if (!(fused && p.fused))
+        MDNN_TRY(gemm_mixed_ws(MDNN_TN, in, o, B, 1.0f, a_in, in, gcur, o, lp, 0.0f, nullptr, 0, gw, o, MDNN_F32,
+                               nullptr, MDNN_ACT_NONE, nullptr, 0, ws + net->fws_off, net->fws_bytes, stream,
+                               nonfinite));
       if (ii > 0) {
         // dX[B, in] = dZ W^T, masked by the input's ReLU  (NT: B operand = W stored [in, out])
         MDNN_TRY(gemm_mixed_ws(MDNN_NT, B, in, o, 1.0f, gcur, o, wptr(p), o, lp, 0.0f, nullptr, 0, gnxt, in, lp,
-                               nullptr, MDNN_ACT_NONE, mask, in, ws + net->fws_off, net->fws_bytes, stream));
+                               nullptr, MDNN_ACT_NONE, mask, in, ws + net->fws_off, net->fws_bytes, stream,
+                               stored_flag));
       }
     } else if (p.L.kind == MDNN_LAYER_CONV) {
       mdnn_conv_shape_t cs = conv_shape(p.L, B);
@@ -378,12 +463,25 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
       MDNN_TRY(mdnn_maxpool2_bwd(B, p.L.h, p.L.w, p.L.c_in, gcur, (const uint8_t*)(ws + p.arg_off),
                                  gnxt, lp, stream));
     }
-    char* t = gcur;
-    gcur = gnxt;
-    gnxt = t;
   }
 
   MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
+  if (fused) {
+    // every test of this step is done: the fused layers' weight gradients,
+    // each applied to its weights as it is produced, then the update of the
+    // other parameters (and the scaler's state)
+    if (nonfinite) MDNN_TRY(finite_check_ranges(net->grads, net->unchecked, net->scaler, as_stream(stream)));
+    for (size_t ii = 0; ii < L; ++ii) {
+      const LayerPlan& p = net->layers[ii];
+      if (!p.fused) continue;
+      MDNN_TRY(mdnn_gemm_tn_update(p.L.c_in, p.L.c_out, B, act_ptr(ii), p.L.c_in, dz_of(ii), p.L.c_out, lp,
+                                   net->master + p.w_off, net->mom ? net->mom + p.w_off : nullptr,
+                                   (char*)net->lowp + p.w_off * lps, p.L.c_out, net->cfg.lr, net->cfg.momentum,
+                                   net->scaler, stream));
+    }
+    return sgd_update_ranges_prechecked(net->rest, net->master, net->grads, net->mom, net->lowp, lp, net->cfg.lr,
+                                        net->cfg.momentum, net->scaler, as_stream(stream));
+  }
 
   // update (and the low-precision working copy)
   if (async)

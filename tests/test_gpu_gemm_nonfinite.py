@@ -8,7 +8,8 @@ general MFMA kernel, the skinny rows / cols / depth kernels, the fp32 kernel
 -- a single Inf planted in A makes a whole row of D non-finite and must set
 the flag; the same product with finite inputs must leave it at 0 and store
 exactly what the call without the flag stores.  The flag is never cleared by
-the library.  The planted value and the all-finite expectation come from the
+the library.  16-bit outputs are tested on the stored values (a finite
+result that rounds to Inf counts).  The planted value and the all-finite expectation come from the
 inputs alone (Inf times a nonzero finite value is not finite), no oracle
 arithmetic is needed.
 """
@@ -78,12 +79,44 @@ def test_flag_set_exactly_when_a_stored_value_is_not_finite(mdnn, case):
     assert int(flag.item()) == 1
 
 
-def test_flag_needs_fp32_output(mdnn):
+CASES16 = [  # layout, m, n, k, dtype of A, B and D: which path
+    ("NN", 4096, 4096, 64, "f16"),    # 256 x 256 pipelined kernel
+    ("NT", 1024, 1024, 128, "bf16"),  # 128 x 128 pipelined kernel
+    ("NN", 200, 136, 100, "f16"),     # general MFMA kernel
+    ("NT", 1024, 1024, 1, "f16"),     # skinny depth (outer product)
+]
+
+
+@pytest.mark.parametrize("case", CASES16, ids=lambda c: "%s_%dx%dx%d_%s" % c)
+def test_flag_on_16bit_outputs(mdnn, case):
+    """A 16-bit D is tested as stored: Inf planted in A sets the flag, and so
+    does (fp16) a finite fp32 result that rounds to Inf -- the same row stored
+    in fp32 stays finite and leaves a fresh flag at 0."""
     import torch
-    A = torch.zeros((64, 64), dtype=torch.float16, device="cuda")
-    D = torch.zeros((64, 64), dtype=torch.float16, device="cuda")
+    layout, m, n, k, dt = case
+    sa = (m, k)
+    sb = (n, k) if layout == "NT" else (k, n)
+    a = W.normal(sa, 62, 1, dt, 1.0)
+    b = W.normal(sb, 62, 2, dt, 1 / np.sqrt(k))
+    A, B = dev(a, dt), dev(b, dt)
+    tdt = torch.float16 if dt == "f16" else torch.bfloat16
+
+    def run(flag, out=dt):
+        D = torch.zeros((m, n), dtype=tdt if out != "f32" else torch.float32, device="cuda")
+        mdnn.mdnn_gemm_mixed_ws(LAYOUT[layout], m, n, k, 1.0, A, A.stride(0), B, B.stride(0), DT[dt], 0.0, None,
+                                0, D, n, DT[out], None, 0, None, 0, None, 0, nonfinite=flag)
+        torch.cuda.synchronize()
+        return D
+
     flag = torch.zeros((1,), dtype=torch.int32, device="cuda")
-    with pytest.raises(mdnn.MdnnError) as e:
-        mdnn.mdnn_gemm_mixed_ws(0, 64, 64, 64, 1.0, A, 64, A, 64, DT["f16"], 0.0, None, 0, D, 64, DT["f16"],
-                                None, 0, None, 0, None, 0, nonfinite=flag)
-    assert e.value.status == mdnn.ERR_DTYPE
+    assert torch.equal(run(None), run(flag)) and int(flag.item()) == 0
+    A[7, 0] = float("inf")
+    got = run(flag)
+    assert not torch.isfinite(got[7]).any() and int(flag.item()) == 1
+    if dt == "f16":
+        A[7, :] = 60000.0   # finite, but row 7 of the product is far beyond fp16's range
+        flag.zero_()
+        got = run(flag)
+        assert not torch.isfinite(got[7]).all() and int(flag.item()) == 1
+        f32 = torch.zeros((1,), dtype=torch.int32, device="cuda")
+        assert torch.isfinite(run(f32, "f32")).all() and int(f32.item()) == 0
