@@ -76,11 +76,12 @@ class _Timer:
         self.ms = self.a.elapsed_time(self.b)
 
 
-def _train_setup(mdnn, cfg, n_batches=10):
+def _train_setup(mdnn, cfg, n_batches=10, fuse_update=False):
     import torch
     import workloads as W
     net = mdnn.Net(cfg.layers, cfg.batch, {"f32": 0, "f16": 1, "bf16": 2}[cfg.dtype], cfg.loss,
-                   cfg.lr, cfg.momentum, cfg.loss_scaling, cfg.init_scale, cfg.n_classes)
+                   cfg.lr, cfg.momentum, cfg.loss_scaling, cfg.init_scale, cfg.n_classes,
+                   fuse_update=fuse_update)
     net.set_params(W.init_params(cfg))
     xs, ts = [], []
     for s in range(n_batches):
@@ -223,7 +224,25 @@ def _clocks():
     return res or None
 
 
-def _step_gemms(cfg):
+UPDATE_OUT = "f32 + SGD update"   # a weight-gradient product that applies the update (fuse_update)
+
+
+def _fused(cfg, i) -> bool:
+    """Whether the train step with fuse_update updates FC layer i inside its
+    weight-gradient product (the library's rule: after the first layer, in and
+    out multiples of 256, a batch multiple of 64, 16-bit storage (fp16 when
+    the loss is scaled), and a product the unfused step would not split over
+    K: at least 128 tiles of 128 x 128, or K < 256)."""
+    import workloads as W
+    l = cfg.layers[i]
+    if i == 0 or l.kind != W.FC or cfg.dtype == "f32" or (cfg.loss_scaling and cfg.dtype != "f16"):
+        return False
+    if l.c_in % 256 or l.c_out % 256 or cfg.batch % 64:
+        return False
+    return (l.c_in // 128) * (l.c_out // 128) >= 128 or cfg.batch < 256
+
+
+def _step_gemms(cfg, fuse_update=False):
     """Every GEMM one step of an FC chain issues, as (layout, M, N, K, out)."""
     import workloads as W
     out, B = [], cfg.batch
@@ -232,7 +251,7 @@ def _step_gemms(cfg):
         if l.kind != W.FC:
             continue
         out.append(("NN", B, l.c_out, l.c_in, "f32" if i == n - 1 else cfg.dtype, i))
-        out.append(("TN", l.c_in, l.c_out, B, "f32", i))
+        out.append(("TN", l.c_in, l.c_out, B, UPDATE_OUT if fuse_update and _fused(cfg, i) else "f32", i))
         if i > 0:
             out.append(("NT", B, l.c_in, l.c_out, cfg.dtype, i))
     return out
@@ -283,13 +302,23 @@ def _replay_group(mdnn, net, cfg, group, reps):
     # (masked, partly zero), which the GPU's power and clock depend on
     g0, g1 = net.output_grad_ptr(0), net.output_grad_ptr(1)
     assert g0 and g1
-    calls = []
+    import torch
+    calls, keep = [], []
     for (layout, M, N, K, out_t, i) in group:
         l = cfg.layers[i]
         a_in = net.activation_ptr(i)
         a_out = net.activation_ptr(i + 1)
         wptr = wbase + offs[i][0] * es
         bias = net.master.data_ptr() + offs[i][1] * 4
+        if out_t == UPDATE_OUT:
+            # the fused update, on copies of the layer's weights, momentum and
+            # working copy (replays must not move the net's own parameters)
+            w0, nw = offs[i][0], M * N
+            cp = (net.master[w0:w0 + nw].clone(), net.mom[w0:w0 + nw].clone() if net.mom is not None else None,
+                  net.lowp[w0:w0 + nw].clone())
+            keep.append(cp)
+            calls.append(("upd", M, N, K, a_in, M, g0, N, cp))
+            continue
         if layout == "NN":
             calls.append((0, M, N, K, a_in, K, wptr, N, a_out, N, 0 if out_t == "f32" else lp,
                           bias, l.act, None, 0))
@@ -305,7 +334,6 @@ def _replay_group(mdnn, net, cfg, group, reps):
     # for the host; the mean launch duration is the elapsed time over the
     # launches (an event pair around every launch added about 5 us to each,
     # against the kernel trace's durations of the same launches)
-    import torch
     # the step's split-K workspace and, for the weight gradients, its loss
     # scaler's overflow flag: the replay takes the kernel paths the step takes
     ws_bytes = max([mdnn.mdnn_gemm_workspace(lp, c[1], c[2], c[3]) for c in calls] + [256])
@@ -313,6 +341,11 @@ def _replay_group(mdnn, net, cfg, group, reps):
     flag = torch.zeros(1, dtype=torch.int32, device="cuda")
 
     def launch(c):
+        if c[0] == "upd":
+            w, v, wl = c[8]
+            mdnn.mdnn_gemm_tn_update(c[1], c[2], c[3], c[4], c[5], c[6], c[7], lp, w, v, wl, c[2], cfg.lr,
+                                     cfg.momentum, net.scaler)
+            return
         mdnn.mdnn_gemm_mixed_ws(c[0], c[1], c[2], c[3], 1.0, c[4], c[5], c[6], c[7], lp, 0.0,
                                 None, 0, c[8], c[9], c[10], c[11], c[12], c[13], c[14], ws, ws_bytes,
                                 nonfinite=flag if c[0] == 2 and c[10] == 0 else None)
@@ -333,6 +366,9 @@ def _replay_group(mdnn, net, cfg, group, reps):
 
 
 GRAPH_CALLS = 32
+# the headline step updates its hidden layers inside their weight-gradient
+# products (mdnn_train_cfg_t.fuse_update: bitwise the same step)
+FUSE_UPDATE = True
 
 
 def _graph_measure(fn, reps_scale=1.0):
@@ -694,7 +730,7 @@ def main():
 
     clocks_before = _clocks()
     cfg = W.wide_mlp_fp16()
-    net, xs, ts = _train_setup(mdnn, cfg)
+    net, xs, ts = _train_setup(mdnn, cfg, fuse_update=FUSE_UPDATE)
     check = _UpdateCheck(mdnn, net)
     ms = _time_steps(net, xs, ts, args.steps, args.warmup, check)
     applied = check.stop(args.steps)
@@ -711,7 +747,7 @@ def main():
     # every kernel instantiation (layout, output type, tile) of the step's
     # GEMMs, its launches replayed as the step issues them; the dominant
     # kernel is the one whose launches take the most time per step
-    gemms = _step_gemms(cfg)
+    gemms = _step_gemms(cfg, FUSE_UPDATE)
     groups = {}
     for g in gemms:
         groups.setdefault((g[0], g[4], _kernel_choice(g[0], g[1], g[2], g[3])), []).append(g)
@@ -731,6 +767,16 @@ def main():
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_F16_TFLOPS, 4), "traffic": None,
                 "kernel": f"{key[2]}, {key[0]} f16 -> {key[1]}, {nl} launches per step",
                 "avg_launch_ms": round(mpl, 4), "flop_per_launch": fpl}
+    if key[1] == UPDATE_OUT:
+        # the product's MFMA work and then its update's HBM bytes (operands,
+        # then weights and momentum read and written, the fp16 copy written),
+        # one after the other in each workgroup: the bound is their sum
+        g = [c for c in gemms if c[0] == key[0] and c[4] == key[1]][0]
+        mn = g[1] * g[2]
+        upd_bytes = 2.0 * (g[1] + g[2]) * g[3] + mn * (18 if cfg.momentum else 10)
+        t_bound = fpl / (PEAK_F16_TFLOPS * 1e12) + upd_bytes / (PEAK_HBM_GBS * 1e9)
+        roofline["update_bytes_per_launch"] = upd_bytes
+        roofline["mfma_then_hbm_bound_frac"] = round(t_bound / (mpl * 1e-3), 4)
     print(f"[bench] dominant kernel {roofline['kernel']}: {mpl:.4f} ms/launch, "
           f"{achieved:.1f} TFLOP/s", file=sys.stderr, flush=True)
 
@@ -747,7 +793,7 @@ def main():
         "config": {"workload": f"{cfg.name}: wide regression MLP 1024->4x4096(ReLU)->1, MSE, "
                                "fp16 storage, fp32 accumulate + master weights, dynamic loss "
                                f"scaling (2^16), SGD momentum {cfg.momentum}, lr {cfg.lr:g}",
-                   "global_batch": cfg.batch, "parallelism": "single GPU",
+                   "global_batch": cfg.batch, "parallelism": "single GPU", "fuse_update": FUSE_UPDATE,
                    "step_tflops": round(step_tf, 1),
                    "graph_ms_per_step": round(graph_ms, 4),
                    "every_timed_update_applied": bool(applied and graph_applied),

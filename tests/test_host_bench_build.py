@@ -74,7 +74,7 @@ def test_traffic_record_lookup(monkeypatch):
     sha = [ln.split(":", 1)[1].strip() for ln in open(path) if ln.startswith("source_sha256:")][0]
     monkeypatch.setattr(bench, "gemm_lds_source_digest", lambda: sha)
     desc = "gemm_lds_kernel (256x256 direct-to-LDS pipeline), {} f16 -> {}, 3 launches per step"
-    for lay, out in (("NN", "f16"), ("NT", "f16"), ("TN", "f32")):
+    for lay, out in (("NN", "f16"), ("NT", "f16"), ("TN", bench.UPDATE_OUT)):
         rec = bench._traffic_record(desc.format(lay, out))
         assert rec is not None and rec > 0, lay
     assert bench._traffic_record("skinny rows kernel, NN f16 -> f32, 1 launches per step") is None
@@ -106,3 +106,21 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stdout + r.stderr
+
+
+def test_fused_layers_of_the_step():
+    """bench.py's mirror of the library's fuse_update rule: the wide MLP's
+    three 4096 x 4096 hidden layers are updated in their weight-gradient
+    products, the first layer (its input is not tested on the way in) and the
+    one-output head are not; LeNet (bf16 FC layers too small to skip the K
+    split) and fp32 nets never."""
+    import workloads as W
+    cfg = W.wide_mlp_fp16()
+    assert [bench._fused(cfg, i) for i in range(len(cfg.layers))] == [False, True, True, True, False]
+    tn = [g for g in bench._step_gemms(cfg, True) if g[0] == "TN"]
+    assert [g[4] for g in tn] == ["f32", bench.UPDATE_OUT, bench.UPDATE_OUT, bench.UPDATE_OUT, "f32"]
+    assert all(g[4] == "f32" for g in bench._step_gemms(cfg, False) if g[0] == "TN")
+    small = W.wide_mlp_fp16(batch=512, width=1024)   # 64 tiles: the unfused step splits K
+    assert not any(bench._fused(small, i) for i in range(len(small.layers)))
+    for c in (W.lenet_bf16(), W.mlp784_fp32()):
+        assert not any(bench._fused(c, i) for i in range(len(c.layers)))
