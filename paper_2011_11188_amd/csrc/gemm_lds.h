@@ -738,16 +738,42 @@ struct UpdateArgs {
   float S, alpha;
   bool mom;
 };
+template <class TL>
+struct UpdateShape {
+  static constexpr int S4 = TL::BN / 4;                  // float4 slots per row
+  static constexpr int ROWS = TL::A_BYTES / (TL::BN * 4);  // rows per pass
+  static constexpr int PER = ROWS * S4 / TL::NT;          // float4 per thread per pass
+  static_assert(ROWS == 32 && ROWS * S4 == PER * TL::NT && TL::WTM % ROWS == 0, "update staging shape");
+};
+typedef float upd_f4v __attribute__((ext_vector_type(4)));
+
+// this thread's weight and momentum quads of pass P
+template <class TL, int P>
+__device__ __forceinline__ void update_loads(const Epilogue& ep, int64_t m0, int64_t n0, int tid, bool mom,
+                                             upd_f4v (&wq)[UpdateShape<TL>::PER],
+                                             upd_f4v (&vq)[UpdateShape<TL>::PER]) {
+  typedef UpdateShape<TL> U;
+#pragma unroll
+  for (int k = 0; k < U::PER; ++k) {
+    const int idx = tid + k * TL::NT, r = idx / U::S4, s = idx % U::S4;
+    const int64_t e = (m0 + P * U::ROWS + r) * ep.ldd + n0 + 4 * s;
+    wq[k] = *(const upd_f4v*)(ep.upd_w + e);
+    if (mom) vq[k] = *(const upd_f4v*)(ep.upd_v + e);
+  }
+}
+
+// Pass P: issue its weight and momentum loads, stage its rows, read them
+// back in row order (the loads' latency hides behind the staging and the
+// barriers), then update.
 template <class T, class TL, int P, int FM, int FN>
 __device__ __forceinline__ void update_pass(const Epilogue& ep, float4* st, int64_t m0, int64_t n0, int wm, int wn,
                                             int lane, int tid, const float4_t (&acc)[FM][FN], const UpdateArgs& u) {
-  typedef float f4v __attribute__((ext_vector_type(4)));
   typedef uint32_t u2v __attribute__((ext_vector_type(2)));
-  constexpr int BN = TL::BN, S4 = BN / 4;          // float4 slots per row
-  constexpr int ROWS = TL::A_BYTES / (BN * 4);     // rows per pass
-  constexpr int PER = ROWS * S4 / TL::NT;           // float4 per thread per pass
-  static_assert(ROWS == 32 && ROWS * S4 == PER * TL::NT && TL::WTM % ROWS == 0, "update staging shape");
+  typedef UpdateShape<TL> U;
+  constexpr int S4 = U::S4, ROWS = U::ROWS, PER = U::PER;
   if constexpr (P * ROWS < TL::BM) {
+    upd_f4v wq[PER], vq[PER];
+    update_loads<TL, P>(ep, m0, n0, tid, u.mom, wq, vq);
     // the waves whose rows fall in this pass (wave row WMP) stage their two
     // fragment rows I0, I0 + 1
     constexpr int WMP = P * ROWS / TL::WTM, I0 = (P * ROWS - WMP * TL::WTM) / 16;
@@ -770,14 +796,6 @@ __device__ __forceinline__ void update_pass(const Epilogue& ep, float4* st, int6
       gq[k] = st[r * S4 + (s ^ (r & 15))];
     }
     __syncthreads();  // the next pass may overwrite the stage
-    f4v wq[PER], vq[PER];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int idx = tid + k * TL::NT, r = idx / S4, s = idx % S4;
-      const int64_t e = (m0 + P * ROWS + r) * ep.ldd + n0 + 4 * s;
-      wq[k] = *(const f4v*)(ep.upd_w + e);
-      if (u.mom) vq[k] = *(const f4v*)(ep.upd_v + e);
-    }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int idx = tid + k * TL::NT, r = idx / S4, s = idx % S4;
@@ -797,8 +815,8 @@ __device__ __forceinline__ void update_pass(const Epilogue& ep, float4* st, int6
           w[c] = fmaf(-ep.upd_lr, g, w[c]);
         }
       }
-      *(f4v*)(ep.upd_w + e) = (f4v){w[0], w[1], w[2], w[3]};
-      if (u.mom) *(f4v*)(ep.upd_v + e) = (f4v){v[0], v[1], v[2], v[3]};
+      *(upd_f4v*)(ep.upd_w + e) = (upd_f4v){w[0], w[1], w[2], w[3]};
+      if (u.mom) *(upd_f4v*)(ep.upd_v + e) = (upd_f4v){v[0], v[1], v[2], v[3]};
       if (ep.upd_lp) {
         u2v q;
         q[0] = (uint32_t)from_f<T>(w[0]) | ((uint32_t)from_f<T>(w[1]) << 16);
