@@ -30,9 +30,12 @@ SHAPES = [  # M, N, K: the pipelined tile the product takes
 
 
 def _scaler(mdnn, scale, reserved=0):
+    """A device scaler; reserved (the pending-overflow flag, the struct's
+    eighth 32-bit field) set when asked."""
+    import torch
     sc = mdnn.make_scaler(scale)
     if reserved:
-        sc.view(__import__("torch").int32)[7] = reserved
+        sc.view(torch.int32)[7] = reserved
     return sc
 
 
