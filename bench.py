@@ -494,6 +494,27 @@ def _sustained_clock(mdnn, net=None, xs=None, ts=None, cfg=None):
     return res
 
 
+def _fuse_ab(mdnn, rounds=3, steps=50):
+    """The headline step with and without fuse_update, alternating in one
+    process (the same box and clock state for both): ms per step of each
+    round, and whether every timed step applied its update."""
+    import torch
+    import workloads as W
+    cfg = W.wide_mlp_fp16()
+    res = {"unfused_ms": [], "fused_ms": [], "every_update_applied": True}
+    for _ in range(rounds):
+        for fuse in (False, True):
+            net, xs, ts = _train_setup(mdnn, cfg, fuse_update=fuse)
+            check = _UpdateCheck(mdnn, net)
+            ms = _time_steps(net, xs, ts, steps, 5, check)
+            res["every_update_applied"] &= bool(check.stop(steps))
+            res["fused_ms" if fuse else "unfused_ms"].append(round(ms, 4))
+            net.close()
+            del net, xs, ts
+            torch.cuda.empty_cache()
+    return res
+
+
 def _split3_sweep(mdnn):
     """fp32 GEMMs through three fp16 MFMA products (section 3.2, Eq. (1)),
     next to the native fp32 (VALU) kernel; inputs fp32 N(0,1)/sqrt(K)."""
@@ -704,7 +725,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--quick", action="store_true", help="headline only (no sub-benchmarks)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
-    ap.add_argument("--only", choices=["gemm", "conv", "split3", "workloads", "async", "clock"],
+    ap.add_argument("--only", choices=["gemm", "conv", "split3", "workloads", "async", "clock", "fuse_ab"],
                     help="profiling runs: the counter calibration copy and one sub-benchmark, printed as JSON "
                          "(no headline line)")
     args = ap.parse_args()
@@ -724,7 +745,7 @@ def main():
     if args.only:
         _copy_calibration(mdnn)
         subs = {"gemm": _gemm_sweep, "conv": _conv_bench, "split3": _split3_sweep, "workloads": _workloads_bench,
-                "async": _async_bench, "clock": _sustained_clock}
+                "async": _async_bench, "clock": _sustained_clock, "fuse_ab": _fuse_ab}
         print(json.dumps({args.only: subs[args.only](mdnn), "clocks": _clocks()}), flush=True)
         return
 
