@@ -229,13 +229,13 @@ UPDATE_OUT = "f32 + SGD update"   # a weight-gradient product that applies the u
 
 def _fused(cfg, i) -> bool:
     """Whether the train step with fuse_update updates FC layer i inside its
-    weight-gradient product (the library's rule: after the first layer, in and
-    out multiples of 256, a batch multiple of 64, 16-bit storage (fp16 when
-    the loss is scaled), and a product the unfused step would not split over
-    K: at least 128 tiles of 128 x 128, or K < 256)."""
+    weight-gradient product (the library's rule: in and out multiples of 256,
+    a batch multiple of 64, 16-bit storage (fp16 when the loss is scaled), and
+    a product the unfused step would not split over K: at least 128 tiles of
+    128 x 128, or K < 256)."""
     import workloads as W
     l = cfg.layers[i]
-    if i == 0 or l.kind != W.FC or cfg.dtype == "f32" or (cfg.loss_scaling and cfg.dtype != "f16"):
+    if l.kind != W.FC or cfg.dtype == "f32" or (cfg.loss_scaling and cfg.dtype != "f16"):
         return False
     if l.c_in % 256 or l.c_out % 256 or cfg.batch % 64:
         return False

@@ -465,7 +465,7 @@ typedef struct {
   float momentum;       /* 0: plain SGD (momentum buffer may be NULL)          */
   int32_t loss_scaling; /* nonzero: dynamic loss scaling via the bound scaler  */
   int32_t n_classes;    /* cross-entropy classes (= last layer's outputs)      */
-  int32_t fuse_update;  /* nonzero: FC layers after the first whose weight
+  int32_t fuse_update;  /* nonzero: FC layers whose weight
                            gradient fits mdnn_gemm_tn_update (in and out
                            multiples of 256, batch a multiple of 64, 16-bit
                            storage; fp16 when the loss is scaled; buffers

@@ -84,6 +84,55 @@ __global__ void cast_kernel(const typename Src::storage* __restrict__ src,
   }
 }
 
+// fp32 -> 16-bit cast that also sets *nonfinite when a stored value is Inf
+// or NaN (an all-ones exponent: finite inputs beyond the type's range count)
+template <class Dst, bool VEC>
+__global__ void cast_checked_kernel(const float* __restrict__ src, typename Dst::storage* __restrict__ dst, int64_t n,
+                                    int32_t* __restrict__ nonfinite) {
+  constexpr uint16_t EXP = Dst::id == MDNN_F16 ? 0x7c00u : 0x7f80u;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  bool bad = false;
+  if (VEC) {
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n; i += stride * 4) {
+      float v[4];
+      load_quad<F32>(src + i, v);
+      store_quad<Dst>(dst + i, v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bad |= (from_f<Dst>(v[e]) & EXP) == EXP;
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+      const uint16_t h = from_f<Dst>(src[i]);
+      dst[i] = h;
+      bad |= (h & EXP) == EXP;
+    }
+  }
+  if (bad) atomicOr(nonfinite, 1);
+}
+
+mdnn_status_t cast_f32_checked(int64_t n, const float* src, void* dst, mdnn_dtype_t d, int32_t* nonfinite,
+                               hipStream_t st) {
+  if (n == 0) return MDNN_SUCCESS;
+  if (d != MDNN_F16 && d != MDNN_BF16) return fail(MDNN_ERR_DTYPE, "cast: the checked cast writes 16-bit values");
+  const bool vec = n % 4 == 0 && aligned(src, 16) && aligned(dst, 8);
+  const unsigned g = stream_grid(ceil_div(n, vec ? 4 : 1));
+  if (d == MDNN_F16) {
+    if (vec)
+      hipLaunchKernelGGL((cast_checked_kernel<F16, true>), dim3(g), dim3(256), 0, st, src, (uint16_t*)dst, n, nonfinite);
+    else
+      hipLaunchKernelGGL((cast_checked_kernel<F16, false>), dim3(g), dim3(256), 0, st, src, (uint16_t*)dst, n,
+                         nonfinite);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((cast_checked_kernel<BF16, true>), dim3(g), dim3(256), 0, st, src, (uint16_t*)dst, n,
+                         nonfinite);
+    else
+      hipLaunchKernelGGL((cast_checked_kernel<BF16, false>), dim3(g), dim3(256), 0, st, src, (uint16_t*)dst, n,
+                         nonfinite);
+  }
+  return check_launch("cast_checked_kernel");
+}
+
 template <class Src, class Dst>
 static void cast_launch(const void* src, void* dst, int64_t n, bool vec, hipStream_t st) {
   const unsigned g = stream_grid(ceil_div(n, vec ? 4 : 1));

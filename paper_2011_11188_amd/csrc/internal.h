@@ -43,6 +43,10 @@ mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t stream);
 // Element-wise conversion between any two storage types (RNE when narrowing).
 mdnn_status_t cast_any(int64_t n, const void* src, mdnn_dtype_t s, void* dst, mdnn_dtype_t d,
                        hipStream_t stream);
+// fp32 -> F16 / BF16 as cast_any, also setting *nonfinite (atomic OR) when a
+// stored value is Inf or NaN.
+mdnn_status_t cast_f32_checked(int64_t n, const float* src, void* dst, mdnn_dtype_t d, int32_t* nonfinite,
+                               hipStream_t stream);
 // Deterministic column sums of a [rows, cols] matrix x of type t (entries
 // where y <= 0 skipped when y != NULL) into fp32 out[cols].  Uses a two-pass
 // reduction when a workspace of column_sums_ws_bytes(rows, cols) bytes is

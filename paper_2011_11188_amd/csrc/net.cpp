@@ -205,13 +205,13 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
     if (p.in_feat > max_feat) max_feat = p.in_feat;
     if (p.out_feat > max_feat) max_feat = p.out_feat;
   }
-  // fuse_update candidates: FC layers after the first (the first layer's
-  // input is not tested for Inf / NaN on the way in) whose weight gradient
-  // takes mdnn_gemm_tn_update's shapes; fp16 storage when the loss is scaled
+  // fuse_update candidates: FC layers whose weight gradient takes
+  // mdnn_gemm_tn_update's shapes; fp16 storage when the loss is scaled
   // (finite fp16 operands give a finite fp32 product, so testing the
-  // operands where they are stored tests the gradient)
+  // operands where they are stored -- the input batch's cast included --
+  // tests the gradient)
   if (cfg->fuse_update && net->lp != MDNN_F32 && (!cfg->loss_scaling || net->lp == MDNN_F16)) {
-    for (size_t i = 1; i < net->layers.size(); ++i) {
+    for (size_t i = 0; i < net->layers.size(); ++i) {
       LayerPlan& p = net->layers[i];
       if (p.L.kind != MDNN_LAYER_FC || p.L.c_in % 256 != 0 || p.L.c_out % 256 != 0 || batch % 64 != 0) continue;
       p.fuse_cand = true;
@@ -267,12 +267,12 @@ extern "C" mdnn_status_t mdnn_net_bind(mdnn_net_t* net, float* master_w, float* 
   for (size_t i = 0; i < net->layers.size(); ++i) {
     LayerPlan& p = net->layers[i];
     p.fused = false;
-    if (!p.fuse_cand || !can_fuse || i == 0) continue;
-    // dW[in, out] = X^T dZ with X = the stored output of layer i - 1; only
-    // where the unfused product would not split K (the fused one never does:
-    // the same summation order keeps the step's results bit for bit)
+    if (!p.fuse_cand || !can_fuse) continue;
+    // dW[in, out] = X^T dZ with X = the stored input of layer i; only where
+    // the unfused product would not split K (the fused one never does: the
+    // same summation order keeps the step's results bit for bit)
     if (gemm_lp_splits(p.L.c_in, p.L.c_out, net->batch) > 1) continue;
-    const char* x = net->ws + net->layers[i - 1].out_off;
+    const char* x = net->ws + (i == 0 ? net->in_off : net->layers[i - 1].out_off);
     const char* wlp = (const char*)net->lowp + p.w_off * dtype_size(net->lp);
     p.fused = gemm_tn_update_ok(net->lp, p.L.c_in, p.L.c_out, net->batch, x, p.L.c_in, net->ws + p.dz_off,
                                 p.L.c_out, net->master + p.w_off, net->mom ? net->mom + p.w_off : nullptr, wlp,
@@ -360,7 +360,10 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
 
   // a1: input batch to the storage type (and, asynchronously, this worker's
   // snapshot of the shared weights)
-  MDNN_TRY(mdnn_cast(B * net->in_feat, x, MDNN_F32, act_ptr(0), lp, stream));
+  if (stored_flag && lp != MDNN_F32)
+    MDNN_TRY(cast_f32_checked(B * net->in_feat, x, act_ptr(0), lp, stored_flag, as_stream(stream)));
+  else
+    MDNN_TRY(mdnn_cast(B * net->in_feat, x, MDNN_F32, act_ptr(0), lp, stream));
   if (async && net->lowp) MDNN_TRY(mdnn_cast(net->n_params, net->master, MDNN_F32, net->lowp, lp, stream));
 
   // forward

@@ -164,13 +164,13 @@ def _same_state(mdnn, a, b, n_fused_ranges):
 
 def _fused_ranges(cfg):
     """Flat (offset, length) of the weights the fused net updates in the
-    product: FC layers after the first with in, out multiples of 256, a batch
-    multiple of 64, and a product of at least 128 tiles of 128 x 128 (so that
-    the unfused step does not split it over K)."""
+    product: FC layers with in, out multiples of 256, a batch multiple of 64,
+    and a product of at least 128 tiles of 128 x 128 (so that the unfused
+    step does not split it over K)."""
     out, off = [], 0
     for i, l in enumerate(cfg.layers):
         nw = l.c_in * l.c_out
-        if (i > 0 and l.c_in % 256 == 0 and l.c_out % 256 == 0 and cfg.batch % 64 == 0
+        if (l.c_in % 256 == 0 and l.c_out % 256 == 0 and cfg.batch % 64 == 0
                 and (l.c_in // 128) * (l.c_out // 128) >= 128):
             out.append((off, nw))
         off += nw + l.c_out
@@ -178,17 +178,21 @@ def _fused_ranges(cfg):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("case", ["scaled_with_overflows", "full_size"])
+@pytest.mark.parametrize("case", ["scaled_with_overflows", "input_beyond_fp16", "full_size"])
 def test_train_step_fused_matches_unfused(mdnn, case):
     """fuse_update changes where the update of the hidden layers' weights
     runs, not what it computes: the trajectories agree bit for bit (loss,
     master weights, momentum, working copy, scaler state, stored gradients),
     here through steps whose update is skipped (initial scale 2^40: the
     scaled gradients overflow in fp16 until the scale has halved enough) and
-    the applied steps after them, and at the benchmark's full size."""
+    the applied steps after them, through an input value that overflows
+    fp16 when the batch is stored (only the input cast can see it before the
+    first layer's fused product runs), and at the benchmark's full size."""
     import torch
     if case == "full_size":
         cfg, steps = W.wide_mlp_fp16(), 4
+    elif case == "input_beyond_fp16":
+        cfg, steps = W.wide_mlp_fp16(batch=512, width=2048), 3
     else:
         cfg, steps = W.wide_mlp_fp16(batch=512, width=2048, init_scale=2.0 ** 40), 30
     fr = _fused_ranges(cfg)
@@ -197,12 +201,16 @@ def test_train_step_fused_matches_unfused(mdnn, case):
     skipped = 0
     for s in range(steps):
         x, t = W.batch_inputs(cfg, s)
+        if case == "input_beyond_fp16" and s == 1:
+            x[5, 7] = 1.0e6   # finite in fp32, Inf once stored in fp16: the step must skip its update
         X, T = dev(x, "f32"), dev(t, "f32")
         la = plain.step(X, T)
         lb = fused.step(X, T)
-        assert torch.equal(la, lb), f"step {s}"
+        assert torch.equal(la.view(torch.int32), lb.view(torch.int32)), f"step {s}"   # bitwise (NaN included)
         _same_state(mdnn, plain, fused, fr)
         skipped += mdnn.read_scaler(fused.scaler)["overflow"]
+        if case == "input_beyond_fp16":
+            assert mdnn.read_scaler(fused.scaler)["overflow"] == (1 if s == 1 else 0), f"step {s}"
     if case != "full_size":
         assert skipped >= 1, "the case is meant to skip updates"
     assert mdnn.read_scaler(fused.scaler)["good_steps"] >= 1

@@ -110,15 +110,14 @@ def test_bench_refuses_more_than_one_gpu():
 
 def test_fused_layers_of_the_step():
     """bench.py's mirror of the library's fuse_update rule: the wide MLP's
-    three 4096 x 4096 hidden layers are updated in their weight-gradient
-    products, the first layer (its input is not tested on the way in) and the
-    one-output head are not; LeNet (bf16 FC layers too small to skip the K
-    split) and fp32 nets never."""
+    first layer (1024 x 4096) and three 4096 x 4096 hidden layers are updated
+    in their weight-gradient products, the one-output head is not; LeNet
+    (bf16 FC layers too small to skip the K split) and fp32 nets never."""
     import workloads as W
     cfg = W.wide_mlp_fp16()
-    assert [bench._fused(cfg, i) for i in range(len(cfg.layers))] == [False, True, True, True, False]
+    assert [bench._fused(cfg, i) for i in range(len(cfg.layers))] == [True, True, True, True, False]
     tn = [g for g in bench._step_gemms(cfg, True) if g[0] == "TN"]
-    assert [g[4] for g in tn] == ["f32", bench.UPDATE_OUT, bench.UPDATE_OUT, bench.UPDATE_OUT, "f32"]
+    assert [g[4] for g in tn] == [bench.UPDATE_OUT] * 4 + ["f32"]
     assert all(g[4] == "f32" for g in bench._step_gemms(cfg, False) if g[0] == "TN")
     small = W.wide_mlp_fp16(batch=512, width=1024)   # 64 tiles: the unfused step splits K
     assert not any(bench._fused(small, i) for i in range(len(small.layers)))
