@@ -792,7 +792,7 @@ def main():
         # the product's MFMA work and then its update's HBM bytes (operands,
         # then weights and momentum read and written, the fp16 copy written),
         # one after the other in each workgroup: the bound is their sum
-        g = [c for c in gemms if c[0] == key[0] and c[4] == key[1]][0]
+        g = groups[key][0]
         mn = g[1] * g[2]
         upd_bytes = 2.0 * (g[1] + g[2]) * g[3] + mn * (18 if cfg.momentum else 10)
         t_bound = fpl / (PEAK_F16_TFLOPS * 1e12) + upd_bytes / (PEAK_HBM_GBS * 1e9)
