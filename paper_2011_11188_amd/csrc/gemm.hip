@@ -168,13 +168,14 @@ colsum_partial_kernel(const typename T::storage* __restrict__ x, const typename 
 constexpr int64_t COLSUM_STRIP_ROWS = 64;
 static bool colsum_strip(mdnn_dtype_t t, int64_t cols) { return t != MDNN_F32 && cols % 512 == 0; }
 
+// block (bx, by): columns bx * 512 .. + 511 of row chunk by
 template <class T>
-__global__ void __launch_bounds__(256)
-colsum_strip_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols, float* __restrict__ partial) {
+__device__ __forceinline__ void colsum_strip_block(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                   float* __restrict__ partial, int64_t bx, int64_t by) {
   __shared__ float4 red[4][2][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t c0 = (int64_t)blockIdx.x * 512 + lane * 8;
-  const int64_t r0 = (int64_t)blockIdx.y * COLSUM_STRIP_ROWS;
+  const int64_t c0 = bx * 512 + lane * 8;
+  const int64_t r0 = by * COLSUM_STRIP_ROWS;
   const int64_t nr = rows - r0 < COLSUM_STRIP_ROWS ? rows - r0 : COLSUM_STRIP_ROWS;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   auto add8 = [&](const uint4& v) {
@@ -206,7 +207,22 @@ colsum_strip_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols, 
     t.x += q ? v.z : v.x;
     t.y += q ? v.w : v.y;
   }
-  *(float2*)(partial + blockIdx.y * cols + (int64_t)blockIdx.x * 512 + 2 * threadIdx.x) = t;
+  *(float2*)(partial + by * cols + bx * 512 + 2 * threadIdx.x) = t;
+}
+
+template <class T>
+__global__ void __launch_bounds__(256)
+colsum_strip_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols, float* __restrict__ partial) {
+  colsum_strip_block<T>(x, rows, cols, partial, blockIdx.x, blockIdx.y);
+}
+
+// several matrices of the same height in one launch (grid z = matrix); the
+// blocks of each are those of colsum_strip_kernel, so the partials are the same
+template <class T>
+__global__ void __launch_bounds__(256) colsum_strip_batch_kernel(StripBatch b, int64_t rows) {
+  const int i = blockIdx.z;
+  if ((int64_t)blockIdx.x * 512 >= b.cols[i]) return;  // the whole block: narrower than the widest
+  colsum_strip_block<T>(b.x[i], rows, b.cols[i], b.partial[i], blockIdx.x, blockIdx.y);
 }
 
 // sum of partial[k][c] over k = ln, ln + 8, ... < chunks, in that order,
@@ -374,6 +390,30 @@ mdnn_status_t column_sums_partial(const void* x, mdnn_dtype_t t, int64_t rows, i
                          cols, vec, partial);
   }
   return check_launch("column sums (partials)");
+}
+
+bool column_sums_strip_ok(const void* x, mdnn_dtype_t t, int64_t cols, const float* partial) {
+  return colsum_strip(t, cols) && aligned(x, 16) && aligned(partial, 8);
+}
+
+mdnn_status_t column_sums_partial_batch(const StripBatch& b, mdnn_dtype_t t, int64_t rows, hipStream_t st) {
+  if (b.n <= 0) return MDNN_SUCCESS;
+  if (b.n > kMaxColsumBatch) return fail(MDNN_ERR_SHAPE, "column sums: batch too large");
+  int64_t widest = 0;
+  for (int i = 0; i < b.n; ++i) {
+    if (!column_sums_strip_ok(b.x[i], t, b.cols[i], b.partial[i]))
+      return fail(MDNN_ERR_SHAPE, "column sums: a batched matrix does not take the strip pass");
+    widest = b.cols[i] > widest ? b.cols[i] : widest;
+  }
+  const int64_t chunks = column_sums_chunks(rows, widest, t);
+  if (widest == 0 || chunks == 0) return MDNN_SUCCESS;
+  if (chunks > 65535) return fail(MDNN_ERR_SHAPE, "column sums: too many rows");
+  const dim3 grid((unsigned)(widest / 512), (unsigned)chunks, (unsigned)b.n);
+  if (t == MDNN_F16)
+    hipLaunchKernelGGL(colsum_strip_batch_kernel<F16>, grid, dim3(256), 0, st, b, rows);
+  else
+    hipLaunchKernelGGL(colsum_strip_batch_kernel<BF16>, grid, dim3(256), 0, st, b, rows);
+  return check_launch("column sums (batched partials)");
 }
 
 mdnn_status_t column_sums_final(const ColsumBatch& b, int32_t* nonfinite, hipStream_t st) {

@@ -83,6 +83,18 @@ struct ColsumBatch {
   int64_t chunks[kMaxColsumBatch], cols[kMaxColsumBatch];
 };
 mdnn_status_t column_sums_final(const ColsumBatch& b, int32_t* nonfinite, hipStream_t stream);
+// Pass 1 for several matrices of one height in one launch, each a 16-bit
+// matrix of a multiple of 512 columns (16-byte aligned rows, 8-byte aligned
+// partials: column_sums_strip_ok); the partials are those column_sums_partial
+// writes.
+struct StripBatch {
+  int32_t n;
+  const uint16_t* x[kMaxColsumBatch];
+  float* partial[kMaxColsumBatch];
+  int64_t cols[kMaxColsumBatch];
+};
+bool column_sums_strip_ok(const void* x, mdnn_dtype_t t, int64_t cols, const float* partial);
+mdnn_status_t column_sums_partial_batch(const StripBatch& b, mdnn_dtype_t t, int64_t rows, hipStream_t stream);
 
 // mdnn_gemm_mixed with an optional workspace (NULL / too small: same as
 // mdnn_gemm_mixed).  With one, fp32 problems whose grid would be a handful of

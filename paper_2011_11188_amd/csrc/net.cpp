@@ -415,6 +415,9 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
   // loss-scaled FC bias gradients: partial column sums per layer now, all
   // layers finished (and checked) in one launch after the loop
   ColsumBatch bias_sums{};
+  // fused layers' output gradients stay in their own buffers: their partial
+  // sums go in one batched launch after the loop
+  StripBatch strips{};
   for (size_t ii = net->layers.size(); ii-- > 0;) {
     const LayerPlan& p = net->layers[ii];
     const char* a_in = act_ptr(ii);
@@ -430,8 +433,17 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
         // done by the loss kernel
       } else if (nonfinite) {
         float* part = (float*)(ws + p.cs_off);
-        MDNN_TRY(column_sums_partial(gcur, lp, B, o, part, as_stream(stream)));
+        if (fused && p.fused && strips.n < kMaxColsumBatch && column_sums_strip_ok(gcur, lp, o, part)) {
+          strips.x[strips.n] = (const uint16_t*)gcur;
+          strips.partial[strips.n] = part;
+          strips.cols[strips.n] = o;
+          ++strips.n;
+        } else {
+          MDNN_TRY(column_sums_partial(gcur, lp, B, o, part, as_stream(stream)));
+        }
         if (bias_sums.n == kMaxColsumBatch) {
+          MDNN_TRY(column_sums_partial_batch(strips, lp, B, as_stream(stream)));
+          strips.n = 0;
           MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
           bias_sums.n = 0;
         }
@@ -468,6 +480,7 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     }
   }
 
+  MDNN_TRY(column_sums_partial_batch(strips, lp, B, as_stream(stream)));
   MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
   if (fused) {
     // every test of this step is done: the fused layers' weight gradients,
