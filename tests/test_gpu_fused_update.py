@@ -13,6 +13,8 @@ momentum and loss scaling, with a scaler whose pending-overflow flag is set
 change).  The train step with fuse_update must follow the unfused step's
 trajectory bit for bit, forced overflows included.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -178,7 +180,7 @@ def _fused_ranges(cfg):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("case", ["scaled_with_overflows", "input_beyond_fp16", "full_size"])
+@pytest.mark.parametrize("case", ["scaled_with_overflows", "input_beyond_fp16", "bf16_unscaled", "full_size"])
 def test_train_step_fused_matches_unfused(mdnn, case):
     """fuse_update changes where the update of the hidden layers' weights
     runs, not what it computes: the trajectories agree bit for bit (loss,
@@ -187,12 +189,16 @@ def test_train_step_fused_matches_unfused(mdnn, case):
     scaled gradients overflow in fp16 until the scale has halved enough) and
     the applied steps after them, through an input value that overflows
     fp16 when the batch is stored (only the input cast can see it before the
-    first layer's fused product runs), and at the benchmark's full size."""
+    first layer's fused product runs), with bf16 storage and no loss scaling
+    (the only way bf16 nets fuse), and at the benchmark's full size."""
     import torch
     if case == "full_size":
         cfg, steps = W.wide_mlp_fp16(), 4
     elif case == "input_beyond_fp16":
         cfg, steps = W.wide_mlp_fp16(batch=512, width=2048), 3
+    elif case == "bf16_unscaled":   # bf16 storage fuses only without loss scaling
+        cfg, steps = dataclasses.replace(W.wide_mlp_fp16(batch=512, width=2048), dtype="bf16",
+                                         loss_scaling=False), 3
     else:
         cfg, steps = W.wide_mlp_fp16(batch=512, width=2048, init_scale=2.0 ** 40), 30
     fr = _fused_ranges(cfg)
@@ -208,9 +214,12 @@ def test_train_step_fused_matches_unfused(mdnn, case):
         lb = fused.step(X, T)
         assert torch.equal(la.view(torch.int32), lb.view(torch.int32)), f"step {s}"   # bitwise (NaN included)
         _same_state(mdnn, plain, fused, fr)
+        if fused.scaler is None:
+            continue
         skipped += mdnn.read_scaler(fused.scaler)["overflow"]
         if case == "input_beyond_fp16":
             assert mdnn.read_scaler(fused.scaler)["overflow"] == (1 if s == 1 else 0), f"step {s}"
-    if case != "full_size":
+    if case in ("scaled_with_overflows", "input_beyond_fp16"):
         assert skipped >= 1, "the case is meant to skip updates"
-    assert mdnn.read_scaler(fused.scaler)["good_steps"] >= 1
+    if fused.scaler is not None:
+        assert mdnn.read_scaler(fused.scaler)["good_steps"] >= 1
