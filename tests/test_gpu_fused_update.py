@@ -94,6 +94,23 @@ def test_fused_update_equals_product_then_update(mdnn, shape, mode):
         assert torch.equal(sc_f, _scaler(mdnn, 1024.0, reserved=1 if mode == "skipped" else 0))
 
 
+def test_fused_update_without_working_copy(mdnn):
+    """w_lp NULL (no working copy), plain SGD with a loss scaler: the same
+    weights as the product stored and mdnn_sgd_update without a copy."""
+    import torch
+    m, n, k = 1024, 4096, 2048
+    A, B = _operands(m, n, k, "f16", 9)
+    w, _, _ = _params(m, n, 15, "f16")
+    g = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    mdnn.mdnn_gemm_mixed(2, m, n, k, 1.0, A, A.stride(0), B, B.stride(0), DT["f16"], 0.0, None, 0, g, n, DT["f32"])
+    rw = w.clone()
+    mdnn.mdnn_sgd_update(m * n, rw, g, None, None, DT["f16"], 0.03, 0.0, _scaler(mdnn, 512.0))
+    mdnn.mdnn_gemm_tn_update(m, n, k, A, A.stride(0), B, B.stride(0), DT["f16"], w, None, None, n, 0.03, 0.0,
+                             _scaler(mdnn, 512.0))
+    torch.cuda.synchronize()
+    assert torch.equal(w, rw)
+
+
 def test_fused_update_padded_rows(mdnn):
     """ldw > N: the columns past N are never touched."""
     import torch
