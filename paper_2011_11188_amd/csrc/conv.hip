@@ -90,7 +90,7 @@ static SplitPlan filter_plan(const ConvGeom& g) {
 
 template <class T>
 static mdnn_status_t bwd_filter_impl(const ConvGeom& g, const void* x, const void* dy, float* dw,
-                                     void* ws, hipStream_t st) {
+                                     void* ws, hipStream_t st, ReduceBatch* defer) {
   typedef typename T::storage S;
   const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
   const bool vdy = aligned(dy, 16) && g.k % 8 == 0;
@@ -104,7 +104,7 @@ static mdnn_status_t bwd_filter_impl(const ConvGeom& g, const void* x, const voi
     ep.k_per_split = p.k_per_split;
   }
   MDNN_TRY((conv_run<T, F32>(a, b, M, N, K, ep, p.splits, st)));
-  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st);
+  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st, defer);
   return MDNN_SUCCESS;
 }
 
@@ -248,10 +248,9 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter_noalloc(const mdnn_conv_shape_t*
   return mdnn_conv2d_bwd_filter(shape, x, dy, io_type, dw, db, ws, need, stream);
 }
 
-extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x,
-                                                const void* dy, mdnn_dtype_t io_type, float* dw,
-                                                float* db, void* workspace, size_t ws_bytes,
-                                                mdnn_stream_t stream) {
+mdnn_status_t mdnn::conv2d_bwd_filter_deferred(const mdnn_conv_shape_t* shape, const void* x, const void* dy,
+                                               mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
+                                               size_t ws_bytes, hipStream_t st, ReduceBatch* defer) {
   ConvGeom g;
   MDNN_TRY(check_conv_shape(shape, g));
   if (!dtype_ok(io_type)) return fail(MDNN_ERR_DTYPE, "conv bwd_filter: unknown io_type");
@@ -265,7 +264,6 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
     return fail(MDNN_ERR_WORKSPACE, "conv bwd_filter: needs %zu bytes of 256-byte aligned workspace",
                 need);
   clear_error();
-  hipStream_t st = as_stream(stream);
   if (g.n == 0) {
     // empty batch: zero gradients
     MDNN_TRY(fill_zero(dw, (size_t)g.k * g.r * g.s * g.c * 4, st));
@@ -273,22 +271,34 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, 
   }
   bool done = false;
   if (pipe_allowed() && conv_small_filter_blocks(g, io_type) > 0) {
-    MDNN_TRY(conv_small_filter(g, x, dy, dw, workspace, io_type, st));
+    MDNN_TRY(conv_small_filter(g, x, dy, dw, workspace, io_type, st, defer));
     done = true;
   }
-  if (!done && pipe_allowed()) MDNN_TRY(conv_pipe_bwd_filter(g, x, dy, dw, workspace, io_type, st, &done));
+  if (!done && pipe_allowed())
+    MDNN_TRY(conv_pipe_bwd_filter(g, x, dy, dw, workspace, io_type, st, &done, defer));
   if (!done) {
     switch (io_type) {
-      case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st)); break;
-      case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st)); break;
-      default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st)); break;
+      case MDNN_F16: MDNN_TRY(bwd_filter_impl<F16>(g, x, dy, dw, workspace, st, defer)); break;
+      case MDNN_BF16: MDNN_TRY(bwd_filter_impl<BF16>(g, x, dy, dw, workspace, st, defer)); break;
+      default: MDNN_TRY(bwd_filter_impl<F32>(g, x, dy, dw, workspace, st, defer)); break;
     }
   }
   if (db) {
     const size_t off = filter_ws_split_bytes(g);
     const size_t cs = column_sums_ws_bytes((int64_t)g.n * g.ho * g.wo, g.k);
     return column_sums(dy, nullptr, io_type, (int64_t)g.n * g.ho * g.wo, g.k, db,
-                       cs ? (char*)workspace + off : nullptr, cs, st);
+                       cs ? (char*)workspace + off : nullptr, cs, st, defer);
   }
   return MDNN_SUCCESS;
+}
+
+extern "C" mdnn_status_t mdnn_conv2d_bwd_filter(const mdnn_conv_shape_t* shape, const void* x,
+                                                const void* dy, mdnn_dtype_t io_type, float* dw,
+                                                float* db, void* workspace, size_t ws_bytes,
+                                                mdnn_stream_t stream) {
+  // the weight and bias sums' second passes in one launch
+  hipStream_t st = as_stream(stream);
+  ReduceBatch batch{};
+  MDNN_TRY(conv2d_bwd_filter_deferred(shape, x, dy, io_type, dw, db, workspace, ws_bytes, st, &batch));
+  return reduce_batch_launch(batch, st);
 }

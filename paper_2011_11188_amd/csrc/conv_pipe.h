@@ -29,8 +29,9 @@ mdnn_status_t conv_pipe_bwd_data(const ConvGeom& g, const void* dy, const void* 
 SplitPlan conv_pipe_filter_plan(const ConvGeom& g);
 
 // Backward filter into fp32 dw[c_out][r*s*c_in]; split partials go to `ws`
-// (conv_pipe_filter_plan(g).splits * M * N floats when splits > 1).
+// (conv_pipe_filter_plan(g).splits * M * N floats when splits > 1), their
+// sum into `defer` when one is given.
 mdnn_status_t conv_pipe_bwd_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
-                                   mdnn_dtype_t io, hipStream_t st, bool* done);
+                                   mdnn_dtype_t io, hipStream_t st, bool* done, ReduceBatch* defer = nullptr);
 
 }  // namespace mdnn

@@ -170,7 +170,7 @@ namespace {
 
 template <class T, class TL>
 mdnn_status_t filter_run(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws, const SplitPlan& p,
-                         hipStream_t st) {
+                         hipStream_t st, ReduceBatch* defer) {
   const int64_t M = g.k, N = (int64_t)g.r * g.s * g.c, K = (int64_t)g.n * g.ho * g.wo;
   const lds::MatArgs a{dy, g.k, g.k};
   const lds::ConvColsArgs b{x, (uint32_t)((int64_t)g.n * g.h * g.w * g.c * 2), g.h, g.w, g.c, g.s, g.pad,
@@ -188,24 +188,24 @@ mdnn_status_t filter_run(const ConvGeom& g, const void* x, const void* dy, float
   }
   MDNN_TRY((run_pipe<T, F32, TL, FILTER_STAGES, lds::MatLoader<false, TL::BM, TL::LA>,
                      lds::ConvColsLoader<TL::BN, TL::LB>>(a, b, M, N, K, ep, p.splits, st)));
-  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st);
+  if (p.splits > 1) return reduce_splits((const float*)ws, p.splits, M, N, dw, st, defer);
   return MDNN_SUCCESS;
 }
 
 }  // namespace
 
 mdnn_status_t conv_pipe_bwd_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
-                                   mdnn_dtype_t io, hipStream_t st, bool* done) {
+                                   mdnn_dtype_t io, hipStream_t st, bool* done, ReduceBatch* defer) {
   *done = false;
   const SplitPlan p = conv_pipe_filter_plan(g);
   if (io == MDNN_F32 || p.splits == 0 || !aligned(x, 16) || !aligned(dy, 16)) return MDNN_SUCCESS;
   if (p.splits > 1 && (!ws || !aligned(ws, 16))) return MDNN_SUCCESS;
   if (g.k <= 64)
-    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileFiltN>(g, x, dy, dw, ws, p, st)
-                             : filter_run<BF16, TileFiltN>(g, x, dy, dw, ws, p, st)));
+    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileFiltN>(g, x, dy, dw, ws, p, st, defer)
+                             : filter_run<BF16, TileFiltN>(g, x, dy, dw, ws, p, st, defer)));
   else
-    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileFiltS>(g, x, dy, dw, ws, p, st)
-                             : filter_run<BF16, TileFiltS>(g, x, dy, dw, ws, p, st)));
+    MDNN_TRY((io == MDNN_F16 ? filter_run<F16, TileFiltS>(g, x, dy, dw, ws, p, st, defer)
+                             : filter_run<BF16, TileFiltS>(g, x, dy, dw, ws, p, st, defer)));
   *done = true;
   return MDNN_SUCCESS;
 }

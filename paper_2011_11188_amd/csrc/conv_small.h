@@ -19,8 +19,9 @@ mdnn_status_t conv_small_fwd(const ConvGeom& g, const void* x, const void* w, co
 // of pixel blocks (the partials it writes:
 // blocks * c_out * r*s*c_in floats), or 0 when the shape does not qualify.
 int64_t conv_small_filter_blocks(const ConvGeom& g, mdnn_dtype_t io);
-// dw = sum over pixel blocks of the partials in ws (fixed order).
+// dw = sum over pixel blocks of the partials in ws (fixed order; the sum
+// goes into `defer` when one is given).
 mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
-                                mdnn_dtype_t io, hipStream_t st);
+                                mdnn_dtype_t io, hipStream_t st, ReduceBatch* defer = nullptr);
 
 }  // namespace mdnn

@@ -608,7 +608,7 @@ static void small_filter_launch(const ConvGeom& g, const void* x, const void* dy
 }
 
 mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy, float* dw, void* ws,
-                                mdnn_dtype_t io, hipStream_t st) {
+                                mdnn_dtype_t io, hipStream_t st, ReduceBatch* defer) {
   const int64_t blocks = conv_small_filter_blocks(g, io);
   const int64_t P = (int64_t)g.n * g.ho * g.wo;
   if (blocks <= 0 || blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "conv: filter gradient shape");
@@ -621,13 +621,13 @@ mdnn_status_t conv_small_filter(const ConvGeom& g, const void* x, const void* dy
       hipLaunchKernelGGL(conv_small_filter_mfma_kernel<BF16>, dim3((unsigned)blocks), dim3(256), 0, st,
                          (const uint16_t*)x, (const uint16_t*)dy, g, P, part);
     MDNN_TRY(check_launch("conv_small_filter_mfma_kernel"));
-    return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st);
+    return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st, defer);
   }
   if (io == MDNN_F16) small_filter_launch<F16>(g, x, dy, P, blocks, part, st);
   else if (io == MDNN_BF16) small_filter_launch<BF16>(g, x, dy, P, blocks, part, st);
   else small_filter_launch<F32>(g, x, dy, P, blocks, part, st);
   MDNN_TRY(check_launch("conv_small_filter_kernel"));
-  return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st);
+  return reduce_splits(part, (int)blocks, g.k, (int64_t)g.r * g.s * g.c, dw, st, defer);
 }
 
 }  // namespace mdnn

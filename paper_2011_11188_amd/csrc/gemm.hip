@@ -37,14 +37,14 @@ __global__ void reduce_splits_kernel(const float* __restrict__ part, int splits,
 // G = 1024 / OPB split groups.  Thread (g, j) sums splits g, g+G, g+2G, ...
 // of output j into four interleaved accumulators (four loads in flight),
 // adds them in order, and the G group sums are combined by a fixed tree in
-// LDS: a fixed order, so the result is deterministic.
+// LDS: a fixed order, so the result is deterministic.  `red` holds 1024
+// floats; `blk` is the block's index within its reduction.
 template <int OPB>
-__global__ void __launch_bounds__(1024)
-reduce_splits_wide_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ out) {
+__device__ __forceinline__ void reduce_wide_block(const float* __restrict__ part, int splits, int64_t n,
+                                                  float* __restrict__ out, int64_t blk, float* red) {
   constexpr int G = 1024 / OPB;
-  __shared__ float red[G][OPB];
   const int j = threadIdx.x % OPB, g = threadIdx.x / OPB;
-  const int64_t e = (int64_t)blockIdx.x * OPB + j;
+  const int64_t e = blk * OPB + j;
   float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
   if (e < n) {
     int k = g;
@@ -56,20 +56,66 @@ reduce_splits_wide_kernel(const float* __restrict__ part, int splits, int64_t n,
     }
     for (; k < splits; k += G) s0 += part[(int64_t)k * n + e];
   }
-  red[g][j] = (s0 + s1) + (s2 + s3);
+  red[g * OPB + j] = (s0 + s1) + (s2 + s3);
   __syncthreads();
 #pragma unroll
   for (int h = G / 2; h > 0; h >>= 1) {
-    if (g < h) red[g][j] += red[g + h][j];
+    if (g < h) red[g * OPB + j] += red[(g + h) * OPB + j];
     __syncthreads();
   }
-  if (g == 0 && e < n) out[e] = red[0][j];
+  if (g == 0 && e < n) out[e] = red[j];
 }
 
-static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream) {
-  if (n <= 16)
+template <int OPB>
+__global__ void __launch_bounds__(1024)
+reduce_splits_wide_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ out) {
+  __shared__ float red[1024];
+  reduce_wide_block<OPB>(part, splits, n, out, blockIdx.x, red);
+}
+
+// Several wide reductions in one launch: block b works on the reduction s
+// with first_block[s] <= b < first_block[s + 1], with that reduction's
+// outputs per block -- the same sums, in the same order, as its own launch.
+__global__ void __launch_bounds__(1024) reduce_batch_kernel(ReduceBatch b) {
+  __shared__ float red[1024];
+  int s = 0;
+  while (s + 1 < b.n && (int64_t)blockIdx.x >= b.first_block[s + 1]) ++s;
+  const int64_t blk = (int64_t)blockIdx.x - b.first_block[s];
+  switch (b.opb[s]) {
+    case 16: reduce_wide_block<16>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
+    case 32: reduce_wide_block<32>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
+    default: reduce_wide_block<64>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
+  }
+}
+
+mdnn_status_t reduce_batch_launch(ReduceBatch& b, hipStream_t stream) {
+  if (b.n == 0) return MDNN_SUCCESS;
+  const ReduceBatch todo = b;
+  b.n = 0;
+  const int64_t blocks = todo.first_block[todo.n];
+  if (blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "split reductions: too many blocks");
+  hipLaunchKernelGGL(reduce_batch_kernel, dim3((unsigned)blocks), dim3(1024), 0, stream, todo);
+  return check_launch("reduce_batch_kernel");
+}
+
+static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream,
+                                 ReduceBatch* defer) {
+  const int opb = n <= 16 ? 16 : n <= 32 ? 32 : 64;
+  if (defer) {
+    if (defer->n == kMaxReduceBatch) MDNN_TRY(reduce_batch_launch(*defer, stream));
+    const int s = defer->n++;
+    if (s == 0) defer->first_block[0] = 0;
+    defer->part[s] = partial;
+    defer->out[s] = out;
+    defer->elems[s] = n;
+    defer->splits[s] = splits;
+    defer->opb[s] = opb;
+    defer->first_block[s + 1] = defer->first_block[s] + ceil_div(n, (int64_t)opb);
+    return MDNN_SUCCESS;
+  }
+  if (opb == 16)
     hipLaunchKernelGGL(reduce_splits_wide_kernel<16>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
-  else if (n <= 32)
+  else if (opb == 32)
     hipLaunchKernelGGL(reduce_splits_wide_kernel<32>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
   else
     hipLaunchKernelGGL(reduce_splits_wide_kernel<64>, dim3((unsigned)ceil_div(n, 64)), dim3(1024), 0, stream,
@@ -78,10 +124,10 @@ static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, fl
 }
 
 mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int64_t cols,
-                            float* out, hipStream_t stream) {
+                            float* out, hipStream_t stream, ReduceBatch* defer) {
   const int64_t n = rows * cols;
   if (n == 0) return MDNN_SUCCESS;
-  if (splits >= 32 && n <= ((int64_t)1 << 18)) return reduce_wide(partial, splits, n, out, stream);
+  if (splits >= 32 && n <= ((int64_t)1 << 18)) return reduce_wide(partial, splits, n, out, stream, defer);
   const int64_t blocks = ceil_div(ceil_div(n, 4), 256);
   hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, partial,
                      splits, n, out);
@@ -323,36 +369,41 @@ size_t column_sums_ws_bytes(int64_t rows, int64_t cols) {
 }
 
 template <class T>
-static void colsum_launch(const void* x, const void* y, int64_t rows, int64_t cols, float* out,
-                          void* ws, size_t ws_bytes, hipStream_t st) {
+static mdnn_status_t colsum_launch(const void* x, const void* y, int64_t rows, int64_t cols, float* out,
+                                   void* ws, size_t ws_bytes, hipStream_t st, ReduceBatch* defer) {
   typedef typename T::storage S;
   const size_t need = column_sums_ws_bytes(rows, cols);
-  if (need > 0 && ws && ws_bytes >= need && aligned(ws, 4)) {
+  const bool vec = aligned(x, 16) && (!y || aligned(y, 16)) && cols % 8 == 0;
+  if (rows <= COLSUM_ROWS) {
+    // one chunk: pass 1 alone gives the sums (its 16-byte row reads keep
+    // more loads in flight than the single-pass kernel)
+    hipLaunchKernelGGL(colsum_partial_kernel<T>, dim3((unsigned)ceil_div(cols, 64), 1u), dim3(256), 0, st,
+                       (const S*)x, (const S*)y, rows, cols, vec, out);
+  } else if (need > 0 && ws && ws_bytes >= need && aligned(ws, 4)) {
     const int64_t chunks = ceil_div(rows, COLSUM_ROWS);
-    const bool vec = aligned(x, 16) && (!y || aligned(y, 16)) && cols % 8 == 0;
     hipLaunchKernelGGL(colsum_partial_kernel<T>, dim3((unsigned)ceil_div(cols, 64), (unsigned)chunks), dim3(256),
                        0, st, (const S*)x, (const S*)y, rows, cols, vec, (float*)ws);
+    MDNN_TRY(check_launch("column sums (partials)"));
     if (chunks >= 32 && cols <= ((int64_t)1 << 18))
-      (void)reduce_wide((const float*)ws, (int)chunks, cols, out, st);
-    else
-      hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
-                         (const float*)ws, chunks, cols, out);
+      return reduce_wide((const float*)ws, (int)chunks, cols, out, st, defer);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
+                       (const float*)ws, chunks, cols, out);
   } else {
     hipLaunchKernelGGL(colsum_single_kernel<T>, dim3((unsigned)ceil_div(cols, 32)), dim3(256), 0, st,
                        (const S*)x, (const S*)y, rows, cols, out);
   }
+  return check_launch("column sums");
 }
 
 mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
-                          float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                          float* out, void* ws, size_t ws_bytes, hipStream_t stream, ReduceBatch* defer) {
   if (cols == 0) return MDNN_SUCCESS;
   if (ceil_div(rows, COLSUM_ROWS) > 65535) ws = nullptr;  // grid limit: single pass
   switch (t) {
-    case MDNN_F32: colsum_launch<F32>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
-    case MDNN_F16: colsum_launch<F16>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
-    default: colsum_launch<BF16>(x, y, rows, cols, out, ws, ws_bytes, stream); break;
+    case MDNN_F32: return colsum_launch<F32>(x, y, rows, cols, out, ws, ws_bytes, stream, defer);
+    case MDNN_F16: return colsum_launch<F16>(x, y, rows, cols, out, ws, ws_bytes, stream, defer);
+    default: return colsum_launch<BF16>(x, y, rows, cols, out, ws, ws_bytes, stream, defer);
   }
-  return check_launch("column sums");
 }
 
 int64_t column_sums_chunks(int64_t rows, int64_t cols, mdnn_dtype_t t) {

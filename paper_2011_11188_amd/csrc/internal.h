@@ -33,10 +33,36 @@ struct SplitPlan {
   int64_t k_per_split;
 };
 
+// Second passes of several split reductions, gathered for one launch.
+// reduce_splits() and column_sums() given a batch append their second pass
+// to it (when it is the many-splits reduction; other second passes launch
+// at once) instead of launching it: the same sums in the same order, done
+// when the caller launches the batch with reduce_batch_launch(), which must
+// come after the partials are written and before their memory is reused.
+// A full batch is launched by the call that would overflow it.
+constexpr int kMaxReduceBatch = 8;
+struct ReduceBatch {
+  int n;
+  const float* part[kMaxReduceBatch];
+  float* out[kMaxReduceBatch];
+  int64_t elems[kMaxReduceBatch];
+  int splits[kMaxReduceBatch];
+  int opb[kMaxReduceBatch];  // outputs per block: 16, 32 or 64
+  int64_t first_block[kMaxReduceBatch + 1];
+};
+mdnn_status_t reduce_batch_launch(ReduceBatch& b, hipStream_t stream);
+
 // Sum `splits` fp32 [rows, cols] partial matrices in split order into
 // out[rows, cols] (fp32).
 mdnn_status_t reduce_splits(const float* partial, int splits, int64_t rows, int64_t cols,
-                            float* out, hipStream_t stream);
+                            float* out, hipStream_t stream, ReduceBatch* defer = nullptr);
+// mdnn_conv2d_bwd_filter with the second passes of its weight and bias
+// sums appended to `defer` (the entry point launches them at once; a caller
+// that keeps each layer's workspace apart can launch several layers' sums
+// together).
+mdnn_status_t conv2d_bwd_filter_deferred(const mdnn_conv_shape_t* shape, const void* x, const void* dy,
+                                         mdnn_dtype_t io_type, float* dw, float* db, void* workspace,
+                                         size_t ws_bytes, hipStream_t stream, ReduceBatch* defer);
 // Zero `bytes` (a multiple of 4) with a fill kernel (no memset nodes, so the
 // caller may capture the stream into a graph).
 mdnn_status_t fill_zero(void* p, size_t bytes, hipStream_t stream);
@@ -53,7 +79,8 @@ mdnn_status_t cast_f32_checked(int64_t n, const float* src, void* dst, mdnn_dtyp
 // given, a single (slower) pass otherwise.
 size_t column_sums_ws_bytes(int64_t rows, int64_t cols);
 mdnn_status_t column_sums(const void* x, const void* y, mdnn_dtype_t t, int64_t rows, int64_t cols,
-                          float* out, void* ws, size_t ws_bytes, hipStream_t stream);
+                          float* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                          ReduceBatch* defer = nullptr);
 // The two passes apart, for a caller that finishes several matrices' sums in
 // one launch: pass 1 writes partial[column_sums_chunks(rows, cols, t)][cols]
 // (fp32, 8-byte aligned; 16-bit rows whose width is a multiple of 512 are

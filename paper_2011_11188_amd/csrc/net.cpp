@@ -31,6 +31,7 @@ struct LayerPlan {
   size_t out_off = 0;                 // act[i+1]
   size_t arg_off = 0;                 // pool argmax
   size_t cs_off = 0;                  // FC: bias-gradient partial column sums
+  size_t cws_off = 0, cws_bytes = 0;  // conv: the filter gradient's own workspace
   bool input_relu = false;            // input produced by a ReLU (directly or through pooling)
   bool last = false;
   // fuse_update: this FC layer's weights are updated inside its weight-gradient
@@ -189,9 +190,12 @@ extern "C" mdnn_status_t mdnn_net_create(const mdnn_layer_t* layers, int32_t n_l
       w = align256(w + (size_t)batch * p.out_feat);
     }
     if (p.L.kind == MDNN_LAYER_CONV) {
+      // a region per layer: its partial sums stay until the backward pass
+      // ends, when all layers' sums are finished in one launch
       mdnn_conv_shape_t cs = conv_shape(p.L, batch);
-      size_t need = mdnn_conv2d_bwd_filter_workspace(&cs, net->lp);
-      if (need > fws) fws = need;
+      p.cws_off = w;
+      p.cws_bytes = mdnn_conv2d_bwd_filter_workspace(&cs, net->lp);
+      w = align256(w + p.cws_bytes);
     }
     if (p.L.kind == MDNN_LAYER_FC) {
       const int64_t in = p.L.c_in, o = p.L.c_out;
@@ -418,6 +422,9 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
   // fused layers' output gradients stay in their own buffers: their partial
   // sums go in one batched launch after the loop
   StripBatch strips{};
+  // convolution layers' weight and bias sums: second passes in one launch
+  // after the loop
+  ReduceBatch conv_sums{};
   for (size_t ii = net->layers.size(); ii-- > 0;) {
     const LayerPlan& p = net->layers[ii];
     const char* a_in = act_ptr(ii);
@@ -470,8 +477,8 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
       }
     } else if (p.L.kind == MDNN_LAYER_CONV) {
       mdnn_conv_shape_t cs = conv_shape(p.L, B);
-      MDNN_TRY(mdnn_conv2d_bwd_filter(&cs, a_in, gcur, lp, gw, gb, ws + net->fws_off, net->fws_bytes,
-                                      stream));
+      MDNN_TRY(conv2d_bwd_filter_deferred(&cs, a_in, gcur, lp, gw, gb, ws + p.cws_off, p.cws_bytes,
+                                          as_stream(stream), &conv_sums));
       if (ii > 0)
         MDNN_TRY(mdnn_conv2d_bwd_data(&cs, gcur, wptr(p), lp, mask, gnxt, lp, stream));
     } else {
@@ -480,6 +487,7 @@ static mdnn_status_t run_step(mdnn_net_t* net, const float* x, const void* targe
     }
   }
 
+  MDNN_TRY(reduce_batch_launch(conv_sums, as_stream(stream)));
   MDNN_TRY(column_sums_partial_batch(strips, lp, B, as_stream(stream)));
   MDNN_TRY(column_sums_final(bias_sums, nonfinite, as_stream(stream)));
   if (fused) {

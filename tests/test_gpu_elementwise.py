@@ -104,6 +104,29 @@ def test_column_sums_tall_and_wide(mdnn, shape):
     assert torch.equal(db, db2)
 
 
+@pytest.mark.parametrize("shape,dt", [((256, 1024), "bf16"), ((37, 72), "f16"), ((200, 77), "f32"), ((1, 8), "bf16"),
+                                      ((256, 10), "f16")])
+def test_column_sums_short(mdnn, shape, dt):
+    """At most 256 rows (a classifier's hidden layer at batch 256): one pass,
+    masked by a ReLU output and unmasked, against the exact sums."""
+    import torch
+    rows, cols = shape
+    dy = W.normal((rows, cols), 31, 1, dt)
+    yv = W.normal((rows, cols), 31, 2, dt)
+    DY, Y = dev(dy, dt), dev(yv, dt)
+    db = torch.empty(cols, dtype=torch.float32, device="cuda")
+    dbm = torch.empty(cols, dtype=torch.float32, device="cuda")
+    dbm2 = torch.empty(cols, dtype=torch.float32, device="cuda")
+    mdnn.mdnn_bias_act_bwd(rows, cols, DY, None, mdnn.ACT_NONE, None, db, DT[dt])
+    mdnn.mdnn_bias_act_bwd(rows, cols, DY, Y, mdnn.ACT_RELU, None, dbm, DT[dt])
+    mdnn.mdnn_bias_act_bwd(rows, cols, DY, Y, mdnn.ACT_RELU, None, dbm2, DT[dt])
+    torch.cuda.synchronize()
+    d64, y64 = decode(dy, dt), decode(yv, dt)
+    assert norm_max_err(host64(db), d64.sum(axis=0)) <= 1e-5
+    assert norm_max_err(host64(dbm), np.where(y64 > 0, d64, 0.0).sum(axis=0)) <= 1e-5
+    assert torch.equal(dbm, dbm2)
+
+
 # c = 12: element-wise kernels; c = 16 and 64 (16-bit types): eight channels
 # per thread with 16-byte accesses
 @pytest.mark.parametrize("c", [12, 16, 64])
