@@ -73,6 +73,22 @@ def test_lenet_bf16_ten_steps(mdnn):
     assert norm_max_err(w, orc.w32) <= 1e-3
 
 
+def test_deep_conv_net_ten_steps(mdnn):
+    """Six 3x3 convolution layers (batch 32, 16x16, 8 channels; every layer's
+    weight and bias sums take the many-splits second pass, more of them than
+    one batched launch holds) and a classifier: losses and master weights
+    against the oracle."""
+    convs = [W.Layer(W.CONV, 1 if i == 0 else 8, 16, 16, 8, 3, 3, 1, W.ACT_RELU) for i in range(6)]
+    cfg = W.TrainConfig(name="deep_conv_bf16_b32", base_seed=1188 + 41,
+                        layers=tuple(convs) + (W.Layer(W.FC, 16 * 16 * 8, c_out=10),),
+                        batch=32, in_features=256, dtype="bf16", loss=W.LOSS_XENT, lr=0.01)
+    gl, net = _trajectory(mdnn, cfg, 10)
+    ol, orc = _oracle_trajectory(cfg, 10)
+    _check(gl, ol)
+    w = net.master.cpu().numpy().astype(np.float64)
+    assert norm_max_err(w, orc.w32) <= 1e-3
+
+
 @pytest.mark.timeout(300)
 def test_wide_mlp_fp16_reduced_ten_steps(mdnn):
     cfg = W.wide_mlp_fp16(batch=512, width=1024)
