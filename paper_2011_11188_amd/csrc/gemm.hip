@@ -88,10 +88,14 @@ __global__ void __launch_bounds__(1024) reduce_batch_kernel(ReduceBatch b) {
   }
 }
 
+static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream,
+                                 ReduceBatch* defer);
+
 mdnn_status_t reduce_batch_launch(ReduceBatch& b, hipStream_t stream) {
   if (b.n == 0) return MDNN_SUCCESS;
   const ReduceBatch todo = b;
   b.n = 0;
+  if (todo.n == 1) return reduce_wide(todo.part[0], todo.splits[0], todo.elems[0], todo.out[0], stream, nullptr);
   const int64_t blocks = todo.first_block[todo.n];
   if (blocks > 0x7fffffffLL) return fail(MDNN_ERR_SHAPE, "split reductions: too many blocks");
   hipLaunchKernelGGL(reduce_batch_kernel, dim3((unsigned)blocks), dim3(1024), 0, stream, todo);

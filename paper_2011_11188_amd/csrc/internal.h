@@ -39,7 +39,8 @@ struct SplitPlan {
 // at once) instead of launching it: the same sums in the same order, done
 // when the caller launches the batch with reduce_batch_launch(), which must
 // come after the partials are written and before their memory is reused.
-// A full batch is launched by the call that would overflow it.
+// A full batch is launched by the call that would overflow it; a batch of
+// one runs as that reduction's own launch.
 constexpr int kMaxReduceBatch = 8;
 struct ReduceBatch {
   int n;
