@@ -34,8 +34,8 @@ static bool pipe_allowed() {
   const int o = gemm_tile_override();
   return !(o >= TILE_256x256 && o <= TILE_64x64);
 }
-// the halo kernel for the forward 3x3 layers it takes unless a kernel family
-// is forced (forcing the pipelined kernels runs the implicit GEMM there too)
+// the halo kernel for the 3x3 layers it takes unless a kernel family is
+// forced (forcing the pipelined kernels runs the implicit GEMM there too)
 static bool halo_allowed() { return gemm_tile_override() == TILE_AUTO; }
 
 static Epilogue plain_epilogue(void* D, int64_t ldd, mdnn_dtype_t d_type) {
@@ -138,7 +138,7 @@ extern "C" mdnn_status_t mdnn_conv2d_fwd(const mdnn_conv_shape_t* shape, const v
   if (pipe_allowed()) {
     if (conv_small_fwd_ok(g)) return conv_small_fwd(g, x, w, ep, io_type, y_type, st);
     bool done = false;
-    if (halo_allowed()) MDNN_TRY(conv_halo_fwd(g, x, w, ep, io_type, y_type, st, &done));
+    if (halo_allowed()) MDNN_TRY(conv_halo(g, false, x, w, ep, io_type, y_type, st, &done));
     if (done) return MDNN_SUCCESS;
     MDNN_TRY(conv_pipe_fwd(g, x, w, ep, io_type, y_type, st, &done));
     if (done) return MDNN_SUCCESS;
@@ -172,6 +172,8 @@ extern "C" mdnn_status_t mdnn_conv2d_bwd_data(const mdnn_conv_shape_t* shape, co
   hipStream_t st = as_stream(stream);
   if (pipe_allowed()) {
     bool done = false;
+    if (halo_allowed()) MDNN_TRY(conv_halo(g, true, dy, w, ep, io_type, dx_type, st, &done));
+    if (done) return MDNN_SUCCESS;
     MDNN_TRY(conv_pipe_bwd_data(g, dy, w, ep, io_type, dx_type, st, &done));
     if (done) return MDNN_SUCCESS;
   }

@@ -1,5 +1,7 @@
-// Forward 3x3 convolutions of 64 input channels (section 2.1's convolution
-// layers; stride 1, padding 1) with the input tile's halo in LDS.
+// 3x3 convolutions of 64 input channels (section 2.1's convolution layers;
+// stride 1, padding 1) with the input tile's halo in LDS: the forward pass,
+// and backward data as the convolution of dy with the filter flipped in
+// both spatial axes and its channel axes swapped (padding 3 - 1 - 1 = 1).
 //
 // A workgroup (4 waves) computes 256 consecutive output pixels (whole image
 // rows of one image, or whole images) x 64 output channels.  It stages the
@@ -11,17 +13,23 @@
 // tap's offset.  Each input pixel comes from L2 into the CU once per tile
 // instead of once per tap.
 //
-// LDS rows (a pixel's 64 channels, or a filter row's 64 input channels) are
-// 128 bytes; their eight 16-byte chunks are stored at chunk ^ (row & 7), so
-// the 16-byte fragment reads of eight consecutive rows touch distinct banks.
+// LDS rows (a pixel's 64 channels, or a forward filter row's 64 input
+// channels) are 128 bytes; their eight 16-byte chunks are stored at
+// chunk ^ (row & 7), so the 16-byte fragment reads of eight consecutive rows
+// touch distinct banks.  Backward data reads the filter with output channels
+// contiguous (w[k][r][s][c] over c), so its stage keeps rows of output
+// channels in the pipelined GEMM's layout for such operands and forms the B
+// fragments with its transposing reads (lds::fragment).
 //
-// Measured against the implicit GEMM's pipelined kernel (fp16, batch 128,
-// fp16 output): 64 -> 64 channels at 32x32, 16.7 against 18.2 us.  Not
-// taken: 128 and 256 input channels (two and four staged chunks: 18.8 vs
-// 15.1 us at 16x16, 32.1 vs 16.2 us at 8x8), 512-pixel tiles (one
-// workgroup per CU: 20.5 us at 32x32) and backward data (the filter
-// transposed through LDS: 22.1 vs 18.6 us at 32x32).
+// Measured against the implicit GEMM's pipelined kernels (fp16, batch 128,
+// fp16 output): 64 -> 64 channels at 32x32, forward 16.7 against 18.2 us.
+// Not taken: 128 and 256 input channels (two and four staged chunks: 18.8
+// vs 15.1 us at 16x16, 32.1 vs 16.2 us at 8x8; the staging is not
+// overlapped with the products), 512-pixel tiles (one workgroup per CU:
+// 20.5 us at 32x32).
 #include "conv_halo.h"
+
+#include "gemm_lds.h"
 
 namespace mdnn {
 
@@ -37,8 +45,8 @@ constexpr int FILT_PER = WSTAGE / 8 / HT;
 static_assert((WSTAGE / 8) % HT == 0, "filter stage splits evenly");
 
 struct HaloArgs {
-  const uint16_t* x;  // [n][h][w][64]
-  const uint16_t* w;  // [cout][3][3][64]
+  const uint16_t* x;  // convolved tensor [n][h][w][64]: x (forward) or dy (backward data)
+  const uint16_t* w;  // forward [cout][3][3][64]; backward data [64][3][3][cout]
   int32_t h, w_img, cout;
   int32_t hr;         // image rows per tile (h when a tile holds whole images)
   int32_t halo_px;    // (TPX / (hr * w)) * (hr + 2) * (w + 2)
@@ -75,26 +83,46 @@ __device__ __forceinline__ void stage_halo(const HaloArgs& a, uint16_t* halo, in
   }
 }
 
-// filter row tr's three taps for output channels n0..n0 + 63: item (s, nl,
-// c8) is 8 input channels of output channel n0 + nl
+// filter row tr's three taps for output channels n0..n0 + 63.  Forward:
+// item (s, nl, c8) is 8 input channels of output channel n0 + nl, stored as
+// rows of input channels.  Backward data: item (s, kl, n8) is output
+// channels n0 + 8 n8 .. + 7 of input channel kl at the flipped tap
+// (2 - tr, 2 - s), stored as rows of output channels in the transposing
+// reads' layout (lds::mn_swz).
+template <bool BWD>
 __device__ __forceinline__ void load_filter(const HaloArgs& a, uint4 (&v)[FILT_PER], int tr, int64_t n0, int tid) {
 #pragma unroll
   for (int u = 0; u < FILT_PER; ++u) {
-    const int it = u * HT + tid, c8 = it & 7, nl = (it >> 3) % TCO, s = (it >> 3) / TCO;
-    v[u] = *(const uint4*)(a.w + ((n0 + nl) * 9 + tr * 3 + s) * HCH + c8 * 8);
+    const int it = u * HT + tid;
+    if constexpr (!BWD) {
+      const int c8 = it & 7, nl = (it >> 3) % TCO, s = (it >> 3) / TCO;
+      v[u] = *(const uint4*)(a.w + ((n0 + nl) * 9 + tr * 3 + s) * HCH + c8 * 8);
+    } else {
+      const int n8 = it & 7, kl = (it >> 3) % HCH, s = (it >> 3) / HCH;
+      v[u] = *(const uint4*)(a.w + ((int64_t)kl * 9 + (2 - tr) * 3 + (2 - s)) * a.cout + n0 + n8 * 8);
+    }
   }
 }
 
+template <bool BWD>
 __device__ __forceinline__ void store_filter(uint16_t* ws, const uint4 (&v)[FILT_PER], int tid) {
 #pragma unroll
   for (int u = 0; u < FILT_PER; ++u) {
-    const int it = u * HT + tid, c8 = it & 7, nl = (it >> 3) % TCO, s = (it >> 3) / TCO;
+    const int it = u * HT + tid;
+    int off;
+    if constexpr (!BWD) {
+      const int c8 = it & 7, nl = (it >> 3) % TCO, s = (it >> 3) / TCO;
+      off = s * TCO * HCH + swz(nl, c8);
+    } else {
+      const int n8 = it & 7, kl = (it >> 3) % HCH, s = (it >> 3) / HCH;
+      off = s * TCO * HCH + kl * TCO + (((n8 >> 1) ^ lds::mn_swz<TCO>(kl)) * 16) + (n8 & 1) * 8;
+    }
     // (component-wise: a whole-vector copy kept the array in scratch memory)
-    *(uint4*)(ws + s * TCO * HCH + swz(nl, c8)) = make_uint4(v[u].x, v[u].y, v[u].z, v[u].w);
+    *(uint4*)(ws + off) = make_uint4(v[u].x, v[u].y, v[u].z, v[u].w);
   }
 }
 
-template <class T, class OutT>
+template <class T, class OutT, bool BWD>
 __global__ void __launch_bounds__(HT) conv_halo_kernel(HaloArgs a, int64_t M, Epilogue ep) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[HALO_MAX_PX * HCH + WSTAGE];
   uint16_t* halo = lds;
@@ -117,6 +145,7 @@ __global__ void __launch_bounds__(HT) conv_halo_kernel(HaloArgs a, int64_t M, Ep
     hb[i] = (il * (a.hr + 2) + yl) * hw2 + xl;
   }
   const int kc = lane >> 4;
+  const lds::LaneFrag fb = lds::lane_frag<false, TCO>(lane);  // backward data's transposing reads
 
   float4_t acc[4][4];
 #pragma unroll
@@ -125,17 +154,17 @@ __global__ void __launch_bounds__(HT) conv_halo_kernel(HaloArgs a, int64_t M, Ep
     for (int j = 0; j < 4; ++j) acc[i][j] = (float4_t){0.f, 0.f, 0.f, 0.f};
 
   uint4 wpre[FILT_PER];
-  load_filter(a, wpre, 0, n0, tid);
+  load_filter<BWD>(a, wpre, 0, n0, tid);
 #pragma unroll 1
   for (int tr = 0; tr < 3; ++tr) {
     if (tr > 0) __syncthreads();  // every wave is done with the previous filter row
-    store_filter(wst, wpre, tid);
+    store_filter<BWD>(wst, wpre, tid);
     if (tr == 0) stage_halo(a, halo, img0, y0, tid);
     __syncthreads();
     // the next filter row's loads run under this row's products (after the
     // last row: a harmless reload of row 0, unconditional so the registers
     // stay registers)
-    load_filter(a, wpre, tr < 2 ? tr + 1 : 0, n0, tid);
+    load_filter<BWD>(a, wpre, tr < 2 ? tr + 1 : 0, n0, tid);
 #pragma unroll
     for (int s = 0; s < 3; ++s)
 #pragma unroll
@@ -145,7 +174,12 @@ __global__ void __launch_bounds__(HT) conv_halo_kernel(HaloArgs a, int64_t M, Ep
 #pragma unroll
         for (int i = 0; i < 4; ++i) af[i] = *(const uint4*)(halo + swz(hb[i] + tr * hw2 + s, c));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bf[j] = *(const uint4*)(wst + s * TCO * HCH + swz(j * 16 + (lane & 15), c));
+        for (int j = 0; j < 4; ++j) {
+          if constexpr (!BWD)
+            bf[j] = *(const uint4*)(wst + s * TCO * HCH + swz(j * 16 + (lane & 15), c));
+          else
+            bf[j] = lds::fragment<false, TCO>((const char*)(wst + s * TCO * HCH), j * 16, kk, fb);
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -168,9 +202,10 @@ __global__ void __launch_bounds__(HT) conv_halo_kernel(HaloArgs a, int64_t M, Ep
 }
 
 // the tile's image rows and halo pixels, or false when the shape does not qualify
-bool halo_plan(const ConvGeom& g, int* hr, int* halo_px) {
+bool halo_plan(const ConvGeom& g, bool bwd, int* hr, int* halo_px) {
+  const int cin = bwd ? g.k : g.c, cout = bwd ? g.c : g.k;
   if (g.r != 3 || g.s != 3 || g.pad != 1 || g.ho != g.h || g.wo != g.w || g.n <= 0) return false;
-  if (g.c != HCH || g.k % TCO != 0 || g.w > TPX) return false;
+  if (cin != HCH || cout % TCO != 0 || g.w > TPX) return false;
   const int64_t hw = (int64_t)g.h * g.w;
   int rows, ipt;
   if (hw >= TPX) {
@@ -183,41 +218,46 @@ bool halo_plan(const ConvGeom& g, int* hr, int* halo_px) {
   const int px = ipt * (rows + 2) * (g.w + 2);
   if (px > HALO_MAX_PX) return false;
   // (global offsets are 64-bit; this bounds the grid)
-  if ((int64_t)g.n * hw / TPX * (g.k / TCO) > 0x7fffffffLL) return false;
+  if ((int64_t)g.n * hw / TPX * (cout / TCO) > 0x7fffffffLL) return false;
   *hr = rows;
   *halo_px = px;
   return true;
 }
 
 template <class T, class OutT>
-mdnn_status_t halo_launch(const HaloArgs& a, int64_t M, const Epilogue& ep, hipStream_t st) {
-  hipLaunchKernelGGL((conv_halo_kernel<T, OutT>), dim3((unsigned)(M / TPX * a.tiles_n)), dim3(HT), 0, st, a, M,
-                     ep);
+mdnn_status_t halo_launch(const HaloArgs& a, bool bwd, int64_t M, const Epilogue& ep, hipStream_t st) {
+  const dim3 grid((unsigned)(M / TPX * a.tiles_n));
+  if (bwd)
+    hipLaunchKernelGGL((conv_halo_kernel<T, OutT, true>), grid, dim3(HT), 0, st, a, M, ep);
+  else
+    hipLaunchKernelGGL((conv_halo_kernel<T, OutT, false>), grid, dim3(HT), 0, st, a, M, ep);
   return check_launch("conv_halo_kernel");
 }
 
 }  // namespace
 
-mdnn_status_t conv_halo_fwd(const ConvGeom& g, const void* x, const void* w, const Epilogue& ep, mdnn_dtype_t io,
-                            mdnn_dtype_t out, hipStream_t st, bool* done) {
+mdnn_status_t conv_halo(const ConvGeom& g, bool bwd, const void* src, const void* w, const Epilogue& ep,
+                        mdnn_dtype_t io, mdnn_dtype_t out, hipStream_t st, bool* done) {
   *done = false;
   int hr = 0, px = 0;
-  if ((io != MDNN_F16 && io != MDNN_BF16) || !halo_plan(g, &hr, &px)) return MDNN_SUCCESS;
-  if (!aligned(x, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
+  if ((io != MDNN_F16 && io != MDNN_BF16) || !halo_plan(g, bwd, &hr, &px)) return MDNN_SUCCESS;
+  if (!aligned(src, 16) || !aligned(w, 16)) return MDNN_SUCCESS;
   HaloArgs a{};
-  a.x = (const uint16_t*)x;
+  a.x = (const uint16_t*)src;
   a.w = (const uint16_t*)w;
   a.h = g.h;
   a.w_img = g.w;
-  a.cout = g.k;
+  a.cout = bwd ? g.c : g.k;
   a.hr = hr;
   a.halo_px = px;
-  a.tiles_n = g.k / TCO;
+  a.tiles_n = a.cout / TCO;
   const int64_t M = (int64_t)g.n * g.h * g.w;
   if (io == MDNN_F16)
-    MDNN_TRY((out == MDNN_F32 ? halo_launch<F16, F32>(a, M, ep, st) : halo_launch<F16, F16>(a, M, ep, st)));
+    MDNN_TRY((out == MDNN_F32 ? halo_launch<F16, F32>(a, bwd, M, ep, st)
+                              : halo_launch<F16, F16>(a, bwd, M, ep, st)));
   else
-    MDNN_TRY((out == MDNN_F32 ? halo_launch<BF16, F32>(a, M, ep, st) : halo_launch<BF16, BF16>(a, M, ep, st)));
+    MDNN_TRY((out == MDNN_F32 ? halo_launch<BF16, F32>(a, bwd, M, ep, st)
+                              : halo_launch<BF16, BF16>(a, bwd, M, ep, st)));
   *done = true;
   return MDNN_SUCCESS;
 }

@@ -1,16 +1,18 @@
-"""GPU parity of the forward 3x3 halo convolution (64 input channels, the
-input tile and its border staged in LDS) against the oracle's direct
-definition, with backward data of the same layers (the implicit GEMM).
+"""GPU parity of the 3x3 halo convolutions (64 channels in the convolved
+tensor, its tile and border staged in LDS): forward and backward data
+against the oracle's direct definitions.
 
 Shapes cover each way a workgroup's 256 output pixels fall on the image:
 eight rows of a 32-wide image, one whole 16x16 image, four whole 8x8 images,
 and rows of a non-square image; output channels 64 and 128 (one and two
-workgroup columns).  Small integers make every product and partial sum exact
-in fp32, so the fp32 outputs must match the oracle bit for bit (padding
-zeros included); the bias + ReLU and mask epilogues stored in 16 bits are
-checked within one ulp plus the accumulation bound; and the same layer
-through the implicit GEMM's pipelined kernel (forced with the pipelined tile
-code) agrees with the oracle too.
+workgroup columns) in each direction (a shape whose forward pass has 64
+input channels runs its backward data on the implicit GEMM unless c_out is
+64 too, and the other way round).  Small integers make every product and
+partial sum exact in fp32, so the fp32 outputs must match the oracle bit for
+bit (padding zeros included); the bias + ReLU and mask epilogues stored in
+16 bits are checked within one ulp plus the accumulation bound; and the same
+layer through the implicit GEMM's pipelined kernels (forced with the
+pipelined tile code) agrees with the oracle too.
 """
 import numpy as np
 import pytest
@@ -23,10 +25,12 @@ from tests.helpers import accum_bound, dev, host64, lowp_close, norm_max_err
 pytestmark = pytest.mark.gpu
 
 HALO = [  # n, h, w, c_in, c_out
-    (2, 32, 32, 64, 64),
-    (3, 16, 16, 64, 128),
-    (8, 8, 8, 64, 128),
-    (1, 16, 32, 64, 64),
+    (2, 32, 32, 64, 64),    # forward and backward data
+    (3, 16, 16, 64, 128),   # forward
+    (3, 16, 16, 128, 64),   # backward data
+    (8, 8, 8, 64, 128),     # forward
+    (8, 8, 8, 128, 64),     # backward data
+    (1, 16, 32, 64, 64),    # forward and backward data
 ]
 
 
@@ -48,7 +52,7 @@ def test_halo_integer_exact(mdnn, shape, dt):
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
-@pytest.mark.parametrize("shape", [HALO[0], HALO[2]])
+@pytest.mark.parametrize("shape", [HALO[0], HALO[4]])
 def test_halo_bias_relu_and_mask_lowp(mdnn, shape, dt):
     """Forward with bias + ReLU stored in the storage type; backward data with
     the ReLU mask of the layer input, stored in the storage type."""
@@ -73,10 +77,10 @@ def test_halo_bias_relu_and_mask_lowp(mdnn, shape, dt):
 
 @pytest.mark.parametrize("tile", [0, 4])
 def test_halo_and_implicit_gemm_against_oracle(mdnn, tile):
-    """Tile code 0 takes the halo kernel, 4 forces the implicit GEMM's
-    pipelined kernel on the same layer: both within 1e-4 of the oracle."""
+    """Tile code 0 takes the halo kernels, 4 forces the implicit GEMM's
+    pipelined kernels on the same layer: both within 1e-4 of the oracle."""
     import torch
-    n, h, w, ci, co = HALO[1]
+    n, h, w, ci, co = HALO[0]
     x = W.normal((n, h, w, ci), 25, 1, "f16", 1 / np.sqrt(9 * ci))
     wt = W.normal((co, 3, 3, ci), 25, 2, "f16", 1 / np.sqrt(9 * ci))
     dy = W.normal((n, h, w, co), 25, 3, "f16")
