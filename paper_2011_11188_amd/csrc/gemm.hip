@@ -81,11 +81,10 @@ __global__ void __launch_bounds__(1024) reduce_batch_kernel(ReduceBatch b) {
   int s = 0;
   while (s + 1 < b.n && (int64_t)blockIdx.x >= b.first_block[s + 1]) ++s;
   const int64_t blk = (int64_t)blockIdx.x - b.first_block[s];
-  switch (b.opb[s]) {
-    case 16: reduce_wide_block<16>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
-    case 32: reduce_wide_block<32>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
-    default: reduce_wide_block<64>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red); break;
-  }
+  if (b.opb[s] == 16)
+    reduce_wide_block<16>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red);
+  else
+    reduce_wide_block<64>(b.part[s], b.splits[s], b.elems[s], b.out[s], blk, red);
 }
 
 static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream,
@@ -104,7 +103,9 @@ mdnn_status_t reduce_batch_launch(ReduceBatch& b, hipStream_t stream) {
 
 static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, float* out, hipStream_t stream,
                                  ReduceBatch* defer) {
-  const int opb = n <= 16 ? 16 : n <= 32 ? 32 : 64;
+  // up to 1024 outputs: 16 per block, 64 split groups (a 64-column bias sum
+  // over 512 row chunks: 8 partials per thread in 4 blocks, not 32 in one)
+  const int opb = n <= 1024 ? 16 : 64;
   if (defer) {
     if (defer->n == kMaxReduceBatch) MDNN_TRY(reduce_batch_launch(*defer, stream));
     const int s = defer->n++;
@@ -117,13 +118,11 @@ static mdnn_status_t reduce_wide(const float* partial, int splits, int64_t n, fl
     defer->first_block[s + 1] = defer->first_block[s] + ceil_div(n, (int64_t)opb);
     return MDNN_SUCCESS;
   }
+  const dim3 grid((unsigned)ceil_div(n, (int64_t)opb));
   if (opb == 16)
-    hipLaunchKernelGGL(reduce_splits_wide_kernel<16>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
-  else if (opb == 32)
-    hipLaunchKernelGGL(reduce_splits_wide_kernel<32>, dim3(1), dim3(1024), 0, stream, partial, splits, n, out);
+    hipLaunchKernelGGL(reduce_splits_wide_kernel<16>, grid, dim3(1024), 0, stream, partial, splits, n, out);
   else
-    hipLaunchKernelGGL(reduce_splits_wide_kernel<64>, dim3((unsigned)ceil_div(n, 64)), dim3(1024), 0, stream,
-                       partial, splits, n, out);
+    hipLaunchKernelGGL(reduce_splits_wide_kernel<64>, grid, dim3(1024), 0, stream, partial, splits, n, out);
   return check_launch("reduce_splits_wide_kernel");
 }
 

@@ -48,7 +48,7 @@ struct ReduceBatch {
   float* out[kMaxReduceBatch];
   int64_t elems[kMaxReduceBatch];
   int splits[kMaxReduceBatch];
-  int opb[kMaxReduceBatch];  // outputs per block: 16, 32 or 64
+  int opb[kMaxReduceBatch];  // outputs per block: 16 or 64
   int64_t first_block[kMaxReduceBatch + 1];
 };
 mdnn_status_t reduce_batch_launch(ReduceBatch& b, hipStream_t stream);

@@ -1,6 +1,7 @@
 """GPU parity of the 3x3 halo convolutions (64 channels in the convolved
 tensor, its tile and border staged in LDS): forward and backward data
-against the oracle's direct definitions.
+against the oracle's direct definitions, with the filter and bias gradients
+of the same layers (the implicit GEMM).
 
 Shapes cover each way a workgroup's 256 output pixels fall on the image:
 eight rows of a 32-wide image, one whole 16x16 image, four whole 8x8 images,
@@ -31,6 +32,7 @@ HALO = [  # n, h, w, c_in, c_out
     (8, 8, 8, 64, 128),     # forward
     (8, 8, 8, 128, 64),     # backward data
     (1, 16, 32, 64, 64),    # forward and backward data
+    (3, 16, 16, 64, 64),    # forward and backward data
 ]
 
 
@@ -45,10 +47,13 @@ def test_halo_integer_exact(mdnn, shape, dt):
     X, Wt, DY = dev(x, dt), dev(wt, dt), dev(dy, dt)
     y = mdnn.conv2d_fwd(X, Wt, 1, out_dtype=torch.float32)
     dx = mdnn.conv2d_bwd_data(DY, Wt, 1, h, w, out_dtype=torch.float32)
+    dwt, db = mdnn.conv2d_bwd_filter(X, DY, 3, 3, 1)
     torch.cuda.synchronize()
     x64, w64, dy64 = decode(x, dt), decode(wt, dt), decode(dy, dt)
     assert np.array_equal(host64(y), ops.conv2d_fwd(x64, w64, 1))
     assert np.array_equal(host64(dx), ops.conv2d_bwd_data(dy64, w64, 1, h, w))
+    assert np.array_equal(host64(dwt), ops.conv2d_bwd_filter(x64, dy64, 1, 3, 3))
+    assert np.array_equal(host64(db), dy64.sum(axis=(0, 1, 2)))
 
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
