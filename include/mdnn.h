@@ -134,9 +134,10 @@ mdnn_status_t mdnn_gemm_mixed_ws(mdnn_layout_t layout, int64_t M, int64_t N, int
  * the 256x256 / 128x128 direct-to-LDS pipelined kernel wherever its
  * preconditions hold (K % 64 == 0, 16-byte aligned operands with leading
  * dimensions multiple of 8, MN-contiguous extents multiple of 8), the
- * automatic choice elsewhere.  Returns 0, or -1 for an unknown code.  Results
- * do not depend on the kernel except through the fp32 summation order of
- * split-K. */
+ * automatic choice elsewhere (3x3 convolutions then run their implicit-GEMM
+ * kernels instead of the LDS-halo kernels).  Returns 0, or -1 for an unknown
+ * code.  Results do not depend on the kernel except through the fp32
+ * summation order of split-K. */
 int mdnn_set_gemm_tile(int code);
 
 /* ---------------------------------------------------------------------------
