@@ -364,3 +364,23 @@ def test_conv_bwd_filter_deterministic(mdnn):
     torch.cuda.synchronize()
     assert torch.equal(a, b)
     del wt
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_conv_bwd_filter_batched_sums_bitwise(mdnn, layer):
+    """With db the weight and bias sums' second passes share one launch
+    (several reductions per grid); without db the weight sums run alone: the
+    same sums in the same order, so dw is bitwise the same, and db is
+    deterministic too."""
+    import torch
+    sh = W.RESNET_LAYERS[layer]
+    x, wt, dy = W.conv_operands(sh)
+    X, DY = dev(x, "f16"), dev(dy, "f16")
+    a, db1 = mdnn.conv2d_bwd_filter(X, DY, 3, 3, 1)
+    b, _ = mdnn.conv2d_bwd_filter(X, DY, 3, 3, 1, with_db=False)
+    c, db2 = mdnn.conv2d_bwd_filter(X, DY, 3, 3, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    assert torch.equal(a.view(torch.int32), c.view(torch.int32))
+    assert torch.equal(db1.view(torch.int32), db2.view(torch.int32))
+    del wt
